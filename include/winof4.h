@@ -1,0 +1,235 @@
+/*
+ * libwinof4 -- integer Winograd F(4x4, 3x3) convolution with tap-wise
+ * power-of-two quantization on AMD Instinct MI355X (gfx950).
+ *
+ * Method: arxiv 2209.12982, Sec. III.  For one output channel and one 4x4
+ * output tile,
+ *     Y = A^T ( S_BG (.) sum_ci q(B^T d B (/) S_B) (.) q(G f G^T (/) S_G) ) A
+ * with per-tap (6x6) power-of-two scales S_B = 2^e_B, S_G = 2^e_G, S_BG =
+ * S_B (.) S_G, and q the int8 quantizer of Eq. quant.  The transform matrices
+ * are the F(4x4,3x3) ones printed in Sec. II.  Products are accumulated over
+ * input channels in int32; the tap scale is applied once, before the back
+ * transform (Sec. III, rearranged scheme).
+ *
+ * Conventions shared by every entry point
+ *   - 3x3 kernel, stride 1, zero padding 1, dilation 1, one group: the only
+ *     layers the paper sends to Winograd (Sec. III, last paragraph).  Other
+ *     geometries are not expressible in this API.
+ *   - Tap t = 6*a + b addresses row a, column b of the 6x6 Winograd tile.
+ *   - Rounding R(v) = floor(v + 1/2) (round half up) for every rounding; the
+ *     int8 quantizer is clamp(R(v / 2^e), -128, 127).  The paper does not
+ *     state a tie-break; this is the reading the library implements.
+ *   - Input tiles are 6x6 windows at stride 4 over the input padded by one
+ *     zero pixel; ceil(H/4) x ceil(W/4) tiles are computed and output pixels
+ *     beyond H or W are discarded (zero padding to a multiple of 4, Sec. V).
+ *   - Activations are int8, NCHW [N][C][H][W] or NHWC [N][H][W][C], dense.
+ *   - "device" pointers are HIP device memory of the current device; "host"
+ *     pointers are ordinary CPU memory, read or written during the call only.
+ *   - Calls on a stream are asynchronous unless stated; nothing is retained
+ *     from a host argument after the call returns.
+ *   - Every function validates all arguments before launching anything and
+ *     reports failure through its return value; nothing aborts or throws.
+ */
+#ifndef WINOF4_H
+#define WINOF4_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum wino_status {
+    WINO_OK = 0,
+    WINO_EINVAL = -1,        /* null pointer, negative size, value out of range   */
+    WINO_EUNSUPPORTED = -2,  /* a size beyond the library's limits                */
+    WINO_ERANGE = -3,        /* plan tables that no integer epilogue can hold     */
+    WINO_ENOMEM = -4,        /* device or host allocation failed                  */
+    WINO_EWORKSPACE = -5,    /* workspace pointer null or smaller than required   */
+    WINO_EHIP = -6           /* a HIP runtime call or kernel launch failed        */
+} wino_status;
+
+typedef enum wino_layout { WINO_NCHW = 0, WINO_NHWC = 1 } wino_layout;
+
+/* SPLIT: input transform to a tap-major int8 workspace, then the tap GEMM
+ * with the output transform fused into its epilogue (two launches).
+ * FUSED: one launch; the input transform runs in the GEMM prologue and no
+ * workspace is used.                                                        */
+typedef enum wino_variant { WINO_SPLIT = 0, WINO_FUSED = 1 } wino_variant;
+
+typedef struct wino_f4_plan_s* wino_f4_plan_t;   /* opaque, immutable after creation */
+
+/*
+ * wino_f4_plan -- the offline step: weight transform U = G f G^T (Eq.
+ * winograd), tap-wise power-of-two weight quantization (Sec. III-B,
+ * straight-forward power-of-two rule), and the per-tap alignment of
+ * S_BG (Sec. III, rearranged scheme), uploaded for stationary reuse by every
+ * later convolution (the "weights transformed once, kept stationary" dataflow
+ * of Sec. IV-B2).
+ *
+ *   out        receives the new plan (host pointer to a handle).
+ *   w_oihw     host fp32 [cout][cin][3][3].  U is computed exactly (no
+ *              floating-point rounding), then Uq = clamp(R(U / 2^e_G)).
+ *   cin, cout  channel counts, 1 .. 65536 each.
+ *   in_exp     host int8 [36]: e_B[t] in [0, 15], the input tap exponents
+ *              (S_B = 2^e_B); see wino_f4_calibrate_input.
+ *   w_exp      host int8 [36] explicit e_G[t] in [-126, 126], or NULL for
+ *              max-abs calibration: e_G[t] = smallest e with
+ *              max_{co,ci} |U_t| <= 128 * 2^e (0 for an all-zero tap).
+ *   bias       host int32 [cout] in units of 2^e_o (see below), or NULL for 0.
+ *   out_shift  output requantization shift in [0, 62]:
+ *              out = clamp(R((Y + bias) / 2^out_shift), -128, 127).
+ *   relu       0 or 1: if 1, out = max(out, 0).
+ *   stream     stream for the upload; the call returns after the upload has
+ *              completed, so the plan is usable on any stream afterwards.
+ *
+ * Exponent bookkeeping: e[t] = e_B[t] + e_G[t], e_o = min_t e[t], and
+ * sh[t] = e[t] - e_o.  The tap GEMM result of tap t is multiplied by 2^sh[t]
+ * exactly, so Y is an exact integer and the real-valued output is Y * 2^e_o.
+ * The plan bounds every intermediate of the output transform; it selects a
+ * 32-bit epilogue when the bound is below 2^31, a 64-bit one when below 2^62,
+ * and returns WINO_ERANGE otherwise.
+ * Errors: WINO_EINVAL (null out/w_oihw/in_exp, values out of range),
+ * WINO_ERANGE, WINO_ENOMEM, WINO_EHIP.  On error *out is set to NULL.
+ */
+wino_status wino_f4_plan(wino_f4_plan_t* out, const float* w_oihw, int32_t cin, int32_t cout,
+                         const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                         int32_t out_shift, int32_t relu, hipStream_t stream);
+
+/*
+ * wino_f4_plan_tables -- the host arithmetic of wino_f4_plan alone, with no
+ * device work: for the same arguments it writes e_g[36], sh[36], e_o,
+ * epilogue_bits and uq [36][cin][cout] (host pointers, any may be NULL).
+ * Lets a plan be inspected on a machine without a GPU.  Errors as for
+ * wino_f4_plan except WINO_EHIP.
+ */
+wino_status wino_f4_plan_tables(const float* w_oihw, int32_t cin, int32_t cout, const int8_t* in_exp,
+                                const int8_t* w_exp, const int32_t* bias, int32_t out_shift, int8_t* e_g,
+                                int8_t* sh, int32_t* e_o, int32_t* epilogue_bits, int8_t* uq);
+
+/* Releases a plan and its device memory.  NULL is ignored.  The caller must
+ * ensure no convolution using the plan is still running. */
+void wino_f4_plan_destroy(wino_f4_plan_t plan);
+
+/*
+ * wino_f4_plan_info -- the plan's tables, for inspection and parity tests.
+ * Any output pointer may be NULL.  e_g, sh: host int8 [36]; e_o: host int32;
+ * epilogue_bits: 32 or 64; uq: host int8 [36][cin][cout] (tap-major,
+ * Uq[t][ci][co]); cin/cout: the plan's channel counts.
+ */
+wino_status wino_f4_plan_info(wino_f4_plan_t plan, int8_t* e_g, int8_t* sh, int32_t* e_o,
+                              int32_t* epilogue_bits, int8_t* uq, int32_t* cin, int32_t* cout);
+
+/*
+ * Workspace bytes that wino_f4_conv_int8 needs for this plan, batch and image
+ * size (SPLIT: the tap-major int8 Winograd-domain input, 36 x tiles x Cin
+ * rounded up to the kernel's blocking; FUSED: 0).  Returns 0 for an invalid
+ * plan or negative sizes.
+ */
+size_t wino_f4_workspace_bytes(wino_f4_plan_t plan, int32_t n, int32_t h, int32_t w,
+                               wino_variant variant);
+
+/*
+ * wino_f4_conv_int8 -- the online path (Sec. III scheme; operator dataflow
+ * of Sec. IV-B2): input transform B^T d B of every 6x6 tile, tap-wise
+ * requantization to int8 with 2^e_B[t], 36 int8 tap GEMMs with int32
+ * accumulation, alignment by 2^sh[t], output transform A^T M A, bias,
+ * requantization and optional ReLU.  Bit-exact integer arithmetic.
+ *
+ *   x          device int8 input, layout `layout`, [n][cin][h][w] or
+ *              [n][h][w][cin]; not modified.
+ *   y          device int8 output, same layout with cout channels; must not
+ *              overlap x or the workspace.
+ *   n, h, w    batch and image size, >= 0 (a zero size is a no-op), with
+ *              n * ceil(h/4) * ceil(w/4) < 2^26 and each of h, w <= 65536.
+ *   workspace  device memory of at least wino_f4_workspace_bytes() bytes
+ *              (ignored for FUSED; may be NULL then); contents are scratch.
+ *   stream     all work is enqueued on this stream; no host synchronization.
+ * A plan may be used concurrently on several streams with separate
+ * workspaces.  Errors: WINO_EINVAL, WINO_EUNSUPPORTED, WINO_EWORKSPACE,
+ * WINO_EHIP (launch failure reported by hipGetLastError).
+ */
+wino_status wino_f4_conv_int8(wino_f4_plan_t plan, const int8_t* x, int8_t* y, int32_t n,
+                              int32_t h, int32_t w, wino_layout layout, wino_variant variant,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * wino_f4_calibrate_input -- max-abs calibration of the input tap scales
+ * (Sec. III: x_max calibrated from observed maxima; power-of-two rule of
+ * Sec. III-B).  Computes absmax[t] = max over all tiles and channels of
+ * |(B^T d B)_t| on the GPU and e_B[t] = min(15, max(0, smallest e with
+ * absmax[t] <= 128 * 2^e)).  Synchronizes `stream` before returning.
+ *   x: device int8 input as for wino_f4_conv_int8.
+ *   absmax: host int32 [36] or NULL;  e_b: host int8 [36] or NULL.
+ * Allocates and frees a small device buffer (an offline step).
+ */
+wino_status wino_f4_calibrate_input(const int8_t* x, int32_t n, int32_t cin, int32_t h,
+                                    int32_t w, wino_layout layout, int32_t* absmax,
+                                    int8_t* e_b, hipStream_t stream);
+
+/*
+ * wino_f4_calibrate_output -- max-abs calibration of the output shift: runs
+ * the online path up to z = Y + bias and returns zmax = max |z| over all
+ * in-image outputs and out_shift = min(62, max(0, smallest s with
+ * zmax <= 128 * 2^s)).  The plan's own out_shift and relu are ignored.
+ * Arguments as for wino_f4_conv_int8 (SPLIT workspace); zmax, out_shift are
+ * host pointers (either may be NULL).  Synchronizes `stream`.
+ */
+wino_status wino_f4_calibrate_output(wino_f4_plan_t plan, const int8_t* x, int32_t n, int32_t h,
+                                     int32_t w, wino_layout layout, void* workspace,
+                                     size_t workspace_bytes, int64_t* zmax, int32_t* out_shift,
+                                     hipStream_t stream);
+
+/*
+ * Stage exports for parity tests (not on the hot path).
+ * wino_f4_debug_input_transform: the int8 tap-major Winograd-domain input
+ *   Vq[t][tile][ci] (tile = (img*ceil(h/4) + ty)*ceil(w/4) + tx), written to
+ *   device int8 `vq` of 36 * tiles * cin bytes.
+ * wino_f4_debug_tap_gemm: the raw int32 tap GEMM results M[t][tile][co]
+ *   (before alignment), written to device int32 `m` of 36 * tiles * cout
+ *   elements.
+ * Both need the SPLIT workspace and run on `stream` without synchronizing.
+ */
+wino_status wino_f4_debug_input_transform(wino_f4_plan_t plan, const int8_t* x, int32_t n,
+                                          int32_t h, int32_t w, wino_layout layout, int8_t* vq,
+                                          void* workspace, size_t workspace_bytes,
+                                          hipStream_t stream);
+wino_status wino_f4_debug_tap_gemm(wino_f4_plan_t plan, const int8_t* x, int32_t n, int32_t h,
+                                   int32_t w, wino_layout layout, int32_t* m, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * direct_conv_quantize_weights -- spatial int8 weights for the direct
+ * baseline: one power-of-two scale per layer, e = smallest e with
+ * max |f| <= 128 * 2^e, w = clamp(R(f / 2^e), -128, 127) (Eq. quant with the
+ * power-of-two rule).  w_oihw: host fp32 [cout][cin][3][3]; w_ohwi: host int8
+ * [cout][3][3][cin] (output); e: host int32 (output).  Exact arithmetic.
+ */
+wino_status direct_conv_quantize_weights(const float* w_oihw, int32_t cout, int32_t cin,
+                                         int8_t* w_ohwi, int32_t* e);
+
+/*
+ * direct_conv_int8 -- the standard (im2col-style) 3x3 convolution the paper
+ * compares against (Sec. IV-A, im2col engine; Sec. V), as an implicit GEMM
+ * on int8 MFMA: z = sum x * w + bias (exact int32), out = clamp(R(z /
+ * 2^out_shift), -128, 127), optional ReLU.  Same geometry and layouts as
+ * wino_f4_conv_int8.
+ *   w_ohwi  device int8 [cout][3][3][cin];  bias: device int32 [cout] or NULL.
+ *   1 <= cin <= 8192 (keeps the int32 accumulator exact), 1 <= cout <= 65536,
+ *   out_shift in [0, 31], relu 0|1.  Asynchronous on `stream`.
+ */
+wino_status direct_conv_int8(const int8_t* x, const int8_t* w_ohwi, const int32_t* bias, int8_t* y,
+                             int32_t n, int32_t cin, int32_t cout, int32_t h, int32_t w,
+                             wino_layout layout, int32_t out_shift, int32_t relu,
+                             hipStream_t stream);
+
+/* Static description of a status code; never NULL. */
+const char* wino_strerror(wino_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WINOF4_H */

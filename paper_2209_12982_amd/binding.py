@@ -1,0 +1,253 @@
+"""ctypes binding of libwinof4 (include/winof4.h).  Argument marshalling only:
+device buffers are torch tensors (their ``data_ptr()``), host tables are numpy
+arrays, and the stream defaults to torch's current stream.  Every step of the
+convolution runs in the library's HIP kernels."""
+import ctypes
+import os
+
+import numpy as np
+
+TAPS = 36
+NCHW, NHWC = 0, 1
+SPLIT, FUSED = 0, 1
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB = None
+
+EXPORTS = [
+    "wino_f4_plan", "wino_f4_plan_tables", "wino_f4_plan_destroy", "wino_f4_plan_info", "wino_f4_workspace_bytes",
+    "wino_f4_conv_int8", "wino_f4_calibrate_input", "wino_f4_calibrate_output",
+    "wino_f4_debug_input_transform", "wino_f4_debug_tap_gemm",
+    "direct_conv_quantize_weights", "direct_conv_int8", "wino_strerror",
+]
+
+
+class LibraryNotBuilt(RuntimeError):
+    pass
+
+
+class WinoError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__(f"{where}: {wino_strerror(status)} ({status})")
+
+
+def library_path():
+    return os.path.join(_HERE, "libwinof4.so")
+
+
+def load_library():
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = library_path()
+    if not os.path.exists(path):
+        raise LibraryNotBuilt(f"{path} is missing; run __graft_entry__.build() or "
+                              "python paper_2209_12982_amd/build.py")
+    lib = ctypes.CDLL(path)
+    P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    sig = {
+        "wino_f4_plan": (I32, [P, P, I32, I32, P, P, P, I32, I32, P]),
+        "wino_f4_plan_tables": (I32, [P, I32, I32, P, P, P, I32, P, P, P, P, P]),
+        "wino_f4_plan_destroy": (None, [P]),
+        "wino_f4_plan_info": (I32, [P, P, P, P, P, P, P, P]),
+        "wino_f4_workspace_bytes": (SZ, [P, I32, I32, I32, I32]),
+        "wino_f4_conv_int8": (I32, [P, P, P, I32, I32, I32, I32, I32, P, SZ, P]),
+        "wino_f4_calibrate_input": (I32, [P, I32, I32, I32, I32, I32, P, P, P]),
+        "wino_f4_calibrate_output": (I32, [P, P, I32, I32, I32, I32, P, SZ, P, P, P]),
+        "wino_f4_debug_input_transform": (I32, [P, P, I32, I32, I32, I32, P, P, SZ, P]),
+        "wino_f4_debug_tap_gemm": (I32, [P, P, I32, I32, I32, I32, P, P, SZ, P]),
+        "direct_conv_quantize_weights": (I32, [P, I32, I32, P, P]),
+        "direct_conv_int8": (I32, [P, P, P, P, I32, I32, I32, I32, I32, I32, I32, I32, P]),
+        "wino_strerror": (ctypes.c_char_p, [I32]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _LIB = lib
+    return lib
+
+
+def exported_symbols():
+    """Names from EXPORTS that the built library resolves."""
+    lib = load_library()
+    return [n for n in EXPORTS if hasattr(lib, n)]
+
+
+def wino_strerror(status):
+    try:
+        return load_library().wino_strerror(int(status)).decode()
+    except LibraryNotBuilt:
+        return f"status {status}"
+
+
+def _check(status, where):
+    if status != 0:
+        raise WinoError(status, where)
+
+
+def _ptr(t):
+    """Device pointer of a torch tensor (or None)."""
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _host(a, dtype, n=None):
+    a = np.ascontiguousarray(np.asarray(a, dtype=dtype))
+    if n is not None and a.size != n:
+        raise ValueError(f"expected {n} values, got {a.size}")
+    return a
+
+
+class WinoF4Plan:
+    """Owns a wino_f4_plan_t; destroyed with the object or by close()."""
+
+    def __init__(self, handle, cin, cout):
+        self.handle = handle
+        self.cin = cin
+        self.cout = cout
+
+    def close(self):
+        if self.handle:
+            load_library().wino_f4_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def wino_f4_plan(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0, relu=False, stream=None):
+    lib = load_library()
+    w = _host(w_oihw, np.float32)
+    cout, cin = w.shape[:2]
+    eb = _host(in_exp, np.int8, TAPS)
+    eg = None if w_exp is None else _host(w_exp, np.int8, TAPS)
+    b = None if bias is None else _host(bias, np.int32, cout)
+    h = ctypes.c_void_p()
+    st = lib.wino_f4_plan(ctypes.byref(h), w.ctypes.data, cin, cout, eb.ctypes.data,
+                          None if eg is None else eg.ctypes.data,
+                          None if b is None else b.ctypes.data, int(out_shift), int(bool(relu)),
+                          _stream(stream))
+    _check(st, "wino_f4_plan")
+    return WinoF4Plan(h, cin, cout)
+
+
+def wino_f4_plan_tables(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0):
+    """Host-only plan arithmetic (no GPU): dict with e_g, sh, e_o,
+    epilogue_bits and uq [36][cin][cout]."""
+    lib = load_library()
+    w = _host(w_oihw, np.float32)
+    cout, cin = w.shape[:2]
+    eb = _host(in_exp, np.int8, TAPS)
+    eg_in = None if w_exp is None else _host(w_exp, np.int8, TAPS)
+    b = None if bias is None else _host(bias, np.int32, cout)
+    eg = np.zeros(TAPS, np.int8)
+    sh = np.zeros(TAPS, np.int8)
+    eo = ctypes.c_int32()
+    bits = ctypes.c_int32()
+    uq = np.zeros((TAPS, cin, cout), np.int8)
+    st = lib.wino_f4_plan_tables(w.ctypes.data, cin, cout, eb.ctypes.data,
+                                 None if eg_in is None else eg_in.ctypes.data,
+                                 None if b is None else b.ctypes.data, int(out_shift),
+                                 eg.ctypes.data, sh.ctypes.data, ctypes.byref(eo), ctypes.byref(bits),
+                                 uq.ctypes.data)
+    _check(st, "wino_f4_plan_tables")
+    return dict(e_g=eg.astype(int).tolist(), sh=sh.astype(int).tolist(), e_o=eo.value,
+                epilogue_bits=bits.value, uq=uq)
+
+
+def wino_f4_plan_info(plan, with_uq=False):
+    lib = load_library()
+    eg = np.zeros(TAPS, np.int8)
+    sh = np.zeros(TAPS, np.int8)
+    eo = ctypes.c_int32()
+    bits = ctypes.c_int32()
+    uq = np.zeros((TAPS, plan.cin, plan.cout), np.int8) if with_uq else None
+    st = lib.wino_f4_plan_info(plan.handle, eg.ctypes.data, sh.ctypes.data, ctypes.byref(eo),
+                               ctypes.byref(bits), None if uq is None else uq.ctypes.data, None, None)
+    _check(st, "wino_f4_plan_info")
+    return dict(e_g=eg.astype(int).tolist(), sh=sh.astype(int).tolist(), e_o=eo.value,
+                epilogue_bits=bits.value, uq=uq)
+
+
+def wino_f4_workspace_bytes(plan, n, h, w, variant=SPLIT):
+    return int(load_library().wino_f4_workspace_bytes(plan.handle, n, h, w, variant))
+
+
+def wino_f4_conv_int8(plan, x, y, n, h, w, layout=NCHW, variant=SPLIT, workspace=None, stream=None):
+    lib = load_library()
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib.wino_f4_conv_int8(plan.handle, _ptr(x), _ptr(y), n, h, w, layout, variant,
+                               _ptr(workspace), ws_bytes, _stream(stream))
+    _check(st, "wino_f4_conv_int8")
+
+
+def wino_f4_calibrate_input(x, n, cin, h, w, layout=NCHW, stream=None):
+    lib = load_library()
+    amax = np.zeros(TAPS, np.int32)
+    eb = np.zeros(TAPS, np.int8)
+    st = lib.wino_f4_calibrate_input(_ptr(x), n, cin, h, w, layout, amax.ctypes.data, eb.ctypes.data,
+                                     _stream(stream))
+    _check(st, "wino_f4_calibrate_input")
+    return eb.astype(int).tolist(), amax.astype(int).tolist()
+
+
+def wino_f4_calibrate_output(plan, x, n, h, w, layout=NCHW, workspace=None, stream=None):
+    lib = load_library()
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    zmax = ctypes.c_int64()
+    shift = ctypes.c_int32()
+    st = lib.wino_f4_calibrate_output(plan.handle, _ptr(x), n, h, w, layout, _ptr(workspace), ws_bytes,
+                                      ctypes.byref(zmax), ctypes.byref(shift), _stream(stream))
+    _check(st, "wino_f4_calibrate_output")
+    return shift.value, zmax.value
+
+
+def wino_f4_debug_input_transform(plan, x, n, h, w, layout, vq, workspace, stream=None):
+    lib = load_library()
+    ws_bytes = workspace.numel() * workspace.element_size()
+    st = lib.wino_f4_debug_input_transform(plan.handle, _ptr(x), n, h, w, layout, _ptr(vq), _ptr(workspace),
+                                           ws_bytes, _stream(stream))
+    _check(st, "wino_f4_debug_input_transform")
+
+
+def wino_f4_debug_tap_gemm(plan, x, n, h, w, layout, m, workspace, stream=None):
+    lib = load_library()
+    ws_bytes = workspace.numel() * workspace.element_size()
+    st = lib.wino_f4_debug_tap_gemm(plan.handle, _ptr(x), n, h, w, layout, _ptr(m), _ptr(workspace),
+                                    ws_bytes, _stream(stream))
+    _check(st, "wino_f4_debug_tap_gemm")
+
+
+def direct_conv_quantize_weights(w_oihw):
+    """Returns (int8 weights [cout][3][3][cin], exponent e)."""
+    lib = load_library()
+    w = _host(w_oihw, np.float32)
+    cout, cin = w.shape[:2]
+    out = np.zeros((cout, 3, 3, cin), np.int8)
+    e = ctypes.c_int32()
+    _check(lib.direct_conv_quantize_weights(w.ctypes.data, cout, cin, out.ctypes.data, ctypes.byref(e)),
+           "direct_conv_quantize_weights")
+    return out, e.value
+
+
+def direct_conv_int8(x, w_ohwi, bias, y, n, cin, cout, h, w, layout=NCHW, out_shift=0, relu=False,
+                     stream=None):
+    lib = load_library()
+    st = lib.direct_conv_int8(_ptr(x), _ptr(w_ohwi), _ptr(bias), _ptr(y), n, cin, cout, h, w, layout,
+                              int(out_shift), int(bool(relu)), _stream(stream))
+    _check(st, "direct_conv_int8")

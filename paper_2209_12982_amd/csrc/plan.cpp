@@ -1,0 +1,383 @@
+// Offline plan: exact weight transform, tap-wise power-of-two quantization
+// and the alignment / epilogue-width decisions (Sec. III, Sec. III-B).
+//
+// U = G f G^T with G = G24 / 24 (G24 integral, Sec. II).  For one tap (a, b)
+// 576 * U = sum_{i,j} G24[a][i] G24[b][j] f[i][j]; every term is an integer
+// of magnitude <= 576 times an fp32 value, hence exact in double.  The sum of
+// the nine terms is kept exact as a non-overlapping floating-point expansion
+// (Shewchuk, "Adaptive Precision Floating-Point Arithmetic and Fast Robust
+// Geometric Predicates", 1997: TwoSum and GROW-EXPANSION), which decides
+// every comparison against a power-of-two range or a rounding threshold
+// without error.  A double approximation of each sum drives the search; the
+// exact expansion is consulted only near a decision boundary.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <limits>
+#include <new>
+#include "winof4_internal.h"
+
+using namespace winof4;
+
+namespace {
+
+const int G24[6][3] = {{6, 0, 0}, {-4, -4, -4}, {-4, 4, -4}, {1, 2, 4}, {1, -2, 4}, {0, 0, 24}};
+const int AT[4][6] = {{1, 1, 1, 1, 1, 0}, {0, 1, -1, 2, -2, 0}, {0, 1, 1, 4, 4, 0}, {0, 1, -1, 8, -8, 1}};
+
+// Knuth's TwoSum: s + e == a + b exactly, s = fl(a + b).
+inline void two_sum(double a, double b, double& s, double& e) {
+    s = a + b;
+    double bv = s - a;
+    double av = s - bv;
+    e = (a - av) + (b - bv);
+}
+
+// Exact sum of n doubles as a non-overlapping expansion ordered by
+// increasing magnitude (zero components dropped).  Returns its length.
+int exact_sum(const double* x, int n, double* out) {
+    int len = 0;
+    double tmp[16];
+    for (int k = 0; k < n; ++k) {
+        double q = x[k];
+        int m = 0;
+        for (int i = 0; i < len; ++i) {
+            double s, e;
+            two_sum(q, out[i], s, e);
+            if (e != 0.0) tmp[m++] = e;
+            q = s;
+        }
+        if (q != 0.0) tmp[m++] = q;
+        std::memcpy(out, tmp, sizeof(double) * m);
+        len = m;
+    }
+    return len;
+}
+
+// Sign of (sum of terms[0..8]) - thr, exactly.
+int exact_sign_minus(const double* terms, double thr) {
+    double x[10], ex[16];
+    std::memcpy(x, terms, sizeof(double) * 9);
+    x[9] = -thr;
+    int len = exact_sum(x, 10, ex);
+    if (len == 0) return 0;
+    return ex[len - 1] > 0 ? 1 : -1;   // the largest component carries the sign
+}
+
+// The nine exact terms of 576 * U[a][b] for one 3x3 kernel.
+void tap_terms(const float* f9, int a, int b, double* terms) {
+    int k = 0;
+    for (int i = 0; i < 3; ++i)
+        for (int j = 0; j < 3; ++j)
+            terms[k++] = (double)(G24[a][i] * G24[b][j]) * (double)f9[i * 3 + j];
+}
+
+// Smallest integer e with |S| <= 73728 * 2^e (73728 = 128 * 576) over a set
+// of sums, decided exactly.  `approx` holds the double approximation of each
+// sum; `terms_of(k, t9)` regenerates the exact terms of sum k.
+template <class TermsOf>
+int exact_cexp_of_max(const std::vector<double>& approx, TermsOf terms_of) {
+    double amax = 0.0;
+    for (double v : approx) amax = std::max(amax, std::fabs(v));
+    if (amax == 0.0) {
+        // approximations are exact zeros only for exact-zero sums (a non-zero
+        // expansion never rounds to zero), so the maximum is 0.
+        return 0;
+    }
+    int e;
+    std::frexp(amax / 73728.0, &e);     // 2^(e-1) <= amax/73728 < 2^e
+    e = e - 1;
+    if (std::ldexp(73728.0, e) < amax) e += 1;
+    const double rel = 1e-9;
+    double t9[9];
+    for (int iter = 0; iter < 8; ++iter) {
+        bool changed = false;
+        // (1) every |S| <= 73728 * 2^e ?
+        double thr = std::ldexp(73728.0, e);
+        for (size_t k = 0; k < approx.size() && !changed; ++k) {
+            if (std::fabs(approx[k]) < thr * (1 - rel)) continue;
+            terms_of(k, t9);
+            if (exact_sign_minus(t9, thr) > 0 || exact_sign_minus(t9, -thr) < 0) {
+                e += 1;
+                changed = true;
+            }
+        }
+        if (changed) continue;
+        // (2) some |S| > 73728 * 2^(e-1) ?
+        double lo = std::ldexp(73728.0, e - 1);
+        bool found = false;
+        for (size_t k = 0; k < approx.size() && !found; ++k) {
+            double v = std::fabs(approx[k]);
+            if (v > lo * (1 + rel)) { found = true; break; }
+            if (v < lo * (1 - rel)) continue;
+            terms_of(k, t9);
+            if (exact_sign_minus(t9, lo) > 0 || exact_sign_minus(t9, -lo) < 0) found = true;
+        }
+        if (!found) { e -= 1; continue; }
+        return e;
+    }
+    return e;
+}
+
+// clamp(R(S / (576 * 2^e)), -128, 127) for the exact sum S of `t9`.
+int8_t exact_quantize(const double* t9, double approx, int e) {
+    double scale = std::ldexp(576.0, e);
+    double u = approx / scale;
+    if (!(u < 200.0)) return 127;       // also catches +inf
+    if (!(u > -200.0)) return -128;
+    double q = std::floor(u + 0.5);
+    for (int guard = 0; guard < 4; ++guard) {
+        // need (q - 1/2) * scale <= S < (q + 1/2) * scale
+        if (exact_sign_minus(t9, (q - 0.5) * scale) < 0) { q -= 1; continue; }
+        if (exact_sign_minus(t9, (q + 0.5) * scale) >= 0) { q += 1; continue; }
+        break;
+    }
+    if (q > 127) q = 127;
+    if (q < -128) q = -128;
+    return (int8_t)q;
+}
+
+}  // namespace
+
+// Host part of the plan: validates the arguments and fills every table of
+// `p` (cin, cout, paddings, e_b, e_g, sh, e_o, epi_bits, uq_host, bias_host).
+static wino_status compute_tables(wino_f4_plan_s* p, const float* w_oihw, int32_t cin, int32_t cout,
+                                  const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                                  int32_t out_shift, int32_t relu) {
+    if (!w_oihw || !in_exp) return WINO_EINVAL;
+    if (cin < 1 || cout < 1) return WINO_EINVAL;
+    if (cin > 65536 || cout > 65536) return WINO_EUNSUPPORTED;
+    if (out_shift < 0 || out_shift > 62 || (relu != 0 && relu != 1)) return WINO_EINVAL;
+    for (int t = 0; t < kTaps; ++t) {
+        if (in_exp[t] < 0 || in_exp[t] > 15) return WINO_EINVAL;
+        if (w_exp && (w_exp[t] < -126 || w_exp[t] > 126)) return WINO_EINVAL;
+    }
+    for (int64_t i = 0; i < (int64_t)cout * cin * 9; ++i)
+        if (!std::isfinite(w_oihw[i])) return WINO_EINVAL;
+
+    p->cin = cin;
+    p->cout = cout;
+    p->cin_pad = (int32_t)round_up(cin, kKStep);
+    p->cout_pad = (int32_t)round_up(cout, kCoutPad);
+    p->out_shift = out_shift;
+    p->relu = relu;
+
+    const int64_t nblk = (int64_t)cout * cin;
+    // double approximations of 576 * U for every (block, tap)
+    std::vector<double> approx;
+    try {
+        approx.resize(nblk * kTaps);
+        p->uq_host.assign((size_t)kTaps * cin * cout, 0);
+        p->bias_host.assign(cout, 0);
+    } catch (...) {
+        return WINO_ENOMEM;
+    }
+    double t9[9], ex[16];
+    for (int64_t k = 0; k < nblk; ++k) {
+        const float* f9 = w_oihw + k * 9;
+        for (int t = 0; t < kTaps; ++t) {
+            tap_terms(f9, t / 6, t % 6, t9);
+            int len = exact_sum(t9, 9, ex);
+            double s = 0.0;
+            for (int i = 0; i < len; ++i) s += ex[i];   // small to large
+            approx[k * kTaps + t] = s;
+        }
+    }
+    // e_G
+    std::vector<double> col(nblk);
+    for (int t = 0; t < kTaps; ++t) {
+        if (w_exp) {
+            p->e_g[t] = w_exp[t];
+            continue;
+        }
+        for (int64_t k = 0; k < nblk; ++k) col[k] = approx[k * kTaps + t];
+        int e = exact_cexp_of_max(col, [&](size_t kk, double* tt) {
+            tap_terms(w_oihw + kk * 9, t / 6, t % 6, tt);
+        });
+        if (e < -126 || e > 126) return WINO_ERANGE;
+        p->e_g[t] = (int8_t)e;
+    }
+    // Uq[t][ci][co]
+    for (int64_t k = 0; k < nblk; ++k) {
+        int co = (int)(k / cin), ci = (int)(k % cin);
+        for (int t = 0; t < kTaps; ++t) {
+            tap_terms(w_oihw + k * 9, t / 6, t % 6, t9);
+            p->uq_host[((size_t)t * cin + ci) * cout + co] =
+                exact_quantize(t9, approx[k * kTaps + t], p->e_g[t]);
+        }
+    }
+    // exponents and alignment
+    int e_o = 1 << 20;
+    for (int t = 0; t < kTaps; ++t) {
+        p->e_b[t] = in_exp[t];
+        e_o = std::min(e_o, (int)in_exp[t] + (int)p->e_g[t]);
+    }
+    p->e_o = e_o;
+    for (int t = 0; t < kTaps; ++t) {
+        int s = (int)in_exp[t] + (int)p->e_g[t] - e_o;
+        if (s > 62) return WINO_ERANGE;
+        p->sh[t] = (int8_t)s;
+    }
+    // Epilogue bound: max over (co, i, j) of
+    //   sum_t |A^T[i][a] A^T[j][b]| 2^sh[t] 128 sum_ci |Uq[t][ci][co]|
+    // plus max|bias| plus the rounding constant.  Every partial sum of the
+    // separable output transform is a sub-sum of such a term set, so this
+    // bounds all of them.
+    int64_t maxbias = 0;
+    for (int co = 0; co < cout; ++co) {
+        p->bias_host[co] = bias ? bias[co] : 0;
+        maxbias = std::max<int64_t>(maxbias, std::llabs((int64_t)p->bias_host[co]));
+    }
+    unsigned __int128 worst = 0;
+    std::vector<int64_t> colsum(kTaps);
+    for (int co = 0; co < cout; ++co) {
+        for (int t = 0; t < kTaps; ++t) {
+            int64_t s = 0;
+            for (int ci = 0; ci < cin; ++ci) s += std::abs((int)p->uq_host[((size_t)t * cin + ci) * cout + co]);
+            colsum[t] = s;
+        }
+        for (int i = 0; i < 4; ++i)
+            for (int j = 0; j < 4; ++j) {
+                unsigned __int128 tot = 0;
+                for (int t = 0; t < kTaps; ++t) {
+                    int c = std::abs(AT[i][t / 6] * AT[j][t % 6]);
+                    tot += (unsigned __int128)c * colsum[t] * 128u * ((unsigned __int128)1 << p->sh[t]);
+                }
+                worst = std::max(worst, tot);
+            }
+    }
+    worst += (unsigned __int128)maxbias;
+    if (out_shift > 0) worst += (unsigned __int128)1 << (out_shift - 1);
+    if (worst < ((unsigned __int128)1 << 31) && out_shift <= 31) p->epi_bits = 32;
+    else if (worst < ((unsigned __int128)1 << 62)) p->epi_bits = 64;
+    else return WINO_ERANGE;
+    return WINO_OK;
+}
+
+extern "C" wino_status wino_f4_plan_tables(const float* w_oihw, int32_t cin, int32_t cout,
+                                           const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                                           int32_t out_shift, int8_t* e_g, int8_t* sh, int32_t* e_o,
+                                           int32_t* epilogue_bits, int8_t* uq) {
+    wino_f4_plan_s* p = new (std::nothrow) wino_f4_plan_s();
+    if (!p) return WINO_ENOMEM;
+    p->uq_dev = nullptr;
+    p->bias_dev = nullptr;
+    wino_status st = compute_tables(p, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, 0);
+    if (st == WINO_OK) st = wino_f4_plan_info(p, e_g, sh, e_o, epilogue_bits, uq, nullptr, nullptr);
+    delete p;
+    return st;
+}
+
+extern "C" wino_status wino_f4_plan(wino_f4_plan_t* out, const float* w_oihw, int32_t cin,
+                                    int32_t cout, const int8_t* in_exp, const int8_t* w_exp,
+                                    const int32_t* bias, int32_t out_shift, int32_t relu,
+                                    hipStream_t stream) {
+    if (!out) return WINO_EINVAL;
+    *out = nullptr;
+    wino_f4_plan_s* p = new (std::nothrow) wino_f4_plan_s();
+    if (!p) return WINO_ENOMEM;
+    p->uq_dev = nullptr;
+    p->bias_dev = nullptr;
+    wino_status st = compute_tables(p, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, relu);
+    if (st != WINO_OK) {
+        delete p;
+        return st;
+    }
+    // device upload: Uq as [36][cout_pad][cin_pad] (GEMM A operand rows =
+    // output channels, k = input channels contiguous), bias [cout_pad]
+    std::vector<int8_t> dev_layout((size_t)kTaps * p->cout_pad * p->cin_pad, 0);
+    for (int t = 0; t < kTaps; ++t)
+        for (int ci = 0; ci < cin; ++ci)
+            for (int co = 0; co < cout; ++co)
+                dev_layout[((size_t)t * p->cout_pad + co) * p->cin_pad + ci] =
+                    p->uq_host[((size_t)t * cin + ci) * cout + co];
+    std::vector<int32_t> bias_pad(p->cout_pad, 0);
+    for (int co = 0; co < cout; ++co) bias_pad[co] = p->bias_host[co];
+    if (hipGetDevice(&p->device) != hipSuccess) { delete p; return WINO_EHIP; }
+    if (hipMalloc(&p->uq_dev, dev_layout.size()) != hipSuccess) { delete p; return WINO_ENOMEM; }
+    if (hipMalloc(&p->bias_dev, bias_pad.size() * sizeof(int32_t)) != hipSuccess) {
+        wino_f4_plan_destroy(p);
+        return WINO_ENOMEM;
+    }
+    bool ok = hipMemcpyAsync(p->uq_dev, dev_layout.data(), dev_layout.size(), hipMemcpyHostToDevice,
+                             stream) == hipSuccess &&
+              hipMemcpyAsync(p->bias_dev, bias_pad.data(), bias_pad.size() * sizeof(int32_t),
+                             hipMemcpyHostToDevice, stream) == hipSuccess &&
+              hipStreamSynchronize(stream) == hipSuccess;
+    if (!ok) {
+        wino_f4_plan_destroy(p);
+        return WINO_EHIP;
+    }
+    *out = p;
+    return WINO_OK;
+}
+
+extern "C" void wino_f4_plan_destroy(wino_f4_plan_t p) {
+    if (!p) return;
+    if (p->uq_dev) hipFree(p->uq_dev);
+    if (p->bias_dev) hipFree(p->bias_dev);
+    delete p;
+}
+
+extern "C" wino_status wino_f4_plan_info(wino_f4_plan_t p, int8_t* e_g, int8_t* sh, int32_t* e_o,
+                                         int32_t* epilogue_bits, int8_t* uq, int32_t* cin,
+                                         int32_t* cout) {
+    if (!p) return WINO_EINVAL;
+    if (e_g) std::memcpy(e_g, p->e_g, kTaps);
+    if (sh) std::memcpy(sh, p->sh, kTaps);
+    if (e_o) *e_o = p->e_o;
+    if (epilogue_bits) *epilogue_bits = p->epi_bits;
+    if (uq) std::memcpy(uq, p->uq_host.data(), p->uq_host.size());
+    if (cin) *cin = p->cin;
+    if (cout) *cout = p->cout;
+    return WINO_OK;
+}
+
+// Spatial int8 weights of the direct baseline (one power-of-two scale per
+// layer).  Each fp32 value v: 73728 * |v| style comparisons are not needed
+// here -- v / 2^e is exact in double (power-of-two scaling of a 24-bit
+// significand), and R is applied with an exact fractional-part test.
+extern "C" wino_status direct_conv_quantize_weights(const float* w_oihw, int32_t cout, int32_t cin,
+                                                    int8_t* w_ohwi, int32_t* e_out) {
+    if (!w_oihw || !w_ohwi || !e_out || cout < 1 || cin < 1) return WINO_EINVAL;
+    int64_t total = (int64_t)cout * cin * 9;
+    double amax = 0.0;
+    for (int64_t i = 0; i < total; ++i) {
+        if (!std::isfinite(w_oihw[i])) return WINO_EINVAL;
+        amax = std::max(amax, std::fabs((double)w_oihw[i]));
+    }
+    int e = 0;
+    if (amax > 0.0) {
+        // smallest e with amax <= 128 * 2^e; amax is exact, so ldexp tests are exact
+        int fe;
+        std::frexp(amax / 128.0, &fe);
+        e = fe - 1;
+        while (std::ldexp(128.0, e) < amax) ++e;
+        while (std::ldexp(128.0, e - 1) >= amax) --e;
+    }
+    for (int co = 0; co < cout; ++co)
+        for (int ci = 0; ci < cin; ++ci)
+            for (int r = 0; r < 3; ++r)
+                for (int c = 0; c < 3; ++c) {
+                    double u = std::ldexp((double)w_oihw[((int64_t)(co * cin + ci) * 3 + r) * 3 + c], -e);
+                    double fl = std::floor(u);
+                    double frac = u - fl;            // exact: u has at most 24 significant bits
+                    double q = frac >= 0.5 ? fl + 1.0 : fl;
+                    q = std::min(127.0, std::max(-128.0, q));
+                    w_ohwi[(((int64_t)co * 3 + r) * 3 + c) * cin + ci] = (int8_t)q;
+                }
+    *e_out = e;
+    return WINO_OK;
+}
+
+extern "C" const char* wino_strerror(wino_status s) {
+    switch (s) {
+        case WINO_OK: return "success";
+        case WINO_EINVAL: return "invalid argument";
+        case WINO_EUNSUPPORTED: return "size beyond the library's limits";
+        case WINO_ERANGE: return "plan tables exceed the integer epilogue range";
+        case WINO_ENOMEM: return "out of memory";
+        case WINO_EWORKSPACE: return "workspace missing or too small";
+        case WINO_EHIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}

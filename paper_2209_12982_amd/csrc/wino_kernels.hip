@@ -1,0 +1,660 @@
+// Online path of integer Winograd F(4x4,3x3) with tap-wise power-of-two
+// quantization (Sec. III), for gfx950.
+//
+//   K1 wino_input_xform   6x6 input tiles (stride 4, halo band staged in LDS),
+//                         V = B^T d B in packed 16-bit integer lanes (the
+//                         separable row-by-row form of Eq. general_wino_xform
+//                         with shared subexpressions, Sec. IV-B1), tap-wise
+//                         requantization R(V / 2^e_B) clamped to int8, and a
+//                         tap-major scatter Vq[36][tiles][Cin].
+//   K2 wino_tap_gemm      36 int8 GEMMs M_t = Uq_t * Vq_t on MFMA with int32
+//                         accumulation; the epilogue aligns taps by 2^sh,
+//                         applies Y = A^T M A, adds bias, requantizes and
+//                         stores int8 (Sec. III rearranged scheme; the
+//                         out_xform / dconv / write steps of the operator
+//                         dataflow, Sec. IV-B2).
+//
+// Bit exactness: all arithmetic is integer.  B^T d B of int8 data is at most
+// 12768 in magnitude and every intermediate of its row pass at most 1278, so
+// 16-bit lanes hold it (with a rounding constant of at most 2^14 added).  The
+// GEMM sums |Vq Uq| <= 2^14 per input channel in int32.  The output transform
+// runs in 32-bit integers when the plan's bound proves every partial sum fits,
+// otherwise in 64-bit.
+#include <type_traits>
+#include "winof4_internal.h"
+
+using namespace winof4;
+
+typedef short v2s __attribute__((ext_vector_type(2)));
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// K1: input transform
+// ---------------------------------------------------------------------------
+constexpr int K1_TX = 16;               // tiles per block along x
+constexpr int K1_CG = 64;               // channels per block
+constexpr int K1_COLS = 4 * K1_TX + 2;  // band width in pixels
+constexpr int K1_CS = 20;               // LDS words per pixel (16 used, 4 pad)
+constexpr int K1_THREADS = 256;
+
+struct K1Args {
+    int n, cin, h, w, th, tw, cin_pad;
+    int ntxb, ncg;
+    int x_vec;                          // 16-byte loads allowed (Cin % 16 == 0, x aligned)
+    long long t_pad;                    // tile stride of a tap plane in Vq
+    TapTables tab;
+};
+
+__device__ __forceinline__ v2s splat(int v) { return (v2s){(short)v, (short)v}; }
+
+// sign-extended bytes 0 and 2 of w as two 16-bit lanes
+__device__ __forceinline__ v2s lanes_even(uint32_t w) {
+    return __builtin_bit_cast(v2s, __builtin_amdgcn_perm(0u, w, 0x020c000cu)) >> splat(8);
+}
+// sign-extended bytes 1 and 3 of w
+__device__ __forceinline__ v2s lanes_odd(uint32_t w) {
+    return __builtin_bit_cast(v2s, w) >> splat(8);
+}
+
+// One-dimensional B^T transform of a 6-vector, twelve additions with shared
+// subexpressions; the rows of B^T (Sec. II) are
+//   4 0 -5 0 1 0 / 0 -4 -4 1 1 0 / 0 4 -4 -1 1 0 / 0 -2 -1 2 1 0 /
+//   0 2 -1 -2 1 0 / 0 4 0 -5 0 1.
+template <class T>
+__device__ __forceinline__ void bt_1d(const T* v, T* r, T two, T four) {
+    T a = v[4] - four * v[2];
+    T b = four * v[1] - v[3];
+    T c = v[4] - v[2];
+    T d = v[1] - v[3];
+    T e = v[0] - v[2];
+    T f = v[5] - v[3];
+    r[0] = four * e + c;
+    r[1] = a - b;
+    r[2] = a + b;
+    r[3] = c - two * d;
+    r[4] = c + two * d;
+    r[5] = four * d + f;
+}
+
+// Stage the halo band of one block into LDS as [row][col][channel] bytes
+// (channel fastest, K1_CS words per pixel).  Rows 4ty-1 .. 4ty+4, columns
+// 4tx0-1 .. 4tx0+4*K1_TX, channels ci0 .. ci0+63; zero outside the image and
+// beyond Cin.
+template <int LAYOUT>
+__device__ __forceinline__ void k1_stage_band(uint32_t* lds, const int8_t* __restrict__ x,
+                                              const K1Args& g, int img, int ty, int tx0, int ci0) {
+    const int h0 = 4 * ty - 1, w0 = 4 * tx0 - 1;
+    if (LAYOUT == WINO_NHWC) {
+        for (int id = threadIdx.x; id < 6 * K1_COLS * 4; id += K1_THREADS) {
+            int pix = id >> 2, part = id & 3;
+            int r = pix / K1_COLS, c = pix - r * K1_COLS;
+            int hh = h0 + r, ww = w0 + c, cb = ci0 + 16 * part;
+            uint4 v = make_uint4(0, 0, 0, 0);
+            if (hh >= 0 && hh < g.h && ww >= 0 && ww < g.w && cb < g.cin) {
+                const int8_t* src = x + (((long long)img * g.h + hh) * g.w + ww) * g.cin + cb;
+                if (g.x_vec) {
+                    v = *(const uint4*)src;
+                } else {
+                    uint32_t wv[4] = {0, 0, 0, 0};
+                    for (int k = 0; k < 16; ++k)
+                        if (cb + k < g.cin) wv[k >> 2] |= (uint32_t)(uint8_t)src[k] << (8 * (k & 3));
+                    v = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+                }
+            }
+            *(uint4*)(lds + pix * K1_CS + 4 * part) = v;
+        }
+    } else {
+        uint8_t* lb = (uint8_t*)lds;
+        for (int id = threadIdx.x; id < K1_CG * 6 * K1_COLS; id += K1_THREADS) {
+            int c = id % K1_COLS;
+            int rest = id / K1_COLS;
+            int r = rest % 6, ch = rest / 6;
+            int hh = h0 + r, ww = w0 + c, ci = ci0 + ch;
+            int8_t v = 0;
+            if (hh >= 0 && hh < g.h && ww >= 0 && ww < g.w && ci < g.cin)
+                v = x[(((long long)img * g.cin + ci) * g.h + hh) * g.w + ww];
+            lb[(r * K1_COLS + c) * K1_CS * 4 + ch] = (uint8_t)v;
+        }
+    }
+}
+
+// MODE 0: write Vq.  MODE 1: per-tap max |V| into tapmax[36] (calibration).
+template <int LAYOUT, int MODE>
+__global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __restrict__ x,
+                                                               int8_t* __restrict__ vq,
+                                                               int* __restrict__ tapmax, K1Args g) {
+    __shared__ uint32_t band[6 * K1_COLS * K1_CS];
+    __shared__ int red[kTaps];
+    int bid = blockIdx.x;
+    const int txb = bid % g.ntxb;
+    bid /= g.ntxb;
+    const int cgi = bid % g.ncg;
+    const int row = bid / g.ncg;          // img * th + ty
+    const int img = row / g.th, ty = row - img * g.th;
+    const int tx0 = txb * K1_TX, ci0 = cgi * K1_CG;
+    if (MODE == 1 && threadIdx.x < kTaps) red[threadIdx.x] = 0;
+
+    k1_stage_band<LAYOUT>(band, x, g, img, ty, tx0, ci0);
+    __syncthreads();
+
+    // thread -> (tile j, channel quad q): 16 quads x 16 tiles
+    const int q = threadIdx.x & 15;
+    const int j = threadIdx.x >> 4;
+    const int tx = tx0 + j;
+    const bool valid = tx < g.tw;
+
+    v2s ev[6][6], od[6][6];
+#pragma unroll
+    for (int r = 0; r < 6; ++r)
+#pragma unroll
+        for (int c = 0; c < 6; ++c) {
+            uint32_t wv = band[(r * K1_COLS + 4 * j + c) * K1_CS + q];
+            ev[r][c] = lanes_even(wv);
+            od[r][c] = lanes_odd(wv);
+        }
+    const v2s two = splat(2), four = splat(4);
+    // columns: T1 = B^T d
+#pragma unroll
+    for (int c = 0; c < 6; ++c) {
+        v2s ve[6], vo[6], re[6], ro[6];
+#pragma unroll
+        for (int r = 0; r < 6; ++r) { ve[r] = ev[r][c]; vo[r] = od[r][c]; }
+        bt_1d(ve, re, two, four);
+        bt_1d(vo, ro, two, four);
+#pragma unroll
+        for (int r = 0; r < 6; ++r) { ev[r][c] = re[r]; od[r][c] = ro[r]; }
+    }
+    // rows: V = T1 B
+#pragma unroll
+    for (int r = 0; r < 6; ++r) {
+        v2s re[6], ro[6];
+        bt_1d(ev[r], re, two, four);
+        bt_1d(od[r], ro, two, four);
+#pragma unroll
+        for (int c = 0; c < 6; ++c) { ev[r][c] = re[c]; od[r][c] = ro[c]; }
+    }
+
+    if (MODE == 0) {
+        if (!valid) return;
+        const long long tile = (long long)row * g.tw + tx;
+        uint32_t* dst = (uint32_t*)(vq + tile * g.cin_pad + ci0) + q;
+        const long long plane = g.t_pad * g.cin_pad / 4;   // words per tap plane
+#pragma unroll
+        for (int t = 0; t < kTaps; ++t) {
+            const int e = g.tab.eb[t];
+            const v2s rnd = splat(e ? (1 << (e - 1)) : 0);
+            const v2s sh = splat(e);
+            v2s a = (ev[t / 6][t % 6] + rnd) >> sh;
+            v2s b = (od[t / 6][t % 6] + rnd) >> sh;
+            a = __builtin_elementwise_min(__builtin_elementwise_max(a, splat(-128)), splat(127));
+            b = __builtin_elementwise_min(__builtin_elementwise_max(b, splat(-128)), splat(127));
+            // bytes: ch0 = a.lo, ch1 = b.lo, ch2 = a.hi, ch3 = b.hi
+            dst[t * plane] = __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, b),
+                                                   __builtin_bit_cast(uint32_t, a), 0x06020400u);
+        }
+    } else {
+        if (valid) {
+#pragma unroll
+            for (int t = 0; t < kTaps; ++t) {
+                v2s a = ev[t / 6][t % 6], b = od[t / 6][t % 6];
+                a = __builtin_elementwise_max(a, -a);
+                b = __builtin_elementwise_max(b, -b);
+                int m = max(max((int)a.x, (int)a.y), max((int)b.x, (int)b.y));
+                atomicMax(&red[t], m);
+            }
+        }
+        __syncthreads();
+        if (threadIdx.x < kTaps) atomicMax(&tapmax[threadIdx.x], red[threadIdx.x]);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// K2: tap GEMM with fused output transform
+// ---------------------------------------------------------------------------
+constexpr int K2_CO = 32;               // output channels per workgroup
+constexpr int K2_TL = 32;               // tiles per workgroup
+constexpr int K2_THREADS = 256;         // 4 waves, each 16 channels x 16 tiles
+
+struct K2Args {
+    int cin_pad, cout, cout_pad;
+    int n, h, w, th, tw;
+    long long ntiles, t_pad;
+    int nbco, nblocks;
+    int out_shift, relu;
+    TapTables tab;
+};
+
+// One-dimensional A^T transform of a 6-vector (rows of A^T, Sec. II:
+// 1 1 1 1 1 0 / 0 1 -1 2 -2 0 / 0 1 1 4 4 0 / 0 1 -1 8 -8 1).
+template <class T>
+__device__ __forceinline__ void at_1d(const T* v, T* y) {
+    T p = v[1] + v[2], m = v[1] - v[2], q = v[3] + v[4], r = v[3] - v[4];
+    y[0] = v[0] + p + q;
+    y[1] = m + (r << 1);
+    y[2] = p + (q << 2);
+    y[3] = m + (r << 3) + v[5];
+}
+
+// XCD-aware block order: hardware dispatches consecutive workgroup ids round
+// robin over the 8 XCDs; remap so that consecutive logical ids (the output
+// channel blocks of one tile block, which share its Vq rows) land on the
+// same XCD and its L2.
+__device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
+    const int nx = 8;
+    const int full = nblocks / nx * nx;
+    if (bid >= full) return bid;
+    return (bid % nx) * (full / nx) + bid / nx;
+}
+
+// MODE 0: store y.  MODE 1: max |Y + bias| into *zmax (calibration).
+// MODE 2: store raw M (debug export).
+template <int LAYOUT, int EPI, int MODE>
+__global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __restrict__ uq,
+                                                            const int8_t* __restrict__ vq,
+                                                            const int32_t* __restrict__ bias,
+                                                            int8_t* __restrict__ y,
+                                                            void* __restrict__ aux, K2Args g) {
+    typedef typename std::conditional<EPI == 64, long long, int>::type acc_t;
+    const int lbid = xcd_remap(blockIdx.x, g.nblocks);
+    const int bco = lbid % g.nbco, btl = lbid / g.nbco;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int co_base = bco * K2_CO + 16 * (wave & 1);
+    const long long tl_base = (long long)btl * K2_TL + 16 * (wave >> 1);
+    const int lr = lane & 15, lk = lane >> 4;
+
+    const int8_t* pa = uq + (long long)(co_base + lr) * g.cin_pad + 16 * lk;
+    const int8_t* pb = vq + (tl_base + lr) * g.cin_pad + 16 * lk;
+    const long long sa = (long long)g.cout_pad * g.cin_pad;   // tap stride of Uq
+    const long long sb = g.t_pad * g.cin_pad;                  // tap stride of Vq
+
+    v4i acc[kTaps];
+#pragma unroll
+    for (int t = 0; t < kTaps; ++t) acc[t] = (v4i){0, 0, 0, 0};
+
+    for (int k0 = 0; k0 < g.cin_pad; k0 += kKStep) {
+#pragma unroll
+        for (int t0 = 0; t0 < kTaps; t0 += 6) {
+            v4i av[6], bv[6];
+#pragma unroll
+            for (int u = 0; u < 6; ++u) {
+                av[u] = *(const v4i*)(pa + (t0 + u) * sa + k0);
+                bv[u] = *(const v4i*)(pb + (t0 + u) * sb + k0);
+            }
+#pragma unroll
+            for (int u = 0; u < 6; ++u)
+                acc[t0 + u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av[u], bv[u], acc[t0 + u], 0, 0, 0);
+        }
+    }
+
+    // accumulator layout: lane holds C[row = 4*lk + r][col = lr], rows are
+    // output channels, columns are tiles
+    const long long tile = tl_base + lr;
+    const bool tile_ok = tile < g.ntiles;
+
+    if (MODE == 2) {
+        int32_t* m_out = (int32_t*)aux;
+        if (!tile_ok) return;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int co = co_base + 4 * lk + r;
+            if (co >= g.cout) continue;
+#pragma unroll
+            for (int t = 0; t < kTaps; ++t) m_out[((long long)t * g.ntiles + tile) * g.cout + co] = acc[t][r];
+        }
+        return;
+    }
+
+    const int img = (int)(tile / ((long long)g.th * g.tw));
+    const int trem = (int)(tile - (long long)img * g.th * g.tw);
+    const int ty = trem / g.tw, tx = trem - ty * g.tw;
+    const int s = g.out_shift;
+    const acc_t rnd = (MODE == 0 && s > 0) ? ((acc_t)1 << (s - 1)) : 0;
+    const int lo = g.relu ? 0 : -128;
+    unsigned long long zmax = 0;
+    uint32_t packed[16];                 // NHWC: 4 output channels per pixel
+#pragma unroll
+    for (int p = 0; p < 16; ++p) packed[p] = 0;
+
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int co = co_base + 4 * lk + r;
+        acc_t mv[kTaps];
+#pragma unroll
+        for (int t = 0; t < kTaps; ++t) mv[t] = (acc_t)acc[t][r] << g.tab.sh[t];
+        // bias (and the rounding constant) enter once through tap (1,1),
+        // whose column of A^T is all ones: A^T (c e_7 e_7^T) A adds c to
+        // every output of the tile.
+        mv[7] += (acc_t)bias[co] + rnd;
+        acc_t rp[6][4];
+#pragma unroll
+        for (int a = 0; a < 6; ++a) at_1d(&mv[6 * a], rp[a]);
+        acc_t yv[4][4];
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            acc_t col[6], o[4];
+#pragma unroll
+            for (int a = 0; a < 6; ++a) col[a] = rp[a][jj];
+            at_1d(col, o);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) yv[i][jj] = o[i];
+        }
+        if (MODE == 1) {
+            if (tile_ok && co < g.cout) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj)
+                        if (4 * ty + i < g.h && 4 * tx + jj < g.w) {
+                            acc_t v = yv[i][jj];
+                            unsigned long long av = (unsigned long long)(v < 0 ? -(long long)v : (long long)v);
+                            zmax = av > zmax ? av : zmax;
+                        }
+            }
+            continue;
+        }
+        int qv[4][4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                acc_t v = yv[i][jj] >> s;
+                v = v < (acc_t)lo ? (acc_t)lo : v;
+                v = v > (acc_t)127 ? (acc_t)127 : v;
+                qv[i][jj] = (int)v;
+            }
+        if (LAYOUT == WINO_NCHW) {
+            if (!tile_ok || co >= g.cout) continue;
+            int8_t* base = y + (((long long)img * g.cout + co) * g.h + 4 * ty) * g.w + 4 * tx;
+            const bool full_cols = (4 * tx + 3 < g.w) && ((g.w & 3) == 0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                if (4 * ty + i >= g.h) continue;
+                if (full_cols) {
+                    uint32_t wv = (uint32_t)(qv[i][0] & 255) | ((uint32_t)(qv[i][1] & 255) << 8) |
+                                  ((uint32_t)(qv[i][2] & 255) << 16) | ((uint32_t)(qv[i][3] & 255) << 24);
+                    *(uint32_t*)(base + (long long)i * g.w) = wv;
+                } else {
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj)
+                        if (4 * tx + jj < g.w) base[(long long)i * g.w + jj] = (int8_t)qv[i][jj];
+                }
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) packed[4 * i + jj] |= (uint32_t)(qv[i][jj] & 255) << (8 * r);
+        }
+    }
+
+    if (MODE == 1) {
+        // wave reduction, then one atomic per wave
+        for (int off = 32; off > 0; off >>= 1) {
+            unsigned long long o = __shfl_xor(zmax, off, 64);
+            zmax = o > zmax ? o : zmax;
+        }
+        if (lane == 0) atomicMax((unsigned long long*)aux, zmax);
+        return;
+    }
+    if (LAYOUT == WINO_NHWC && tile_ok) {
+        const int co0 = co_base + 4 * lk;
+        const bool full = (co0 + 3 < g.cout) && ((g.cout & 3) == 0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const int hh = 4 * ty + i, ww = 4 * tx + jj;
+                if (hh >= g.h || ww >= g.w) continue;
+                int8_t* dst = y + (((long long)img * g.h + hh) * g.w + ww) * g.cout + co0;
+                if (full) {
+                    *(uint32_t*)dst = packed[4 * i + jj];
+                } else {
+                    for (int r = 0; r < 4; ++r)
+                        if (co0 + r < g.cout) dst[r] = (int8_t)(packed[4 * i + jj] >> (8 * r));
+                }
+            }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// host-side helpers
+// ---------------------------------------------------------------------------
+struct Geometry {
+    int n, h, w, th, tw;
+    long long ntiles, t_pad;
+};
+
+wino_status geometry(int32_t n, int32_t h, int32_t w, Geometry& g) {
+    if (n < 0 || h < 0 || w < 0) return WINO_EINVAL;
+    if (h > 65536 || w > 65536) return WINO_EUNSUPPORTED;
+    g.n = n;
+    g.h = h;
+    g.w = w;
+    g.th = (h + 3) / 4;
+    g.tw = (w + 3) / 4;
+    g.ntiles = (long long)n * g.th * g.tw;
+    if (g.ntiles >= (1ll << 26)) return WINO_EUNSUPPORTED;
+    g.t_pad = round_up(g.ntiles, kTilePad);
+    return WINO_OK;
+}
+
+size_t vq_bytes(const wino_f4_plan_s* p, const Geometry& g) {
+    return (size_t)kTaps * (size_t)g.t_pad * (size_t)p->cin_pad;
+}
+
+TapTables tables_of(const wino_f4_plan_s* p) {
+    TapTables t;
+    for (int i = 0; i < kTaps; ++i) {
+        t.eb[i] = p->e_b[i];
+        t.sh[i] = p->sh[i];
+    }
+    return t;
+}
+
+K1Args k1_args(const Geometry& g, int cin, int cin_pad, const TapTables& tab) {
+    K1Args a;
+    a.n = g.n;
+    a.cin = cin;
+    a.h = g.h;
+    a.w = g.w;
+    a.th = g.th;
+    a.tw = g.tw;
+    a.cin_pad = cin_pad;
+    a.ntxb = (g.tw + K1_TX - 1) / K1_TX;
+    a.ncg = cin_pad / K1_CG;
+    a.t_pad = g.t_pad;
+    a.tab = tab;
+    a.x_vec = 0;
+    return a;
+}
+
+template <int MODE>
+wino_status launch_k1(const K1Args& a, wino_layout layout, const int8_t* x, int8_t* vq, int* tapmax,
+                      hipStream_t stream) {
+    long long blocks = (long long)a.ntxb * a.ncg * a.n * a.th;
+    if (blocks == 0) return WINO_OK;
+    if (blocks > 0x7fffffffll) return WINO_EUNSUPPORTED;
+    K1Args args = a;
+    args.x_vec = (a.cin % 16 == 0) && (((uintptr_t)x & 15) == 0);
+    if (layout == WINO_NHWC)
+        hipLaunchKernelGGL((wino_input_xform<WINO_NHWC, MODE>), dim3((unsigned)blocks), dim3(K1_THREADS), 0,
+                           stream, x, vq, tapmax, args);
+    else
+        hipLaunchKernelGGL((wino_input_xform<WINO_NCHW, MODE>), dim3((unsigned)blocks), dim3(K1_THREADS), 0,
+                           stream, x, vq, tapmax, args);
+    return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
+}
+
+template <int MODE>
+wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout layout, const int8_t* vq,
+                      int8_t* y, void* aux, hipStream_t stream) {
+    K2Args a;
+    a.cin_pad = p->cin_pad;
+    a.cout = p->cout;
+    a.cout_pad = p->cout_pad;
+    a.n = g.n;
+    a.h = g.h;
+    a.w = g.w;
+    a.th = g.th;
+    a.tw = g.tw;
+    a.ntiles = g.ntiles;
+    a.t_pad = g.t_pad;
+    a.nbco = p->cout_pad / K2_CO;
+    long long nbtl = (g.ntiles + K2_TL - 1) / K2_TL;
+    long long blocks = nbtl * a.nbco;
+    if (blocks == 0) return WINO_OK;
+    if (blocks > 0x7fffffffll) return WINO_EUNSUPPORTED;
+    a.nblocks = (int)blocks;
+    a.out_shift = p->out_shift;
+    a.relu = p->relu;
+    a.tab = tables_of(p);
+    dim3 grid((unsigned)blocks), block(K2_THREADS);
+#define K2_LAUNCH(L, E)                                                                              \
+    hipLaunchKernelGGL((wino_tap_gemm<L, E, MODE>), grid, block, 0, stream, p->uq_dev, vq, p->bias_dev, \
+                       y, aux, a)
+    if (layout == WINO_NHWC) {
+        if (p->epi_bits == 32) K2_LAUNCH(WINO_NHWC, 32); else K2_LAUNCH(WINO_NHWC, 64);
+    } else {
+        if (p->epi_bits == 32) K2_LAUNCH(WINO_NCHW, 32); else K2_LAUNCH(WINO_NCHW, 64);
+    }
+#undef K2_LAUNCH
+    return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
+}
+
+wino_status check_common(const wino_f4_plan_s* p, const void* x, int32_t n, int32_t h, int32_t w,
+                         wino_layout layout, Geometry& g) {
+    if (!p || !x) return WINO_EINVAL;
+    if (layout != WINO_NCHW && layout != WINO_NHWC) return WINO_EINVAL;
+    return geometry(n, h, w, g);
+}
+
+int cexp_int(unsigned long long a) {
+    // smallest e >= 0 with a <= 128 * 2^e (callers clamp at 0 anyway)
+    int e = 0;
+    while ((unsigned long long)128 << e < a && e < 62) ++e;
+    return e;
+}
+
+}  // namespace
+
+extern "C" size_t wino_f4_workspace_bytes(wino_f4_plan_t p, int32_t n, int32_t h, int32_t w,
+                                          wino_variant variant) {
+    Geometry g;
+    if (!p || geometry(n, h, w, g) != WINO_OK) return 0;
+    if (variant == WINO_FUSED) return 0;
+    return vq_bytes(p, g);
+}
+
+// FUSED is served by the kernel in wino_fused.hip.
+wino_status wino_f4_conv_fused(const wino_f4_plan_s* p, const int8_t* x, int8_t* y, int n, int h, int w,
+                               wino_layout layout, hipStream_t stream);
+
+extern "C" wino_status wino_f4_conv_int8(wino_f4_plan_t p, const int8_t* x, int8_t* y, int32_t n,
+                                         int32_t h, int32_t w, wino_layout layout, wino_variant variant,
+                                         void* ws, size_t ws_bytes, hipStream_t stream) {
+    Geometry g;
+    wino_status st = check_common(p, x, n, h, w, layout, g);
+    if (st != WINO_OK) return st;
+    if (!y) return WINO_EINVAL;
+    if (variant != WINO_SPLIT && variant != WINO_FUSED) return WINO_EINVAL;
+    if (g.ntiles == 0) return WINO_OK;
+    if (variant == WINO_FUSED) return wino_f4_conv_fused(p, x, y, n, h, w, layout, stream);
+    if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
+    int8_t* vq = (int8_t*)ws;
+    st = launch_k1<0>(k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, vq, nullptr, stream);
+    if (st != WINO_OK) return st;
+    return launch_k2<0>(p, g, layout, vq, y, nullptr, stream);
+}
+
+extern "C" wino_status wino_f4_calibrate_input(const int8_t* x, int32_t n, int32_t cin, int32_t h, int32_t w,
+                                               wino_layout layout, int32_t* absmax, int8_t* e_b,
+                                               hipStream_t stream) {
+    if (!x || cin < 1) return WINO_EINVAL;
+    if (cin > 65536) return WINO_EUNSUPPORTED;
+    if (layout != WINO_NCHW && layout != WINO_NHWC) return WINO_EINVAL;
+    Geometry g;
+    wino_status st = geometry(n, h, w, g);
+    if (st != WINO_OK) return st;
+    int host[kTaps] = {0};
+    if (g.ntiles > 0) {
+        int* dmax = nullptr;
+        if (hipMalloc(&dmax, sizeof(int) * kTaps) != hipSuccess) return WINO_ENOMEM;
+        TapTables tab = {};
+        bool ok = hipMemsetAsync(dmax, 0, sizeof(int) * kTaps, stream) == hipSuccess;
+        if (ok) ok = launch_k1<1>(k1_args(g, cin, (int)round_up(cin, kKStep), tab), layout, x, nullptr, dmax,
+                                  stream) == WINO_OK;
+        if (ok) ok = hipMemcpyAsync(host, dmax, sizeof(int) * kTaps, hipMemcpyDeviceToHost, stream) == hipSuccess;
+        if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
+        hipFree(dmax);
+        if (!ok) return WINO_EHIP;
+    }
+    for (int t = 0; t < kTaps; ++t) {
+        if (absmax) absmax[t] = host[t];
+        if (e_b) {
+            int e = cexp_int((unsigned long long)host[t]);
+            e_b[t] = (int8_t)(e > 15 ? 15 : e);
+        }
+    }
+    return WINO_OK;
+}
+
+extern "C" wino_status wino_f4_calibrate_output(wino_f4_plan_t p, const int8_t* x, int32_t n, int32_t h,
+                                                int32_t w, wino_layout layout, void* ws, size_t ws_bytes,
+                                                int64_t* zmax, int32_t* out_shift, hipStream_t stream) {
+    Geometry g;
+    wino_status st = check_common(p, x, n, h, w, layout, g);
+    if (st != WINO_OK) return st;
+    unsigned long long host = 0;
+    if (g.ntiles > 0) {
+        if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
+        unsigned long long* dmax = nullptr;
+        if (hipMalloc(&dmax, sizeof(unsigned long long)) != hipSuccess) return WINO_ENOMEM;
+        bool ok = hipMemsetAsync(dmax, 0, sizeof(unsigned long long), stream) == hipSuccess;
+        if (ok) ok = launch_k1<0>(k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr,
+                                  stream) == WINO_OK;
+        if (ok) ok = launch_k2<1>(p, g, layout, (const int8_t*)ws, nullptr, dmax, stream) == WINO_OK;
+        if (ok) ok = hipMemcpyAsync(&host, dmax, sizeof(host), hipMemcpyDeviceToHost, stream) == hipSuccess;
+        if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
+        hipFree(dmax);
+        if (!ok) return WINO_EHIP;
+    }
+    if (zmax) *zmax = (int64_t)host;
+    if (out_shift) *out_shift = cexp_int(host);
+    return WINO_OK;
+}
+
+extern "C" wino_status wino_f4_debug_input_transform(wino_f4_plan_t p, const int8_t* x, int32_t n, int32_t h,
+                                                     int32_t w, wino_layout layout, int8_t* vq_out, void* ws,
+                                                     size_t ws_bytes, hipStream_t stream) {
+    Geometry g;
+    wino_status st = check_common(p, x, n, h, w, layout, g);
+    if (st != WINO_OK) return st;
+    if (!vq_out) return WINO_EINVAL;
+    if (g.ntiles == 0) return WINO_OK;
+    if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
+    st = launch_k1<0>(k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
+    if (st != WINO_OK) return st;
+    // compact [36][t_pad][cin_pad] -> [36][ntiles][cin], one 2-D copy per tap plane
+    for (int t = 0; t < kTaps; ++t)
+        if (hipMemcpy2DAsync(vq_out + (size_t)t * g.ntiles * p->cin, (size_t)p->cin,
+                             (const int8_t*)ws + (size_t)t * g.t_pad * p->cin_pad, (size_t)p->cin_pad,
+                             (size_t)p->cin, (size_t)g.ntiles, hipMemcpyDeviceToDevice, stream) != hipSuccess)
+            return WINO_EHIP;
+    return WINO_OK;
+}
+
+extern "C" wino_status wino_f4_debug_tap_gemm(wino_f4_plan_t p, const int8_t* x, int32_t n, int32_t h,
+                                              int32_t w, wino_layout layout, int32_t* m_out, void* ws,
+                                              size_t ws_bytes, hipStream_t stream) {
+    Geometry g;
+    wino_status st = check_common(p, x, n, h, w, layout, g);
+    if (st != WINO_OK) return st;
+    if (!m_out) return WINO_EINVAL;
+    if (g.ntiles == 0) return WINO_OK;
+    if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
+    st = launch_k1<0>(k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
+    if (st != WINO_OK) return st;
+    return launch_k2<2>(p, g, layout, (const int8_t*)ws, nullptr, m_out, stream);
+}

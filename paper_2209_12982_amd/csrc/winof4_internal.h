@@ -1,0 +1,40 @@
+// Internal definitions shared by the host plan and the kernel launchers.
+#pragma once
+#include <stdint.h>
+#include <vector>
+#include <hip/hip_runtime.h>
+#include "../../include/winof4.h"
+
+namespace winof4 {
+
+constexpr int kTaps = 36;
+// Channel padding granule: one int8 MFMA k-step.
+constexpr int kKStep = 64;
+// Output-channel padding granule of the tap-GEMM workgroup.
+constexpr int kCoutPad = 64;
+// Tile padding granule of the tap-GEMM workgroup.
+constexpr int kTilePad = 64;
+
+inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+// Per-tap tables passed by value to the kernels (they land in the kernarg
+// segment and are read through scalar loads).
+struct TapTables {
+    int8_t eb[kTaps];   // input tap exponents e_B
+    int8_t sh[kTaps];   // alignment shifts e_B + e_G - e_o
+};
+
+}  // namespace winof4
+
+struct wino_f4_plan_s {
+    int32_t cin, cout, cin_pad, cout_pad;
+    int8_t e_b[winof4::kTaps], e_g[winof4::kTaps], sh[winof4::kTaps];
+    int32_t e_o;
+    int32_t out_shift, relu;
+    int32_t epi_bits;                 // 32 or 64
+    int32_t device;
+    int8_t* uq_dev;                   // [36][cout_pad][cin_pad], zero padded
+    int32_t* bias_dev;                // [cout_pad], zero padded
+    std::vector<int8_t> uq_host;      // [36][cin][cout]
+    std::vector<int32_t> bias_host;   // [cout]
+};

@@ -1,0 +1,175 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, bit for
+bit (integer path: exact equality is the only correct result)."""
+import numpy as np
+import pytest
+
+import paper_2209_12982_amd as W
+import workloads
+from oracle import direct, tapwise
+
+from gpu_util import empty_out, from_device_nchw, run_conv, to_device, torch_dev, workspace
+
+pytestmark = pytest.mark.gpu
+
+LAYOUTS = [W.NCHW, W.NHWC]
+
+
+def _plan_pair(f, eb, bias, out_shift, relu, e_g=None):
+    gp = W.wino_f4_plan(f, eb, w_exp=e_g, bias=bias, out_shift=out_shift, relu=relu)
+    op = tapwise.make_plan(f, eb, e_g=e_g, bias=bias, out_shift=out_shift, relu=relu)
+    return gp, op
+
+
+SHAPES = [
+    # n, cin, cout, h, w
+    (1, 1, 1, 1, 1),
+    (1, 3, 5, 7, 9),
+    (2, 16, 16, 8, 8),
+    (1, 64, 64, 17, 13),
+    (2, 70, 80, 12, 30),
+    (1, 130, 33, 5, 66),
+    (3, 8, 100, 2, 3),
+]
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("shape", SHAPES)
+def test_input_transform_bitexact(shape, layout):
+    torch = torch_dev()
+    n, cin, cout, h, w = shape
+    x, f, b = workloads.random_case(1, n, cin, cout, h, w, signed=True)
+    eb = [int(v) for v in np.random.default_rng(2).integers(0, 9, 36)]
+    gp = W.wino_f4_plan(f, eb, bias=b)
+    ws = workspace(gp, n, h, w)
+    th, tw = tapwise.tile_grid(h, w)
+    vq = torch.empty((36, n * th * tw, cin), dtype=torch.int8, device="cuda")
+    W.wino_f4_debug_input_transform(gp, to_device(x, layout), n, h, w, layout, vq, ws)
+    torch.cuda.synchronize()
+    ref = tapwise.input_taps_quantized(x, eb)
+    assert (vq.cpu().numpy() == ref).all()
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("shape", SHAPES)
+def test_tap_gemm_bitexact(shape, layout):
+    torch = torch_dev()
+    n, cin, cout, h, w = shape
+    x, f, b = workloads.random_case(3, n, cin, cout, h, w, signed=True)
+    eb = [int(v) for v in np.random.default_rng(4).integers(0, 9, 36)]
+    gp, op = _plan_pair(f, eb, b, 0, False)
+    ws = workspace(gp, n, h, w)
+    th, tw = tapwise.tile_grid(h, w)
+    m = torch.empty((36, n * th * tw, cout), dtype=torch.int32, device="cuda")
+    W.wino_f4_debug_tap_gemm(gp, to_device(x, layout), n, h, w, layout, m, ws)
+    torch.cuda.synchronize()
+    ref = tapwise.tap_gemm(tapwise.input_taps_quantized(x, eb), op["uq"])
+    assert (m.cpu().numpy().astype(np.int64) == ref).all()
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("relu,out_shift", [(False, 9), (True, 12)])
+def test_conv_bitexact_random(shape, layout, relu, out_shift):
+    n, cin, cout, h, w = shape
+    x, f, b = workloads.random_case(5, n, cin, cout, h, w, signed=True)
+    eb = tapwise.calibrate_input_exps(x)
+    gp, op = _plan_pair(f, eb, b, out_shift, relu)
+    assert W.wino_f4_plan_info(gp)["epilogue_bits"] == 32
+    y = run_conv(gp, x, layout)
+    ref = tapwise.conv_int8(x, op)
+    assert (y == ref).all(), f"{(y != ref).sum()} mismatches"
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_conv_int64_epilogue(layout):
+    """Large alignment shifts force the 64-bit output transform."""
+    n, cin, cout, h, w = 1, 20, 24, 11, 10
+    x, f, b = workloads.random_case(6, n, cin, cout, h, w, signed=True)
+    eb = [0] * 36
+    eb[35] = 15
+    eb[0] = 14
+    gp, op = _plan_pair(f, eb, b, 20, False)
+    assert W.wino_f4_plan_info(gp)["epilogue_bits"] == 64
+    y = run_conv(gp, x, layout)
+    assert (y == tapwise.conv_int8(x, op)).all()
+
+
+def test_conv_deterministic_repeat():
+    n, cin, cout, h, w = 2, 96, 96, 30, 30
+    x, f, b = workloads.random_case(7, n, cin, cout, h, w, signed=False, zero_frac=0.5)
+    eb = tapwise.calibrate_input_exps(x)
+    gp = W.wino_f4_plan(f, eb, bias=b, out_shift=11)
+    y1 = run_conv(gp, x, W.NHWC)
+    y2 = run_conv(gp, x, W.NHWC)
+    assert (y1 == y2).all()
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("shape", [(1, 3, 5, 7, 9), (2, 64, 40, 16, 20), (1, 200, 8, 9, 9)])
+def test_calibrate_input_matches_oracle(shape, layout):
+    torch_dev()
+    n, cin, cout, h, w = shape
+    x, f, b = workloads.random_case(8, n, cin, cout, h, w, signed=True)
+    eb, amax = W.wino_f4_calibrate_input(to_device(x, layout), n, cin, h, w, layout)
+    assert amax == tapwise.input_tap_absmax(x)
+    assert eb == tapwise.calibrate_input_exps(x)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_calibrate_output_matches_oracle(layout):
+    torch_dev()
+    n, cin, cout, h, w = 2, 24, 40, 13, 18
+    x, f, b = workloads.random_case(9, n, cin, cout, h, w, signed=False, zero_frac=0.3)
+    eb = tapwise.calibrate_input_exps(x)
+    gp, op = _plan_pair(f, eb, b, 0, False)
+    s, zmax = W.wino_f4_calibrate_output(gp, to_device(x, layout), n, h, w, layout, workspace(gp, n, h, w))
+    z = tapwise.prequant_output(x, op)
+    assert zmax == int(np.abs(z).max())
+    assert s == tapwise.calibrate_out_shift(x, op)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("shape", [(1, 16, 16, 32, 32), (2, 3, 5, 7, 9), (1, 70, 130, 9, 14)])
+def test_direct_conv_bitexact(shape, layout):
+    torch = torch_dev()
+    n, cin, cout, h, w = shape
+    x, f, b = workloads.random_case(10, n, cin, cout, h, w, signed=True)
+    w_ohwi, e = W.direct_conv_quantize_weights(f)
+    wq_ref, e_ref = direct.quantize_weights_pow2(f)
+    assert e == e_ref and (w_ohwi == wq_ref.transpose(0, 2, 3, 1)).all()
+    y = empty_out(n, cout, h, w, layout)
+    W.direct_conv_int8(to_device(x, layout), torch.from_numpy(w_ohwi).cuda(), torch.from_numpy(b).cuda(), y,
+                       n, cin, cout, h, w, layout, 9, False)
+    torch.cuda.synchronize()
+    ref = direct.conv_int8(x, wq_ref, b, 9, False)
+    assert (from_device_nchw(y, layout) == ref).all()
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_config_c1_bitexact(layout):
+    """C1 as specified: out_shift 8 (the literal value), calibrated e_B."""
+    x, layers = workloads.generate("C1")
+    f, b, spec = layers[0]
+    eb_gpu, _ = W.wino_f4_calibrate_input(to_device(x, layout), *[x.shape[0], spec.cin, spec.h, spec.w], layout)
+    eb = tapwise.calibrate_input_exps(x)
+    assert eb_gpu == eb
+    gp, op = _plan_pair(f, eb, b, 8, False)
+    y = run_conv(gp, x, layout)
+    assert (y == tapwise.conv_int8(x, op)).all()
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_config_c2_bitexact(layout):
+    x, layers = workloads.generate("C2")
+    f, b, spec = layers[0]
+    n = x.shape[0]
+    xd = to_device(x, layout)
+    eb, _ = W.wino_f4_calibrate_input(xd, n, spec.cin, spec.h, spec.w, layout)
+    assert eb == tapwise.calibrate_input_exps(x)
+    gp0 = W.wino_f4_plan(f, eb, bias=b)
+    s, _ = W.wino_f4_calibrate_output(gp0, xd, n, spec.h, spec.w, layout, workspace(gp0, n, spec.h, spec.w))
+    op = tapwise.make_plan(f, eb, bias=b, out_shift=0)
+    assert s == tapwise.calibrate_out_shift(x, op)
+    gp, op = _plan_pair(f, eb, b, s, False)
+    y = run_conv(gp, x, layout)
+    assert (y == tapwise.conv_int8(x, op)).all()
