@@ -1,0 +1,217 @@
+#!/usr/bin/env python3
+"""Benchmark of the integer Winograd F(4x4,3x3) layer with tap-wise
+power-of-two quantization on one MI355X.
+
+One step = one pass of the whole online path over one batch: input transform
+with tap-wise requant (K1) and the 36-tap int8 MFMA GEMM with the fused
+output transform, bias and requant (K2), i.e. one wino_f4_conv_int8 call.
+Inputs are resident in HBM before the timed region.  The default workload is
+the largest layer (N=4, 256->256, 160x160, NHWC), the configuration the
+tap-GEMM MFMA-utilisation target refers to.
+
+Printed on one JSON line: the contract fields, the roofline of the dominant
+kernel (durations from HIP events on the launch stream), both kernels'
+figures, the direct int8 convolution of the same library on the same layer
+(speed-up), and the CPU oracle timed on a bounded sample.
+"""
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "Winograd F4 int8 conv: effective TOPS (direct-equiv) + % of int8 MFMA peak"
+PEAK_INT8_TOPS = 5000.0      # MI355X dense int8 MFMA, TOP/s
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, GB/s
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="C5", help="C1 .. C5 (C3: first layer)")
+    ap.add_argument("--layout", default="nhwc", choices=["nchw", "nhwc"])
+    ap.add_argument("--variant", default="split", choices=["split", "fused"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-direct", action="store_true")
+    ap.add_argument("--cpu-images", type=int, default=0, help="oracle sample size (images); 0 = auto")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run a plain 256 MiB device-to-device copy (scale reference for HBM counters)")
+    return ap.parse_args()
+
+
+def time_loop(torch, fn, steps):
+    """Average ms per call over `steps` back-to-back calls, HIP events on the
+    current stream (the stream every library call is enqueued on)."""
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(steps):
+        fn()
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / steps
+
+
+def cpu_baseline(x, layers_plan, n_img, spec):
+    """The oracle's online path (a-1 .. a-6, plan excluded) on the first
+    n_img images of the same workload."""
+    import numpy as np
+    from oracle import tapwise
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    xs = np.ascontiguousarray(x[:n_img])
+    t0 = time.perf_counter()
+    tapwise.conv_int8(xs, layers_plan)
+    dt = time.perf_counter() - t0
+    ops = 2.0 * 9 * n_img * spec.h * spec.w * spec.cin * spec.cout
+    return {"value": ops / dt / 1e12, "unit": "TOPS", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n_img} of {x.shape[0]} images of the same layer, full online path "
+                      f"(numpy int64 transforms, float64 BLAS tap GEMM), {dt:.2f} s",
+            "seconds": dt, "host_cpus": os.cpu_count(),
+            "affinity": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the layer shards by batch with no communication; see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2209_12982_amd as W
+    import workloads
+
+    torch.cuda.set_device(0)
+    layout = W.NHWC if args.layout == "nhwc" else W.NCHW
+    variant = W.SPLIT if args.variant == "split" else W.FUSED
+    wl = workloads.WORKLOADS[args.config]
+    x, layers = workloads.generate(args.config)
+    f, bias, spec = layers[0]
+    n, cin, cout, h, w = x.shape[0], spec.cin, spec.cout, spec.h, spec.w
+    xa = x if layout == W.NCHW else np.ascontiguousarray(x.transpose(0, 2, 3, 1))
+    xd = torch.from_numpy(xa).cuda()
+    yshape = (n, cout, h, w) if layout == W.NCHW else (n, h, w, cout)
+    y = torch.empty(yshape, dtype=torch.int8, device="cuda")
+
+    # offline: calibration and plan (not timed)
+    eb, _ = W.wino_f4_calibrate_input(xd, n, cin, h, w, layout)
+    plan0 = W.wino_f4_plan(f, eb, bias=bias, out_shift=0, relu=spec.relu)
+    ws = torch.empty(max(1, W.wino_f4_workspace_bytes(plan0, n, h, w, W.SPLIT)), dtype=torch.int8, device="cuda")
+    out_shift = spec.out_shift
+    if out_shift is None:
+        out_shift, _ = W.wino_f4_calibrate_output(plan0, xd, n, h, w, layout, ws)
+    plan = W.wino_f4_plan(f, eb, bias=bias, out_shift=out_shift, relu=spec.relu)
+    info = W.wino_f4_plan_info(plan)
+
+    def step():
+        W.wino_f4_conv_int8(plan, xd, y, n, h, w, layout, variant, ws if variant == W.SPLIT else None)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ms = time_loop(torch, step, args.steps)
+
+    # per-kernel durations: the same two launches, events between them
+    th, tw = (h + 3) // 4, (w + 3) // 4
+    T = n * th * tw
+    k1_ms = k2_ms = None
+    if variant == W.SPLIT:
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        for k in range(args.steps):
+            ev[k][0].record()
+            W.wino_f4_input_transform(plan, xd, n, h, w, layout, ws)
+            ev[k][1].record()
+            W.wino_f4_tap_gemm(plan, ws, y, n, h, w, layout)
+            ev[k][2].record()
+        torch.cuda.synchronize()
+        k1_ms = statistics.mean(e[0].elapsed_time(e[1]) for e in ev)
+        k2_ms = statistics.mean(e[1].elapsed_time(e[2]) for e in ev)
+
+    direct_ops = 2.0 * 9 * n * h * w * cin * cout
+    tap_ops = 2.0 * 36 * T * cin * cout
+    value = direct_ops / (ms * 1e-3) / 1e12
+    k1_bytes = n * h * w * cin + 36 * T * cin                 # read x, write Vq
+    k2_bytes = 36 * T * cin + 36 * cin * cout + n * h * w * cout + 4 * cout
+    kernels = {}
+    if k1_ms is not None:
+        kernels["wino_input_xform"] = {"ms": k1_ms, "bound": "hbm", "bytes": k1_bytes,
+                                       "GB/s": k1_bytes / (k1_ms * 1e-3) / 1e9,
+                                       "frac": k1_bytes / (k1_ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
+        kernels["wino_tap_gemm"] = {"ms": k2_ms, "bound": "mfma", "ops": tap_ops,
+                                    "TOP/s": tap_ops / (k2_ms * 1e-3) / 1e12,
+                                    "frac": tap_ops / (k2_ms * 1e-3) / 1e12 / PEAK_INT8_TOPS,
+                                    "GB/s_algorithmic": k2_bytes / (k2_ms * 1e-3) / 1e9}
+        dom = "wino_tap_gemm" if k2_ms >= k1_ms else "wino_input_xform"
+        if dom == "wino_tap_gemm":
+            roofline = {"kernel": dom, "bound": "mfma", "achieved": kernels[dom]["TOP/s"],
+                        "peak": PEAK_INT8_TOPS, "unit": "TOP/s", "frac": kernels[dom]["frac"], "traffic": None}
+        else:
+            roofline = {"kernel": dom, "bound": "hbm", "achieved": kernels[dom]["GB/s"],
+                        "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": kernels[dom]["frac"], "traffic": None}
+    else:
+        roofline = {"kernel": "wino_fused", "bound": "mfma", "achieved": tap_ops / (ms * 1e-3) / 1e12,
+                    "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
+                    "frac": tap_ops / (ms * 1e-3) / 1e12 / PEAK_INT8_TOPS, "traffic": None}
+
+    direct = None
+    if not args.no_direct:
+        wq, _ = W.direct_conv_quantize_weights(f)
+        wd = torch.from_numpy(wq).cuda()
+        bd = torch.from_numpy(np.asarray(bias, np.int32)).cuda()
+        yd = torch.empty_like(y)
+
+        def dstep():
+            W.direct_conv_int8(xd, wd, bd, yd, n, cin, cout, h, w, layout, 8, spec.relu)
+
+        for _ in range(max(2, args.warmup // 2)):
+            dstep()
+        dms = time_loop(torch, dstep, max(5, args.steps // 2))
+        direct = {"ms": dms, "TOPS": direct_ops / (dms * 1e-3) / 1e12, "speedup": dms / ms,
+                  "mfma_frac": direct_ops / (dms * 1e-3) / 1e12 / PEAK_INT8_TOPS}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import tapwise
+        oplan = tapwise.make_plan(f, eb, bias=bias, out_shift=out_shift, relu=spec.relu)
+        per_img = 2.0 * 9 * h * w * cin * cout
+        n_img = args.cpu_images or max(1, min(n, int(round(1.0e11 / per_img))))
+        cpu = cpu_baseline(x, oplan, n_img, spec)
+
+    if args.copy_probe:
+        src = torch.empty(256 << 20, dtype=torch.int8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
+    line = {
+        "metric": METRIC, "value": value, "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "int8", "data": "synthetic",
+        "config": {"workload": f"{args.config}: {wl.desc}", "n": n, "cin": cin, "cout": cout, "h": h, "w": w,
+                   "layout": args.layout, "variant": args.variant, "tiles": T,
+                   "e_b": eb, "e_g": info["e_g"], "out_shift": out_shift,
+                   "epilogue_bits": info["epilogue_bits"]},
+        "roofline": roofline,
+        "kernels": kernels,
+        "tap_gemm_mfma_frac_of_step": tap_ops / (ms * 1e-3) / 1e12 / PEAK_INT8_TOPS,
+        "direct_conv": direct,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -156,6 +156,23 @@ wino_status wino_f4_conv_int8(wino_f4_plan_t plan, const int8_t* x, int8_t* y, i
                               void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * The two launches of the SPLIT variant as separate calls, for callers that
+ * schedule or time them individually; wino_f4_conv_int8(SPLIT) equals
+ * wino_f4_input_transform followed by wino_f4_tap_gemm on the same stream.
+ * wino_f4_input_transform: x -> workspace (Vq, the tap-major int8
+ *   Winograd-domain input: B^T d B and the tap-wise requantization).
+ * wino_f4_tap_gemm: workspace -> y (the 36 tap GEMMs, alignment, A^T M A,
+ *   bias, requantization, ReLU, store).  `workspace` must hold the Vq
+ *   written by wino_f4_input_transform for the same plan, n, h, w.
+ * Arguments, errors and stream semantics as for wino_f4_conv_int8.
+ */
+wino_status wino_f4_input_transform(wino_f4_plan_t plan, const int8_t* x, int32_t n, int32_t h, int32_t w,
+                                    wino_layout layout, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream);
+wino_status wino_f4_tap_gemm(wino_f4_plan_t plan, const void* workspace, size_t workspace_bytes, int8_t* y,
+                             int32_t n, int32_t h, int32_t w, wino_layout layout, hipStream_t stream);
+
+/*
  * wino_f4_calibrate_input -- max-abs calibration of the input tap scales
  * (Sec. III: x_max calibrated from observed maxima; power-of-two rule of
  * Sec. III-B).  Computes absmax[t] = max over all tiles and channels of

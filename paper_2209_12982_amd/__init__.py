@@ -11,6 +11,7 @@ from .binding import (  # noqa: F401
     LibraryNotBuilt, WinoError, WinoF4Plan,
     library_path, load_library, exported_symbols,
     wino_f4_plan, wino_f4_plan_tables, wino_f4_plan_info, wino_f4_workspace_bytes, wino_f4_conv_int8,
+    wino_f4_input_transform, wino_f4_tap_gemm,
     wino_f4_calibrate_input, wino_f4_calibrate_output,
     wino_f4_debug_input_transform, wino_f4_debug_tap_gemm,
     direct_conv_quantize_weights, direct_conv_int8, wino_strerror,

@@ -16,7 +16,7 @@ _LIB = None
 
 EXPORTS = [
     "wino_f4_plan", "wino_f4_plan_tables", "wino_f4_plan_destroy", "wino_f4_plan_info", "wino_f4_workspace_bytes",
-    "wino_f4_conv_int8", "wino_f4_calibrate_input", "wino_f4_calibrate_output",
+    "wino_f4_conv_int8", "wino_f4_input_transform", "wino_f4_tap_gemm", "wino_f4_calibrate_input", "wino_f4_calibrate_output",
     "wino_f4_debug_input_transform", "wino_f4_debug_tap_gemm",
     "direct_conv_quantize_weights", "direct_conv_int8", "wino_strerror",
 ]
@@ -53,6 +53,8 @@ def load_library():
         "wino_f4_plan_info": (I32, [P, P, P, P, P, P, P, P]),
         "wino_f4_workspace_bytes": (SZ, [P, I32, I32, I32, I32]),
         "wino_f4_conv_int8": (I32, [P, P, P, I32, I32, I32, I32, I32, P, SZ, P]),
+        "wino_f4_input_transform": (I32, [P, P, I32, I32, I32, I32, P, SZ, P]),
+        "wino_f4_tap_gemm": (I32, [P, P, SZ, P, I32, I32, I32, I32, P]),
         "wino_f4_calibrate_input": (I32, [P, I32, I32, I32, I32, I32, P, P, P]),
         "wino_f4_calibrate_output": (I32, [P, P, I32, I32, I32, I32, P, SZ, P, P, P]),
         "wino_f4_debug_input_transform": (I32, [P, P, I32, I32, I32, I32, P, P, SZ, P]),
@@ -194,6 +196,20 @@ def wino_f4_conv_int8(plan, x, y, n, h, w, layout=NCHW, variant=SPLIT, workspace
     st = lib.wino_f4_conv_int8(plan.handle, _ptr(x), _ptr(y), n, h, w, layout, variant,
                                _ptr(workspace), ws_bytes, _stream(stream))
     _check(st, "wino_f4_conv_int8")
+
+
+def wino_f4_input_transform(plan, x, n, h, w, layout, workspace, stream=None):
+    lib = load_library()
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib.wino_f4_input_transform(plan.handle, _ptr(x), n, h, w, layout, _ptr(workspace), ws_bytes,
+                                       _stream(stream)), "wino_f4_input_transform")
+
+
+def wino_f4_tap_gemm(plan, workspace, y, n, h, w, layout, stream=None):
+    lib = load_library()
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib.wino_f4_tap_gemm(plan.handle, _ptr(workspace), ws_bytes, _ptr(y), n, h, w, layout,
+                                _stream(stream)), "wino_f4_tap_gemm")
 
 
 def wino_f4_calibrate_input(x, n, cin, h, w, layout=NCHW, stream=None):

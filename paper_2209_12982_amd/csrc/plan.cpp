@@ -282,13 +282,15 @@ extern "C" wino_status wino_f4_plan(wino_f4_plan_t* out, const float* w_oihw, in
         delete p;
         return st;
     }
-    // device upload: Uq as [36][cout_pad][cin_pad] (GEMM A operand rows =
-    // output channels, k = input channels contiguous), bias [cout_pad]
+    // device upload: Uq k-blocked as [36][cin_pad/64][cout_pad][64] (GEMM A
+    // operand: rows = output channels, 64 input channels contiguous per row,
+    // so one k step of one tap is a single contiguous block), bias [cout_pad]
     std::vector<int8_t> dev_layout((size_t)kTaps * p->cout_pad * p->cin_pad, 0);
+    const int nkb = p->cin_pad / kKStep;
     for (int t = 0; t < kTaps; ++t)
         for (int ci = 0; ci < cin; ++ci)
             for (int co = 0; co < cout; ++co)
-                dev_layout[((size_t)t * p->cout_pad + co) * p->cin_pad + ci] =
+                dev_layout[(((size_t)t * nkb + ci / kKStep) * p->cout_pad + co) * kKStep + ci % kKStep] =
                     p->uq_host[((size_t)t * cin + ci) * cout + co];
     std::vector<int32_t> bias_pad(p->cout_pad, 0);
     for (int co = 0; co < cout; ++co) bias_pad[co] = p->bias_host[co];

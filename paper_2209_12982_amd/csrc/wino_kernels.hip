@@ -6,7 +6,9 @@
 //                         separable row-by-row form of Eq. general_wino_xform
 //                         with shared subexpressions, Sec. IV-B1), tap-wise
 //                         requantization R(V / 2^e_B) clamped to int8, and a
-//                         tap-major scatter Vq[36][tiles][Cin].
+//                         tap-major scatter into Vq[36][Cin/64][tiles][64]
+//                         (k-blocked: 64 input channels contiguous per tile,
+//                         the "fractal" C1/C0 split of Sec. IV-A).
 //   K2 wino_tap_gemm      36 int8 GEMMs M_t = Uq_t * Vq_t on MFMA with int32
 //                         accumulation; the epilogue aligns taps by 2^sh,
 //                         applies Y = A^T M A, adds bias, requantizes and
@@ -20,6 +22,7 @@
 // GEMM sums |Vq Uq| <= 2^14 per input channel in int32.  The output transform
 // runs in 32-bit integers when the plan's bound proves every partial sum fits,
 // otherwise in 64-bit.
+#include <algorithm>
 #include <type_traits>
 #include "winof4_internal.h"
 
@@ -179,7 +182,8 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
     if (MODE == 0) {
         if (!valid) return;
         const long long tile = (long long)row * g.tw + tx;
-        uint32_t* dst = (uint32_t*)(vq + tile * g.cin_pad + ci0) + q;
+        // Vq[t][cgi][tile][64]: this block's 64 channels are k block cgi
+        uint32_t* dst = (uint32_t*)(vq + ((long long)cgi * g.t_pad + tile) * K1_CG) + q;
         const long long plane = g.t_pad * g.cin_pad / 4;   // words per tap plane
 #pragma unroll
         for (int t = 0; t < kTaps; ++t) {
@@ -213,9 +217,29 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
 // ---------------------------------------------------------------------------
 // K2: tap GEMM with fused output transform
 // ---------------------------------------------------------------------------
-constexpr int K2_CO = 32;               // output channels per workgroup
+// Workgroup = 8 waves computing 64 output channels x 32 tiles for all 36
+// taps; wave w owns channels 16*(w%4).. and tiles 16*(w/4).. (one 16x16
+// int8 MFMA block per tap, 36 x 4 int32 accumulators per lane).  The k loop
+// runs over input channels in steps of 64; each step is split into six tap
+// groups ("stages").  A stage's Uq slice (6 taps x 64 rows x 64 B) and Vq
+// slice (6 taps x 32 rows x 64 B) are copied global -> LDS by the
+// direct-to-LDS load (no VGPR staging) into a ring of four stage buffers, so
+// three stages are in flight while one feeds the MFMAs: enough bytes in
+// flight per CU to cover the L2 latency.  Every such load writes 1 KB of LDS
+// contiguously (16 bytes per lane); the 16-byte slot of a row holding input
+// bytes [16p, 16p+16) is p ^ ((row >> 1) & 3).  Measured on gfx950, this
+// swizzle lets the fragment reads (16 rows x one 16-byte part per 16 lanes)
+// run at the full 256 B/clk per CU; unswizzled or padded rows run 1.5x slower.
+constexpr int K2_CO = 64;               // output channels per workgroup
 constexpr int K2_TL = 32;               // tiles per workgroup
-constexpr int K2_THREADS = 256;         // 4 waves, each 16 channels x 16 tiles
+constexpr int K2_THREADS = 512;
+constexpr int K2_G = 6;                 // taps per stage
+constexpr int K2_A_BYTES = K2_G * K2_CO * 64;   // 24 KB
+constexpr int K2_B_BYTES = K2_G * K2_TL * 64;   // 12 KB
+constexpr int K2_STAGE = K2_A_BYTES + K2_B_BYTES;
+constexpr int K2_KB = K2_STAGE / 1024;          // 1-KB load instructions per stage (36)
+constexpr int K2_NBUF = 4;
+constexpr int K2_LPW = 5;                       // load instructions per wave per stage
 
 struct K2Args {
     int cin_pad, cout, cout_pad;
@@ -248,6 +272,22 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
     return (bid % nx) * (full / nx) + bid / nx;
 }
 
+__device__ __forceinline__ int k2_slot(int row, int part) { return part ^ ((row >> 1) & 3); }
+
+// Workgroup barrier without the implicit wait for outstanding global loads
+// that __syncthreads() carries: the caller waits for exactly the loads it
+// needs with s_waitcnt.  The empty asm statements keep the compiler from
+// moving LDS accesses across the barrier.
+__device__ __forceinline__ void k2_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// s_waitcnt vmcnt(n) leaving the other counters untouched (gfx9 encoding:
+// vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8]).
+#define K2_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(0x0f70 | (n))
+
 // MODE 0: store y.  MODE 1: max |Y + bias| into *zmax (calibration).
 // MODE 2: store raw M (debug export).
 template <int LAYOUT, int EPI, int MODE>
@@ -257,34 +297,86 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
                                                             int8_t* __restrict__ y,
                                                             void* __restrict__ aux, K2Args g) {
     typedef typename std::conditional<EPI == 64, long long, int>::type acc_t;
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[K2_NBUF * K2_STAGE];
     const int lbid = xcd_remap(blockIdx.x, g.nblocks);
     const int bco = lbid % g.nbco, btl = lbid / g.nbco;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int co_base = bco * K2_CO + 16 * (wave & 1);
-    const long long tl_base = (long long)btl * K2_TL + 16 * (wave >> 1);
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6, lane = tid & 63;
+    const int cw = wave & 3, tw = wave >> 2;
+    const int co_blk = bco * K2_CO;
+    const long long tl_blk = (long long)btl * K2_TL;
+    const int co_base = co_blk + 16 * cw;
+    const long long tl_base = tl_blk + 16 * tw;
     const int lr = lane & 15, lk = lane >> 4;
-
-    const int8_t* pa = uq + (long long)(co_base + lr) * g.cin_pad + 16 * lk;
-    const int8_t* pb = vq + (tl_base + lr) * g.cin_pad + 16 * lk;
+    // k-blocked operands: Uq[36][cin_pad/64][cout_pad][64], Vq[36][cin_pad/64][t_pad][64]
     const long long sa = (long long)g.cout_pad * g.cin_pad;   // tap stride of Uq
     const long long sb = g.t_pad * g.cin_pad;                  // tap stride of Vq
+    const long long ka = (long long)g.cout_pad * kKStep;      // k-block stride of Uq
+    const long long kb = g.t_pad * kKStep;                     // k-block stride of Vq
+
+    // This wave's five 1-KB load instructions of a stage: global source of
+    // this lane (stage 0) and LDS destination offset within a stage buffer.
+    // Waves 4..7 have only four distinct ones; their fifth repeats the
+    // fourth (same bytes to the same place).
+    const int8_t* src[K2_LPW];
+    int dst[K2_LPW];
+#pragma unroll
+    for (int i = 0; i < K2_LPW; ++i) {
+        int j = wave + 8 * i;
+        if (j >= K2_KB) j -= 8;
+        const int rr = lane >> 2, slot = lane & 3;
+        if (j < K2_A_BYTES / 1024) {
+            const int u = j >> 2, row = 16 * (j & 3) + rr;
+            src[i] = uq + u * sa + (long long)(co_blk + row) * kKStep + 16 * k2_slot(row, slot);
+        } else {
+            const int jj = j - K2_A_BYTES / 1024;
+            const int u = jj >> 1, row = 16 * (jj & 1) + rr;
+            src[i] = vq + u * sb + (tl_blk + row) * kKStep + 16 * k2_slot(row, slot);
+        }
+        dst[i] = j * 1024;
+    }
+    const int nkc = g.cin_pad / kKStep;
+    const int nstage = nkc * (kTaps / K2_G);
+    auto issue = [&](int st) {
+        const int kc = st / (kTaps / K2_G), grp = st - kc * (kTaps / K2_G);
+        uint8_t* base = lds + (st & (K2_NBUF - 1)) * K2_STAGE;
+#pragma unroll
+        for (int i = 0; i < K2_LPW; ++i) {
+            const bool is_a = dst[i] < K2_A_BYTES;
+            const long long off = (long long)(K2_G * grp) * (is_a ? sa : sb) + kc * (is_a ? ka : kb);
+            __builtin_amdgcn_global_load_lds((const void*)(src[i] + off),
+                                             (__attribute__((address_space(3))) void*)(base + dst[i]), 16, 0, 0);
+        }
+    };
 
     v4i acc[kTaps];
 #pragma unroll
     for (int t = 0; t < kTaps; ++t) acc[t] = (v4i){0, 0, 0, 0};
 
-    for (int k0 = 0; k0 < g.cin_pad; k0 += kKStep) {
+    // fragment offsets within a stage buffer (tap u adds u * rows * 64)
+    const int row_a = 16 * cw + lr, row_b = 16 * tw + lr;
+    const int frag_a = row_a * 64 + 16 * k2_slot(row_a, lk);
+    const int frag_b = K2_A_BYTES + row_b * 64 + 16 * k2_slot(row_b, lk);
+
+    for (int st = 0; st < K2_NBUF - 1 && st < nstage; ++st) issue(st);
+    for (int kc = 0; kc < nkc; ++kc) {
 #pragma unroll
-        for (int t0 = 0; t0 < kTaps; t0 += 6) {
-            v4i av[6], bv[6];
+        for (int grp = 0; grp < kTaps / K2_G; ++grp) {
+            const int st = kc * (kTaps / K2_G) + grp;
+            const int ahead = nstage - 1 - st;        // stages issued after this one
+            if (ahead >= 2) K2_WAIT_VM(2 * K2_LPW);
+            else if (ahead == 1) K2_WAIT_VM(K2_LPW);
+            else K2_WAIT_VM(0);
+            k2_barrier();                              // stage st visible; stage st-1 consumed
+            if (st + K2_NBUF - 1 < nstage) issue(st + K2_NBUF - 1);
+            const uint8_t* base = lds + (st & (K2_NBUF - 1)) * K2_STAGE;
 #pragma unroll
-            for (int u = 0; u < 6; ++u) {
-                av[u] = *(const v4i*)(pa + (t0 + u) * sa + k0);
-                bv[u] = *(const v4i*)(pb + (t0 + u) * sb + k0);
+            for (int u = 0; u < K2_G; ++u) {
+                v4i av = *(const v4i*)(base + frag_a + u * K2_CO * 64);
+                v4i bv = *(const v4i*)(base + frag_b + u * K2_TL * 64);
+                acc[K2_G * grp + u] =
+                    __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bv, acc[K2_G * grp + u], 0, 0, 0);
             }
-#pragma unroll
-            for (int u = 0; u < 6; ++u)
-                acc[t0 + u] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av[u], bv[u], acc[t0 + u], 0, 0, 0);
         }
     }
 
@@ -568,6 +660,28 @@ extern "C" wino_status wino_f4_conv_int8(wino_f4_plan_t p, const int8_t* x, int8
     return launch_k2<0>(p, g, layout, vq, y, nullptr, stream);
 }
 
+extern "C" wino_status wino_f4_input_transform(wino_f4_plan_t p, const int8_t* x, int32_t n, int32_t h,
+                                               int32_t w, wino_layout layout, void* ws, size_t ws_bytes,
+                                               hipStream_t stream) {
+    Geometry g;
+    wino_status st = check_common(p, x, n, h, w, layout, g);
+    if (st != WINO_OK) return st;
+    if (g.ntiles == 0) return WINO_OK;
+    if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
+    return launch_k1<0>(k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
+}
+
+extern "C" wino_status wino_f4_tap_gemm(wino_f4_plan_t p, const void* ws, size_t ws_bytes, int8_t* y, int32_t n,
+                                        int32_t h, int32_t w, wino_layout layout, hipStream_t stream) {
+    Geometry g;
+    wino_status st = check_common(p, ws, n, h, w, layout, g);
+    if (st != WINO_OK) return st;
+    if (!y) return WINO_EINVAL;
+    if (g.ntiles == 0) return WINO_OK;
+    if (ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
+    return launch_k2<0>(p, g, layout, (const int8_t*)ws, y, nullptr, stream);
+}
+
 extern "C" wino_status wino_f4_calibrate_input(const int8_t* x, int32_t n, int32_t cin, int32_t h, int32_t w,
                                                wino_layout layout, int32_t* absmax, int8_t* e_b,
                                                hipStream_t stream) {
@@ -636,12 +750,18 @@ extern "C" wino_status wino_f4_debug_input_transform(wino_f4_plan_t p, const int
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
     st = launch_k1<0>(k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
     if (st != WINO_OK) return st;
-    // compact [36][t_pad][cin_pad] -> [36][ntiles][cin], one 2-D copy per tap plane
+    // compact [36][cin_pad/64][t_pad][64] -> [36][ntiles][cin], one 2-D copy
+    // per (tap, k block)
+    const int nkb = p->cin_pad / kKStep;
     for (int t = 0; t < kTaps; ++t)
-        if (hipMemcpy2DAsync(vq_out + (size_t)t * g.ntiles * p->cin, (size_t)p->cin,
-                             (const int8_t*)ws + (size_t)t * g.t_pad * p->cin_pad, (size_t)p->cin_pad,
-                             (size_t)p->cin, (size_t)g.ntiles, hipMemcpyDeviceToDevice, stream) != hipSuccess)
-            return WINO_EHIP;
+        for (int b = 0; b < nkb; ++b) {
+            const int width = std::min(kKStep, p->cin - b * kKStep);
+            if (width <= 0) break;
+            if (hipMemcpy2DAsync(vq_out + (size_t)t * g.ntiles * p->cin + (size_t)b * kKStep, (size_t)p->cin,
+                                 (const int8_t*)ws + ((size_t)t * nkb + b) * g.t_pad * kKStep, (size_t)kKStep,
+                                 (size_t)width, (size_t)g.ntiles, hipMemcpyDeviceToDevice, stream) != hipSuccess)
+                return WINO_EHIP;
+        }
     return WINO_OK;
 }
 

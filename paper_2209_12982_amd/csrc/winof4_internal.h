@@ -3,7 +3,7 @@
 #include <stdint.h>
 #include <vector>
 #include <hip/hip_runtime.h>
-#include "../../include/winof4.h"
+#include "winof4.h"
 
 namespace winof4 {
 
@@ -33,7 +33,7 @@ struct wino_f4_plan_s {
     int32_t out_shift, relu;
     int32_t epi_bits;                 // 32 or 64
     int32_t device;
-    int8_t* uq_dev;                   // [36][cout_pad][cin_pad], zero padded
+    int8_t* uq_dev;                   // [36][cin_pad/64][cout_pad][64], zero padded
     int32_t* bias_dev;                // [cout_pad], zero padded
     std::vector<int8_t> uq_host;      // [36][cin][cout]
     std::vector<int32_t> bias_host;   // [cout]
