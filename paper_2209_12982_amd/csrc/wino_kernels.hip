@@ -464,8 +464,8 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
             for (int i = 0; i < 4; ++i) {
                 if (4 * ty + i >= g.h) continue;
                 if (full_cols) {
-                    uint32_t wv = (uint32_t)(qv[i][0] & 255) | ((uint32_t)(qv[i][1] & 255) << 8) |
-                                  ((uint32_t)(qv[i][2] & 255) << 16) | ((uint32_t)(qv[i][3] & 255) << 24);
+                    uint32_t wv = __builtin_amdgcn_perm((uint32_t)qv[i][1], (uint32_t)qv[i][0], 0x0c0c0400u) |
+                                  (__builtin_amdgcn_perm((uint32_t)qv[i][3], (uint32_t)qv[i][2], 0x0c0c0400u) << 16);
                     *(uint32_t*)(base + (long long)i * g.w) = wv;
                 } else {
 #pragma unroll
@@ -492,21 +492,22 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
     }
     if (LAYOUT == WINO_NHWC && tile_ok) {
         const int co0 = co_base + 4 * lk;
-        const bool full = (co0 + 3 < g.cout) && ((g.cout & 3) == 0);
+        const long long rs = (long long)g.w * g.cout;
+        int8_t* ob = y + (((long long)img * g.h + 4 * ty) * g.w + 4 * tx) * g.cout + co0;
+        const bool full = (co0 + 3 < g.cout) && ((g.cout & 3) == 0) && (4 * ty + 3 < g.h) && (4 * tx + 3 < g.w);
+        if (full) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-                const int hh = 4 * ty + i, ww = 4 * tx + jj;
-                if (hh >= g.h || ww >= g.w) continue;
-                int8_t* dst = y + (((long long)img * g.h + hh) * g.w + ww) * g.cout + co0;
-                if (full) {
-                    *(uint32_t*)dst = packed[4 * i + jj];
-                } else {
+                for (int jj = 0; jj < 4; ++jj) *(uint32_t*)(ob + i * rs + jj * g.cout) = packed[4 * i + jj];
+        } else {
+            for (int i = 0; i < 4; ++i)
+                for (int jj = 0; jj < 4; ++jj) {
+                    if (4 * ty + i >= g.h || 4 * tx + jj >= g.w) continue;
                     for (int r = 0; r < 4; ++r)
-                        if (co0 + r < g.cout) dst[r] = (int8_t)(packed[4 * i + jj] >> (8 * r));
+                        if (co0 + r < g.cout) ob[i * rs + jj * g.cout + r] = (int8_t)(packed[4 * i + jj] >> (8 * r));
                 }
-            }
+        }
     }
 }
 

@@ -129,7 +129,9 @@ def test_calibrate_output_matches_oracle(layout):
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
-@pytest.mark.parametrize("shape", [(1, 16, 16, 32, 32), (2, 3, 5, 7, 9), (1, 70, 130, 9, 14)])
+@pytest.mark.parametrize("shape", [(1, 16, 16, 32, 32), (2, 3, 5, 7, 9), (1, 70, 130, 9, 14),
+                                   (2, 64, 130, 9, 14), (1, 128, 64, 17, 23), (3, 192, 40, 5, 7),
+                                   (1, 64, 256, 1, 1), (2, 256, 128, 16, 16)])
 def test_direct_conv_bitexact(shape, layout):
     torch = torch_dev()
     n, cin, cout, h, w = shape
