@@ -1,0 +1,68 @@
+"""GPU parity at the full configuration sizes: the HIP path's calibration,
+plan tables and every output byte (by SHA-256 of the NCHW int8 output, plus
+sampled values for diagnosis) against the oracle's results stored in
+tests/golden/configs.json, which tests/golden/make_golden.py writes from the
+oracle alone."""
+import hashlib
+import json
+import os
+
+import numpy as np
+import pytest
+
+import paper_2209_12982_amd as W
+import workloads
+
+from gpu_util import from_device_nchw, to_device, torch_dev, workspace
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "configs.json")))
+
+
+def _run_layer(x, f, b, spec, rec, layout, variant=W.SPLIT):
+    torch = torch_dev()
+    n, cin, h, w = x.shape
+    xd = to_device(x, layout)
+    eb, amax = W.wino_f4_calibrate_input(xd, n, cin, h, w, layout)
+    assert eb == rec["e_b"], "input tap exponents differ from the oracle"
+    plan0 = W.wino_f4_plan(f, eb, bias=b, out_shift=0, relu=spec.relu)
+    info0 = W.wino_f4_plan_info(plan0)
+    assert info0["e_g"] == rec["e_g"] and info0["sh"] == rec["sh"] and info0["e_o"] == rec["e_o"]
+    if spec.out_shift is None:
+        s, zmax = W.wino_f4_calibrate_output(plan0, xd, n, h, w, layout, workspace(plan0, n, h, w))
+        assert zmax == rec["zmax"] and s == rec["out_shift"]
+    else:
+        s = spec.out_shift
+    plan = W.wino_f4_plan(f, eb, bias=b, out_shift=s, relu=spec.relu)
+    shape = (n, spec.cout, h, w) if layout == W.NCHW else (n, h, w, spec.cout)
+    y = torch.full(shape, 77, dtype=torch.int8, device="cuda")
+    ws = workspace(plan, n, h, w, variant) if variant == W.SPLIT else None
+    W.wino_f4_conv_int8(plan, xd, y, n, h, w, layout, variant, ws)
+    torch.cuda.synchronize()
+    yn = from_device_nchw(y, layout)
+    for idx, v in rec["samples"]:
+        assert int(yn[tuple(idx)]) == v, f"sample {idx}: {int(yn[tuple(idx)])} != {v}"
+    assert hashlib.sha256(yn.tobytes()).hexdigest() == rec["sha256_nchw"]
+    return yn
+
+
+@pytest.mark.parametrize("layout", [W.NHWC, W.NCHW])
+@pytest.mark.parametrize("name", ["C4", "C5"])
+def test_full_size_layer_bitexact(name, layout):
+    x, layers = workloads.generate(name)
+    f, b, spec = layers[0]
+    _run_layer(x, f, b, spec, GOLDEN[name]["layers"][0], layout)
+
+
+@pytest.mark.parametrize("layout", [W.NHWC, W.NCHW])
+def test_c3_chain_bitexact(layout):
+    """Four chained layers; each layer's input is the GPU's own previous
+    output (max-pooled where the stage halves the image), and every layer
+    must match the oracle's chain byte for byte."""
+    x, layers = workloads.generate("C3")
+    cur = x
+    for k, (f, b, spec) in enumerate(layers):
+        if k > 0:
+            cur = workloads.next_layer_input(cur, spec)
+        cur = _run_layer(cur, f, b, spec, GOLDEN["C3"]["layers"][k], layout)

@@ -117,6 +117,21 @@ def generate(name, n=None, seed=None):
     return x, layers
 
 
+def next_layer_input(y_prev, spec_next):
+    """Input of the next layer of a chain from the previous layer's int8
+    NCHW output.  Where the next layer's image is half the size (a new
+    network stage) the activations are max-pooled 2x2 with stride 2; the
+    configuration names the stage sizes but not the downsampling, and
+    max-pooling is exact on int8 and keeps the ReLU-like distribution."""
+    n, c, h, w = y_prev.shape
+    assert c == spec_next.cin, (c, spec_next.cin)
+    if (h, w) == (spec_next.h, spec_next.w):
+        return np.ascontiguousarray(y_prev)
+    assert (h // 2, w // 2) == (spec_next.h, spec_next.w) and h % 2 == 0 and w % 2 == 0
+    v = y_prev.reshape(n, c, h // 2, 2, w // 2, 2)
+    return np.ascontiguousarray(v.max(axis=(3, 5)))
+
+
 def random_case(seed, n, cin, cout, h, w, signed=True, zero_frac=0.0, wscale=None):
     """A generic random layer for parity sweeps: full-range int8 (or
     non-negative) activations, normal weights, bias U[-64, 64]."""
