@@ -123,6 +123,16 @@ __device__ __forceinline__ void k1_stage_band(uint32_t* lds, const int8_t* __res
     }
 }
 
+// Consecutive workgroup ids are dispatched round robin over the 8 XCDs
+// (workgroup i runs on XCD i % 8); this maps them to logical ids so that each
+// XCD works through one contiguous range of logical blocks.
+__device__ __forceinline__ int k1_xcd_remap(int bid, int nblocks) {
+    const int nx = 8;
+    const int full = nblocks / nx * nx;
+    if (bid >= full) return bid;
+    return (bid % nx) * (full / nx) + bid / nx;
+}
+
 // MODE 0: write Vq.  MODE 1: per-tap max |V| into tapmax[36] (calibration).
 template <int LAYOUT, int MODE>
 __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __restrict__ x,
@@ -130,11 +140,15 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
                                                                int* __restrict__ tapmax, K1Args g) {
     __shared__ uint32_t band[6 * K1_COLS * K1_CS];
     __shared__ int red[kTaps];
-    int bid = blockIdx.x;
-    const int txb = bid % g.ntxb;
-    bid /= g.ntxb;
+    // Logical block order: channel group fastest, then tile-column block,
+    // then tile row; consecutive logical ids are kept on one XCD (its L2),
+    // so the channel groups sharing each 128-byte line of an NHWC pixel and
+    // the tile rows sharing halo rows are read by concurrent workgroups.
+    int bid = k1_xcd_remap((int)blockIdx.x, (int)gridDim.x);
     const int cgi = bid % g.ncg;
-    const int row = bid / g.ncg;          // img * th + ty
+    bid /= g.ncg;
+    const int txb = bid % g.ntxb;
+    const int row = bid / g.ntxb;         // img * th + ty
     const int img = row / g.th, ty = row - img * g.th;
     const int tx0 = txb * K1_TX, ci0 = cgi * K1_CG;
     if (MODE == 1 && threadIdx.x < kTaps) red[threadIdx.x] = 0;
@@ -224,22 +238,26 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
 // groups ("stages").  A stage's Uq slice (6 taps x 64 rows x 64 B) and Vq
 // slice (6 taps x 32 rows x 64 B) are copied global -> LDS by the
 // direct-to-LDS load (no VGPR staging) into a ring of four stage buffers, so
-// three stages are in flight while one feeds the MFMAs: enough bytes in
-// flight per CU to cover the L2 latency.  Every such load writes 1 KB of LDS
+// three stages are in flight while one feeds the MFMAs.  (Measured on
+// gfx950: two 4-wave workgroups per CU with 32x32 tiles and three-stage
+// rings were 1.4x slower -- more L2 traffic, shallower rings.)  Every such load writes 1 KB of LDS
 // contiguously (16 bytes per lane); the 16-byte slot of a row holding input
 // bytes [16p, 16p+16) is p ^ ((row >> 1) & 3).  Measured on gfx950, this
 // swizzle lets the fragment reads (16 rows x one 16-byte part per 16 lanes)
 // run at the full 256 B/clk per CU; unswizzled or padded rows run 1.5x slower.
 constexpr int K2_CO = 64;               // output channels per workgroup
 constexpr int K2_TL = 32;               // tiles per workgroup
-constexpr int K2_THREADS = 512;
+constexpr int K2_THREADS = 512;         // waves: (K2_CO/16) x (K2_TL/16), each 16x16
+constexpr int K2_WAVES = K2_THREADS / 64;
 constexpr int K2_G = 6;                 // taps per stage
-constexpr int K2_A_BYTES = K2_G * K2_CO * 64;   // 24 KB
-constexpr int K2_B_BYTES = K2_G * K2_TL * 64;   // 12 KB
+constexpr int K2_A_BYTES = K2_G * K2_CO * 64;
+constexpr int K2_B_BYTES = K2_G * K2_TL * 64;
 constexpr int K2_STAGE = K2_A_BYTES + K2_B_BYTES;
-constexpr int K2_KB = K2_STAGE / 1024;          // 1-KB load instructions per stage (36)
-constexpr int K2_NBUF = 4;
-constexpr int K2_LPW = 5;                       // load instructions per wave per stage
+constexpr int K2_KB = K2_STAGE / 1024;          // 1-KB load instructions per stage
+constexpr int K2_NBUF = 4;                      // ring depth (3 stages in flight)
+constexpr int K2_LPW = (K2_KB + K2_WAVES - 1) / K2_WAVES;   // load instructions per wave per stage
+static_assert((K2_CO / 16) * (K2_TL / 16) == K2_WAVES, "one 16x16 block per wave");
+static_assert(K2_NBUF * K2_STAGE <= 160 * 1024, "LDS");
 
 struct K2Args {
     int cin_pad, cout, cout_pad;
@@ -302,7 +320,7 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
     const int bco = lbid % g.nbco, btl = lbid / g.nbco;
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
-    const int cw = wave & 3, tw = wave >> 2;
+    const int cw = wave % (K2_CO / 16), tw = wave / (K2_CO / 16);
     const int co_blk = bco * K2_CO;
     const long long tl_blk = (long long)btl * K2_TL;
     const int co_base = co_blk + 16 * cw;
@@ -314,23 +332,23 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
     const long long ka = (long long)g.cout_pad * kKStep;      // k-block stride of Uq
     const long long kb = g.t_pad * kKStep;                     // k-block stride of Vq
 
-    // This wave's five 1-KB load instructions of a stage: global source of
-    // this lane (stage 0) and LDS destination offset within a stage buffer.
-    // Waves 4..7 have only four distinct ones; their fifth repeats the
-    // fourth (same bytes to the same place).
+    // This wave's 1-KB load instructions of a stage: global source of this
+    // lane (stage 0) and LDS destination offset within a stage buffer.
     const int8_t* src[K2_LPW];
     int dst[K2_LPW];
 #pragma unroll
     for (int i = 0; i < K2_LPW; ++i) {
-        int j = wave + 8 * i;
-        if (j >= K2_KB) j -= 8;
+        // when the stage's loads do not split evenly, the last round repeats
+        // an earlier load (same bytes to the same place)
+        int j = wave + K2_WAVES * i;
+        if (j >= K2_KB) j -= K2_WAVES;
         const int rr = lane >> 2, slot = lane & 3;
         if (j < K2_A_BYTES / 1024) {
-            const int u = j >> 2, row = 16 * (j & 3) + rr;
+            const int u = j / (K2_CO / 16), row = 16 * (j % (K2_CO / 16)) + rr;
             src[i] = uq + u * sa + (long long)(co_blk + row) * kKStep + 16 * k2_slot(row, slot);
         } else {
             const int jj = j - K2_A_BYTES / 1024;
-            const int u = jj >> 1, row = 16 * (jj & 1) + rr;
+            const int u = jj / (K2_TL / 16), row = 16 * (jj % (K2_TL / 16)) + rr;
             src[i] = vq + u * sb + (tl_blk + row) * kKStep + 16 * k2_slot(row, slot);
         }
         dst[i] = j * 1024;
@@ -339,13 +357,19 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
     const int nstage = nkc * (kTaps / K2_G);
     auto issue = [&](int st) {
         const int kc = st / (kTaps / K2_G), grp = st - kc * (kTaps / K2_G);
-        uint8_t* base = lds + (st & (K2_NBUF - 1)) * K2_STAGE;
+        uint8_t* base = lds + (st % K2_NBUF) * K2_STAGE;
 #pragma unroll
         for (int i = 0; i < K2_LPW; ++i) {
             const bool is_a = dst[i] < K2_A_BYTES;
             const long long off = (long long)(K2_G * grp) * (is_a ? sa : sb) + kc * (is_a ? ka : kb);
-            __builtin_amdgcn_global_load_lds((const void*)(src[i] + off),
-                                             (__attribute__((address_space(3))) void*)(base + dst[i]), 16, 0, 0);
+            // Vq is streamed once per output-channel block: non-temporal, so it
+            // does not push the small, hot Uq out of L2
+            if (is_a)
+                __builtin_amdgcn_global_load_lds((const void*)(src[i] + off),
+                                                 (__attribute__((address_space(3))) void*)(base + dst[i]), 16, 0, 0);
+            else
+                __builtin_amdgcn_global_load_lds((const void*)(src[i] + off),
+                                                 (__attribute__((address_space(3))) void*)(base + dst[i]), 16, 0, 2);
         }
     };
 
@@ -364,12 +388,13 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
         for (int grp = 0; grp < kTaps / K2_G; ++grp) {
             const int st = kc * (kTaps / K2_G) + grp;
             const int ahead = nstage - 1 - st;        // stages issued after this one
+            static_assert(K2_NBUF == 4 && 2 * K2_LPW <= 15, "wait counts below assume two stages ahead");
             if (ahead >= 2) K2_WAIT_VM(2 * K2_LPW);
             else if (ahead == 1) K2_WAIT_VM(K2_LPW);
             else K2_WAIT_VM(0);
             k2_barrier();                              // stage st visible; stage st-1 consumed
             if (st + K2_NBUF - 1 < nstage) issue(st + K2_NBUF - 1);
-            const uint8_t* base = lds + (st & (K2_NBUF - 1)) * K2_STAGE;
+            const uint8_t* base = lds + (st % K2_NBUF) * K2_STAGE;
 #pragma unroll
             for (int u = 0; u < K2_G; ++u) {
                 v4i av = *(const v4i*)(base + frag_a + u * K2_CO * 64);
