@@ -1,0 +1,287 @@
+// Device code shared by the input-transform, tap-GEMM and fused kernels:
+// the F(4x4,3x3) transforms of Sec. II in integer form, the tap-wise
+// requantization of Sec. III, the fused output-transform epilogue, and the
+// LDS / barrier / wait helpers of the operand rings.
+#pragma once
+#include <type_traits>
+#include "winof4_internal.h"
+
+namespace winof4 {
+
+typedef short v2s __attribute__((ext_vector_type(2)));
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ v2s splat(int v) { return (v2s){(short)v, (short)v}; }
+
+// sign-extended bytes 0 and 2 of w as two 16-bit lanes
+__device__ __forceinline__ v2s lanes_even(uint32_t w) {
+    return __builtin_bit_cast(v2s, __builtin_amdgcn_perm(0u, w, 0x020c000cu)) >> splat(8);
+}
+// sign-extended bytes 1 and 3 of w
+__device__ __forceinline__ v2s lanes_odd(uint32_t w) { return __builtin_bit_cast(v2s, w) >> splat(8); }
+
+// One-dimensional B^T transform of a 6-vector, twelve additions with shared
+// subexpressions; the rows of B^T (Sec. II) are
+//   4 0 -5 0 1 0 / 0 -4 -4 1 1 0 / 0 4 -4 -1 1 0 / 0 -2 -1 2 1 0 /
+//   0 2 -1 -2 1 0 / 0 4 0 -5 0 1.
+template <class T>
+__device__ __forceinline__ void bt_1d(const T* v, T* r, T two, T four) {
+    T a = v[4] - four * v[2];
+    T b = four * v[1] - v[3];
+    T c = v[4] - v[2];
+    T d = v[1] - v[3];
+    T e = v[0] - v[2];
+    T f = v[5] - v[3];
+    r[0] = four * e + c;
+    r[1] = a - b;
+    r[2] = a + b;
+    r[3] = c - two * d;
+    r[4] = c + two * d;
+    r[5] = four * d + f;
+}
+
+// V = B^T d B for four channels of one 6x6 tile.  wv[r][c] holds the int8
+// values of the four channels at tile pixel (r, c), channel k in byte k.
+// On return ev[r][c] holds V[r][c] of channels (0, 2) and od[r][c] of
+// channels (1, 3), as 16-bit lanes: |V| <= 12768 for int8 inputs and the
+// row-pass intermediates are at most 1278, so 16 bits hold everything.
+__device__ __forceinline__ void input_tile_transform(const uint32_t (&wv)[6][6], v2s (&ev)[6][6],
+                                                     v2s (&od)[6][6]) {
+#pragma unroll
+    for (int r = 0; r < 6; ++r)
+#pragma unroll
+        for (int c = 0; c < 6; ++c) {
+            ev[r][c] = lanes_even(wv[r][c]);
+            od[r][c] = lanes_odd(wv[r][c]);
+        }
+    const v2s two = splat(2), four = splat(4);
+    // columns: T1 = B^T d
+#pragma unroll
+    for (int c = 0; c < 6; ++c) {
+        v2s ve[6], vo[6], re[6], ro[6];
+#pragma unroll
+        for (int r = 0; r < 6; ++r) {
+            ve[r] = ev[r][c];
+            vo[r] = od[r][c];
+        }
+        bt_1d(ve, re, two, four);
+        bt_1d(vo, ro, two, four);
+#pragma unroll
+        for (int r = 0; r < 6; ++r) {
+            ev[r][c] = re[r];
+            od[r][c] = ro[r];
+        }
+    }
+    // rows: V = T1 B
+#pragma unroll
+    for (int r = 0; r < 6; ++r) {
+        v2s re[6], ro[6];
+        bt_1d(ev[r], re, two, four);
+        bt_1d(od[r], ro, two, four);
+#pragma unroll
+        for (int c = 0; c < 6; ++c) {
+            ev[r][c] = re[c];
+            od[r][c] = ro[c];
+        }
+    }
+}
+
+// Tap-wise requantization of tap t (Sec. III, power-of-two scale 2^e_B):
+// clamp(R(V / 2^e), -128, 127) with R(v) = floor(v + 1/2), for the four
+// channels, packed back into one word (channel k in byte k).
+__device__ __forceinline__ uint32_t requant_pack(v2s ev, v2s od, int e) {
+    const v2s rnd = splat(e ? (1 << (e - 1)) : 0);
+    const v2s sh = splat(e);
+    v2s a = (ev + rnd) >> sh;
+    v2s b = (od + rnd) >> sh;
+    a = __builtin_elementwise_min(__builtin_elementwise_max(a, splat(-128)), splat(127));
+    b = __builtin_elementwise_min(__builtin_elementwise_max(b, splat(-128)), splat(127));
+    // bytes: ch0 = a.lo, ch1 = b.lo, ch2 = a.hi, ch3 = b.hi
+    return __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, b), __builtin_bit_cast(uint32_t, a), 0x06020400u);
+}
+
+// One-dimensional A^T transform of a 6-vector (rows of A^T, Sec. II:
+// 1 1 1 1 1 0 / 0 1 -1 2 -2 0 / 0 1 1 4 4 0 / 0 1 -1 8 -8 1).
+template <class T>
+__device__ __forceinline__ void at_1d(const T* v, T* y) {
+    T p = v[1] + v[2], m = v[1] - v[2], q = v[3] + v[4], r = v[3] - v[4];
+    y[0] = v[0] + p + q;
+    y[1] = m + (r << 1);
+    y[2] = p + (q << 2);
+    y[3] = m + (r << 3) + v[5];
+}
+
+// Consecutive workgroup ids are dispatched round robin over the 8 XCDs
+// (workgroup i runs on XCD i % 8).  Remap so that each XCD works through one
+// contiguous range of logical block ids, i.e. blocks with neighbouring ids
+// share that XCD's L2.
+__device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
+    const int nx = 8;
+    const int full = nblocks / nx * nx;
+    if (bid >= full) return bid;
+    return (bid % nx) * (full / nx) + bid / nx;
+}
+
+// 16-byte slot holding bytes [16p, 16p+16) of a 64-byte LDS row.  Measured
+// on gfx950, this swizzle lets the MFMA fragment reads (16 rows x one 16-byte
+// part per 16 lanes) run at the full 256 B/clk per CU; unswizzled or padded
+// rows run 1.5x slower.
+__device__ __forceinline__ int lds_slot(int row, int part) { return part ^ ((row >> 1) & 3); }
+
+// Workgroup barrier without the implicit wait for outstanding global loads
+// that __syncthreads() carries: callers wait for exactly the loads they need
+// with s_waitcnt.  The empty asm statements keep the compiler from moving
+// LDS accesses across the barrier.
+__device__ __forceinline__ void ring_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// s_waitcnt vmcnt(n) leaving the other counters untouched (gfx9 encoding:
+// vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8]).
+#define WINO_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(0x0f70 | (n))
+
+// Epilogue of a 16-channel x 16-tile MFMA block holding all 36 taps: the
+// accumulator of tap t, register r, lane l is M_t[co_base + 4*(l/16) + r]
+// [tile tl_base + l%16].  Per output channel: align taps by 2^sh (exact), add
+// bias and the rounding constant once through tap (1,1) (its column of A^T is
+// all ones, so A^T (c e_7 e_7^T) A adds c to every output of the tile), apply
+// Y = A^T M A in two separable passes, then shift, clamp, ReLU, crop, store.
+// MODE 0: store y.  MODE 1: max |Y + bias| into *aux (calibration).
+// MODE 2: store raw M to aux [36][ntiles][cout] (debug export).
+// G provides cout, h, w, th, tw, ntiles, out_shift, relu, tab.
+template <int LAYOUT, int EPI, int MODE, class G>
+__device__ __forceinline__ void tap_epilogue(const v4i (&acc)[kTaps], const G& g, const int32_t* __restrict__ bias,
+                                             int8_t* __restrict__ y, void* __restrict__ aux, int co_base,
+                                             long long tl_base, int lane) {
+    typedef typename std::conditional<EPI == 64, long long, int>::type acc_t;
+    const int lr = lane & 15, lk = lane >> 4;
+    const long long tile = tl_base + lr;
+    const bool tile_ok = tile < g.ntiles;
+
+    if (MODE == 2) {
+        int32_t* m_out = (int32_t*)aux;
+        if (!tile_ok) return;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int co = co_base + 4 * lk + r;
+            if (co >= g.cout) continue;
+#pragma unroll
+            for (int t = 0; t < kTaps; ++t) m_out[((long long)t * g.ntiles + tile) * g.cout + co] = acc[t][r];
+        }
+        return;
+    }
+
+    const long long tt = tile_ok ? tile : 0;
+    const int img = (int)(tt / ((long long)g.th * g.tw));
+    const int trem = (int)(tt - (long long)img * g.th * g.tw);
+    const int ty = trem / g.tw, tx = trem - ty * g.tw;
+    const int s = g.out_shift;
+    const acc_t rnd = (MODE == 0 && s > 0) ? ((acc_t)1 << (s - 1)) : 0;
+    const int lo = g.relu ? 0 : -128;
+    unsigned long long zmax = 0;
+    uint32_t packed[16];  // NHWC: 4 output channels per pixel
+#pragma unroll
+    for (int p = 0; p < 16; ++p) packed[p] = 0;
+
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int co = co_base + 4 * lk + r;
+        acc_t mv[kTaps];
+#pragma unroll
+        for (int t = 0; t < kTaps; ++t) mv[t] = (acc_t)acc[t][r] << g.tab.sh[t];
+        mv[7] += (acc_t)bias[co] + rnd;
+        acc_t rp[6][4];
+#pragma unroll
+        for (int a = 0; a < 6; ++a) at_1d(&mv[6 * a], rp[a]);
+        acc_t yv[4][4];
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            acc_t col[6], o[4];
+#pragma unroll
+            for (int a = 0; a < 6; ++a) col[a] = rp[a][jj];
+            at_1d(col, o);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) yv[i][jj] = o[i];
+        }
+        if (MODE == 1) {
+            if (tile_ok && co < g.cout) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj)
+                        if (4 * ty + i < g.h && 4 * tx + jj < g.w) {
+                            acc_t v = yv[i][jj];
+                            unsigned long long av = (unsigned long long)(v < 0 ? -(long long)v : (long long)v);
+                            zmax = av > zmax ? av : zmax;
+                        }
+            }
+            continue;
+        }
+        int qv[4][4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                acc_t v = yv[i][jj] >> s;
+                v = v < (acc_t)lo ? (acc_t)lo : v;
+                v = v > (acc_t)127 ? (acc_t)127 : v;
+                qv[i][jj] = (int)v;
+            }
+        if (LAYOUT == WINO_NCHW) {
+            if (!tile_ok || co >= g.cout) continue;
+            int8_t* base = y + (((long long)img * g.cout + co) * g.h + 4 * ty) * g.w + 4 * tx;
+            const bool full_cols = (4 * tx + 3 < g.w) && ((g.w & 3) == 0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                if (4 * ty + i >= g.h) continue;
+                if (full_cols) {
+                    uint32_t wv = __builtin_amdgcn_perm((uint32_t)qv[i][1], (uint32_t)qv[i][0], 0x0c0c0400u) |
+                                  (__builtin_amdgcn_perm((uint32_t)qv[i][3], (uint32_t)qv[i][2], 0x0c0c0400u) << 16);
+                    *(uint32_t*)(base + (long long)i * g.w) = wv;
+                } else {
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj)
+                        if (4 * tx + jj < g.w) base[(long long)i * g.w + jj] = (int8_t)qv[i][jj];
+                }
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) packed[4 * i + jj] |= (uint32_t)(qv[i][jj] & 255) << (8 * r);
+        }
+    }
+
+    if (MODE == 1) {
+        // wave reduction, then one atomic per wave
+        for (int off = 32; off > 0; off >>= 1) {
+            unsigned long long o = __shfl_xor(zmax, off, 64);
+            zmax = o > zmax ? o : zmax;
+        }
+        if (lane == 0) atomicMax((unsigned long long*)aux, zmax);
+        return;
+    }
+    if (LAYOUT == WINO_NHWC && tile_ok) {
+        const int co0 = co_base + 4 * lk;
+        const long long rs = (long long)g.w * g.cout;
+        int8_t* ob = y + (((long long)img * g.h + 4 * ty) * g.w + 4 * tx) * g.cout + co0;
+        const bool full = (co0 + 3 < g.cout) && ((g.cout & 3) == 0) && (4 * ty + 3 < g.h) && (4 * tx + 3 < g.w);
+        if (full) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) *(uint32_t*)(ob + i * rs + jj * g.cout) = packed[4 * i + jj];
+        } else {
+            for (int i = 0; i < 4; ++i)
+                for (int jj = 0; jj < 4; ++jj) {
+                    if (4 * ty + i >= g.h || 4 * tx + jj >= g.w) continue;
+                    for (int r = 0; r < 4; ++r)
+                        if (co0 + r < g.cout) ob[i * rs + jj * g.cout + r] = (int8_t)(packed[4 * i + jj] >> (8 * r));
+                }
+        }
+    }
+}
+
+}  // namespace winof4

@@ -23,13 +23,9 @@
 // runs in 32-bit integers when the plan's bound proves every partial sum fits,
 // otherwise in 64-bit.
 #include <algorithm>
-#include <type_traits>
-#include "winof4_internal.h"
+#include "wino_device.h"
 
 using namespace winof4;
-
-typedef short v2s __attribute__((ext_vector_type(2)));
-typedef int v4i __attribute__((ext_vector_type(4)));
 
 namespace {
 
@@ -49,37 +45,6 @@ struct K1Args {
     long long t_pad;                    // tile stride of a tap plane in Vq
     TapTables tab;
 };
-
-__device__ __forceinline__ v2s splat(int v) { return (v2s){(short)v, (short)v}; }
-
-// sign-extended bytes 0 and 2 of w as two 16-bit lanes
-__device__ __forceinline__ v2s lanes_even(uint32_t w) {
-    return __builtin_bit_cast(v2s, __builtin_amdgcn_perm(0u, w, 0x020c000cu)) >> splat(8);
-}
-// sign-extended bytes 1 and 3 of w
-__device__ __forceinline__ v2s lanes_odd(uint32_t w) {
-    return __builtin_bit_cast(v2s, w) >> splat(8);
-}
-
-// One-dimensional B^T transform of a 6-vector, twelve additions with shared
-// subexpressions; the rows of B^T (Sec. II) are
-//   4 0 -5 0 1 0 / 0 -4 -4 1 1 0 / 0 4 -4 -1 1 0 / 0 -2 -1 2 1 0 /
-//   0 2 -1 -2 1 0 / 0 4 0 -5 0 1.
-template <class T>
-__device__ __forceinline__ void bt_1d(const T* v, T* r, T two, T four) {
-    T a = v[4] - four * v[2];
-    T b = four * v[1] - v[3];
-    T c = v[4] - v[2];
-    T d = v[1] - v[3];
-    T e = v[0] - v[2];
-    T f = v[5] - v[3];
-    r[0] = four * e + c;
-    r[1] = a - b;
-    r[2] = a + b;
-    r[3] = c - two * d;
-    r[4] = c + two * d;
-    r[5] = four * d + f;
-}
 
 // Stage the halo band of one block into LDS as [row][col][channel] bytes
 // (channel fastest, K1_CS words per pixel).  Rows 4ty-1 .. 4ty+4, columns
@@ -123,16 +88,6 @@ __device__ __forceinline__ void k1_stage_band(uint32_t* lds, const int8_t* __res
     }
 }
 
-// Consecutive workgroup ids are dispatched round robin over the 8 XCDs
-// (workgroup i runs on XCD i % 8); this maps them to logical ids so that each
-// XCD works through one contiguous range of logical blocks.
-__device__ __forceinline__ int k1_xcd_remap(int bid, int nblocks) {
-    const int nx = 8;
-    const int full = nblocks / nx * nx;
-    if (bid >= full) return bid;
-    return (bid % nx) * (full / nx) + bid / nx;
-}
-
 // MODE 0: write Vq.  MODE 1: per-tap max |V| into tapmax[36] (calibration).
 template <int LAYOUT, int MODE>
 __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __restrict__ x,
@@ -144,7 +99,7 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
     // then tile row; consecutive logical ids are kept on one XCD (its L2),
     // so the channel groups sharing each 128-byte line of an NHWC pixel and
     // the tile rows sharing halo rows are read by concurrent workgroups.
-    int bid = k1_xcd_remap((int)blockIdx.x, (int)gridDim.x);
+    int bid = xcd_remap((int)blockIdx.x, (int)gridDim.x);
     const int cgi = bid % g.ncg;
     bid /= g.ncg;
     const int txb = bid % g.ntxb;
@@ -162,36 +117,13 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
     const int tx = tx0 + j;
     const bool valid = tx < g.tw;
 
-    v2s ev[6][6], od[6][6];
+    uint32_t wv[6][6];
 #pragma unroll
     for (int r = 0; r < 6; ++r)
 #pragma unroll
-        for (int c = 0; c < 6; ++c) {
-            uint32_t wv = band[(r * K1_COLS + 4 * j + c) * K1_CS + q];
-            ev[r][c] = lanes_even(wv);
-            od[r][c] = lanes_odd(wv);
-        }
-    const v2s two = splat(2), four = splat(4);
-    // columns: T1 = B^T d
-#pragma unroll
-    for (int c = 0; c < 6; ++c) {
-        v2s ve[6], vo[6], re[6], ro[6];
-#pragma unroll
-        for (int r = 0; r < 6; ++r) { ve[r] = ev[r][c]; vo[r] = od[r][c]; }
-        bt_1d(ve, re, two, four);
-        bt_1d(vo, ro, two, four);
-#pragma unroll
-        for (int r = 0; r < 6; ++r) { ev[r][c] = re[r]; od[r][c] = ro[r]; }
-    }
-    // rows: V = T1 B
-#pragma unroll
-    for (int r = 0; r < 6; ++r) {
-        v2s re[6], ro[6];
-        bt_1d(ev[r], re, two, four);
-        bt_1d(od[r], ro, two, four);
-#pragma unroll
-        for (int c = 0; c < 6; ++c) { ev[r][c] = re[c]; od[r][c] = ro[c]; }
-    }
+        for (int c = 0; c < 6; ++c) wv[r][c] = band[(r * K1_COLS + 4 * j + c) * K1_CS + q];
+    v2s ev[6][6], od[6][6];
+    input_tile_transform(wv, ev, od);
 
     if (MODE == 0) {
         if (!valid) return;
@@ -200,18 +132,7 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
         uint32_t* dst = (uint32_t*)(vq + ((long long)cgi * g.t_pad + tile) * K1_CG) + q;
         const long long plane = g.t_pad * g.cin_pad / 4;   // words per tap plane
 #pragma unroll
-        for (int t = 0; t < kTaps; ++t) {
-            const int e = g.tab.eb[t];
-            const v2s rnd = splat(e ? (1 << (e - 1)) : 0);
-            const v2s sh = splat(e);
-            v2s a = (ev[t / 6][t % 6] + rnd) >> sh;
-            v2s b = (od[t / 6][t % 6] + rnd) >> sh;
-            a = __builtin_elementwise_min(__builtin_elementwise_max(a, splat(-128)), splat(127));
-            b = __builtin_elementwise_min(__builtin_elementwise_max(b, splat(-128)), splat(127));
-            // bytes: ch0 = a.lo, ch1 = b.lo, ch2 = a.hi, ch3 = b.hi
-            dst[t * plane] = __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, b),
-                                                   __builtin_bit_cast(uint32_t, a), 0x06020400u);
-        }
+        for (int t = 0; t < kTaps; ++t) dst[t * plane] = requant_pack(ev[t / 6][t % 6], od[t / 6][t % 6], g.tab.eb[t]);
     } else {
         if (valid) {
 #pragma unroll
@@ -268,44 +189,6 @@ struct K2Args {
     TapTables tab;
 };
 
-// One-dimensional A^T transform of a 6-vector (rows of A^T, Sec. II:
-// 1 1 1 1 1 0 / 0 1 -1 2 -2 0 / 0 1 1 4 4 0 / 0 1 -1 8 -8 1).
-template <class T>
-__device__ __forceinline__ void at_1d(const T* v, T* y) {
-    T p = v[1] + v[2], m = v[1] - v[2], q = v[3] + v[4], r = v[3] - v[4];
-    y[0] = v[0] + p + q;
-    y[1] = m + (r << 1);
-    y[2] = p + (q << 2);
-    y[3] = m + (r << 3) + v[5];
-}
-
-// XCD-aware block order: hardware dispatches consecutive workgroup ids round
-// robin over the 8 XCDs; remap so that consecutive logical ids (the output
-// channel blocks of one tile block, which share its Vq rows) land on the
-// same XCD and its L2.
-__device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
-    const int nx = 8;
-    const int full = nblocks / nx * nx;
-    if (bid >= full) return bid;
-    return (bid % nx) * (full / nx) + bid / nx;
-}
-
-__device__ __forceinline__ int k2_slot(int row, int part) { return part ^ ((row >> 1) & 3); }
-
-// Workgroup barrier without the implicit wait for outstanding global loads
-// that __syncthreads() carries: the caller waits for exactly the loads it
-// needs with s_waitcnt.  The empty asm statements keep the compiler from
-// moving LDS accesses across the barrier.
-__device__ __forceinline__ void k2_barrier() {
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
-
-// s_waitcnt vmcnt(n) leaving the other counters untouched (gfx9 encoding:
-// vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8]).
-#define K2_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(0x0f70 | (n))
-
 // MODE 0: store y.  MODE 1: max |Y + bias| into *zmax (calibration).
 // MODE 2: store raw M (debug export).
 template <int LAYOUT, int EPI, int MODE>
@@ -314,7 +197,6 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
                                                             const int32_t* __restrict__ bias,
                                                             int8_t* __restrict__ y,
                                                             void* __restrict__ aux, K2Args g) {
-    typedef typename std::conditional<EPI == 64, long long, int>::type acc_t;
     __shared__ __attribute__((aligned(1024))) uint8_t lds[K2_NBUF * K2_STAGE];
     const int lbid = xcd_remap(blockIdx.x, g.nblocks);
     const int bco = lbid % g.nbco, btl = lbid / g.nbco;
@@ -345,11 +227,11 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
         const int rr = lane >> 2, slot = lane & 3;
         if (j < K2_A_BYTES / 1024) {
             const int u = j / (K2_CO / 16), row = 16 * (j % (K2_CO / 16)) + rr;
-            src[i] = uq + u * sa + (long long)(co_blk + row) * kKStep + 16 * k2_slot(row, slot);
+            src[i] = uq + u * sa + (long long)(co_blk + row) * kKStep + 16 * lds_slot(row, slot);
         } else {
             const int jj = j - K2_A_BYTES / 1024;
             const int u = jj / (K2_TL / 16), row = 16 * (jj % (K2_TL / 16)) + rr;
-            src[i] = vq + u * sb + (tl_blk + row) * kKStep + 16 * k2_slot(row, slot);
+            src[i] = vq + u * sb + (tl_blk + row) * kKStep + 16 * lds_slot(row, slot);
         }
         dst[i] = j * 1024;
     }
@@ -379,8 +261,8 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
 
     // fragment offsets within a stage buffer (tap u adds u * rows * 64)
     const int row_a = 16 * cw + lr, row_b = 16 * tw + lr;
-    const int frag_a = row_a * 64 + 16 * k2_slot(row_a, lk);
-    const int frag_b = K2_A_BYTES + row_b * 64 + 16 * k2_slot(row_b, lk);
+    const int frag_a = row_a * 64 + 16 * lds_slot(row_a, lk);
+    const int frag_b = K2_A_BYTES + row_b * 64 + 16 * lds_slot(row_b, lk);
 
     for (int st = 0; st < K2_NBUF - 1 && st < nstage; ++st) issue(st);
     for (int kc = 0; kc < nkc; ++kc) {
@@ -389,10 +271,10 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
             const int st = kc * (kTaps / K2_G) + grp;
             const int ahead = nstage - 1 - st;        // stages issued after this one
             static_assert(K2_NBUF == 4 && 2 * K2_LPW <= 15, "wait counts below assume two stages ahead");
-            if (ahead >= 2) K2_WAIT_VM(2 * K2_LPW);
-            else if (ahead == 1) K2_WAIT_VM(K2_LPW);
-            else K2_WAIT_VM(0);
-            k2_barrier();                              // stage st visible; stage st-1 consumed
+            if (ahead >= 2) WINO_WAIT_VM(2 * K2_LPW);
+            else if (ahead == 1) WINO_WAIT_VM(K2_LPW);
+            else WINO_WAIT_VM(0);
+            ring_barrier();                              // stage st visible; stage st-1 consumed
             if (st + K2_NBUF - 1 < nstage) issue(st + K2_NBUF - 1);
             const uint8_t* base = lds + (st % K2_NBUF) * K2_STAGE;
 #pragma unroll
@@ -405,135 +287,7 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
         }
     }
 
-    // accumulator layout: lane holds C[row = 4*lk + r][col = lr], rows are
-    // output channels, columns are tiles
-    const long long tile = tl_base + lr;
-    const bool tile_ok = tile < g.ntiles;
-
-    if (MODE == 2) {
-        int32_t* m_out = (int32_t*)aux;
-        if (!tile_ok) return;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int co = co_base + 4 * lk + r;
-            if (co >= g.cout) continue;
-#pragma unroll
-            for (int t = 0; t < kTaps; ++t) m_out[((long long)t * g.ntiles + tile) * g.cout + co] = acc[t][r];
-        }
-        return;
-    }
-
-    const int img = (int)(tile / ((long long)g.th * g.tw));
-    const int trem = (int)(tile - (long long)img * g.th * g.tw);
-    const int ty = trem / g.tw, tx = trem - ty * g.tw;
-    const int s = g.out_shift;
-    const acc_t rnd = (MODE == 0 && s > 0) ? ((acc_t)1 << (s - 1)) : 0;
-    const int lo = g.relu ? 0 : -128;
-    unsigned long long zmax = 0;
-    uint32_t packed[16];                 // NHWC: 4 output channels per pixel
-#pragma unroll
-    for (int p = 0; p < 16; ++p) packed[p] = 0;
-
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int co = co_base + 4 * lk + r;
-        acc_t mv[kTaps];
-#pragma unroll
-        for (int t = 0; t < kTaps; ++t) mv[t] = (acc_t)acc[t][r] << g.tab.sh[t];
-        // bias (and the rounding constant) enter once through tap (1,1),
-        // whose column of A^T is all ones: A^T (c e_7 e_7^T) A adds c to
-        // every output of the tile.
-        mv[7] += (acc_t)bias[co] + rnd;
-        acc_t rp[6][4];
-#pragma unroll
-        for (int a = 0; a < 6; ++a) at_1d(&mv[6 * a], rp[a]);
-        acc_t yv[4][4];
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-            acc_t col[6], o[4];
-#pragma unroll
-            for (int a = 0; a < 6; ++a) col[a] = rp[a][jj];
-            at_1d(col, o);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) yv[i][jj] = o[i];
-        }
-        if (MODE == 1) {
-            if (tile_ok && co < g.cout) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int jj = 0; jj < 4; ++jj)
-                        if (4 * ty + i < g.h && 4 * tx + jj < g.w) {
-                            acc_t v = yv[i][jj];
-                            unsigned long long av = (unsigned long long)(v < 0 ? -(long long)v : (long long)v);
-                            zmax = av > zmax ? av : zmax;
-                        }
-            }
-            continue;
-        }
-        int qv[4][4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-                acc_t v = yv[i][jj] >> s;
-                v = v < (acc_t)lo ? (acc_t)lo : v;
-                v = v > (acc_t)127 ? (acc_t)127 : v;
-                qv[i][jj] = (int)v;
-            }
-        if (LAYOUT == WINO_NCHW) {
-            if (!tile_ok || co >= g.cout) continue;
-            int8_t* base = y + (((long long)img * g.cout + co) * g.h + 4 * ty) * g.w + 4 * tx;
-            const bool full_cols = (4 * tx + 3 < g.w) && ((g.w & 3) == 0);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                if (4 * ty + i >= g.h) continue;
-                if (full_cols) {
-                    uint32_t wv = __builtin_amdgcn_perm((uint32_t)qv[i][1], (uint32_t)qv[i][0], 0x0c0c0400u) |
-                                  (__builtin_amdgcn_perm((uint32_t)qv[i][3], (uint32_t)qv[i][2], 0x0c0c0400u) << 16);
-                    *(uint32_t*)(base + (long long)i * g.w) = wv;
-                } else {
-#pragma unroll
-                    for (int jj = 0; jj < 4; ++jj)
-                        if (4 * tx + jj < g.w) base[(long long)i * g.w + jj] = (int8_t)qv[i][jj];
-                }
-            }
-        } else {
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int jj = 0; jj < 4; ++jj) packed[4 * i + jj] |= (uint32_t)(qv[i][jj] & 255) << (8 * r);
-        }
-    }
-
-    if (MODE == 1) {
-        // wave reduction, then one atomic per wave
-        for (int off = 32; off > 0; off >>= 1) {
-            unsigned long long o = __shfl_xor(zmax, off, 64);
-            zmax = o > zmax ? o : zmax;
-        }
-        if (lane == 0) atomicMax((unsigned long long*)aux, zmax);
-        return;
-    }
-    if (LAYOUT == WINO_NHWC && tile_ok) {
-        const int co0 = co_base + 4 * lk;
-        const long long rs = (long long)g.w * g.cout;
-        int8_t* ob = y + (((long long)img * g.h + 4 * ty) * g.w + 4 * tx) * g.cout + co0;
-        const bool full = (co0 + 3 < g.cout) && ((g.cout & 3) == 0) && (4 * ty + 3 < g.h) && (4 * tx + 3 < g.w);
-        if (full) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int jj = 0; jj < 4; ++jj) *(uint32_t*)(ob + i * rs + jj * g.cout) = packed[4 * i + jj];
-        } else {
-            for (int i = 0; i < 4; ++i)
-                for (int jj = 0; jj < 4; ++jj) {
-                    if (4 * ty + i >= g.h || 4 * tx + jj >= g.w) continue;
-                    for (int r = 0; r < 4; ++r)
-                        if (co0 + r < g.cout) ob[i * rs + jj * g.cout + r] = (int8_t)(packed[4 * i + jj] >> (8 * r));
-                }
-        }
-    }
+    tap_epilogue<LAYOUT, EPI, MODE>(acc, g, bias, y, aux, co_base, tl_base, lane);
 }
 
 // ---------------------------------------------------------------------------

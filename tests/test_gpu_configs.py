@@ -47,16 +47,16 @@ def _run_layer(x, f, b, spec, rec, layout, variant=W.SPLIT):
     return yn
 
 
-@pytest.mark.parametrize("layout", [W.NHWC, W.NCHW])
+@pytest.mark.parametrize("layout,variant", [(W.NHWC, W.SPLIT), (W.NCHW, W.SPLIT), (W.NHWC, W.FUSED)])
 @pytest.mark.parametrize("name", ["C4", "C5"])
-def test_full_size_layer_bitexact(name, layout):
+def test_full_size_layer_bitexact(name, layout, variant):
     x, layers = workloads.generate(name)
     f, b, spec = layers[0]
-    _run_layer(x, f, b, spec, GOLDEN[name]["layers"][0], layout)
+    _run_layer(x, f, b, spec, GOLDEN[name]["layers"][0], layout, variant)
 
 
-@pytest.mark.parametrize("layout", [W.NHWC, W.NCHW])
-def test_c3_chain_bitexact(layout):
+@pytest.mark.parametrize("layout,variant", [(W.NHWC, W.SPLIT), (W.NCHW, W.SPLIT), (W.NHWC, W.FUSED)])
+def test_c3_chain_bitexact(layout, variant):
     """Four chained layers; each layer's input is the GPU's own previous
     output (max-pooled where the stage halves the image), and every layer
     must match the oracle's chain byte for byte."""
@@ -65,4 +65,4 @@ def test_c3_chain_bitexact(layout):
     for k, (f, b, spec) in enumerate(layers):
         if k > 0:
             cur = workloads.next_layer_input(cur, spec)
-        cur = _run_layer(cur, f, b, spec, GOLDEN["C3"]["layers"][k], layout)
+        cur = _run_layer(cur, f, b, spec, GOLDEN["C3"]["layers"][k], layout, variant)

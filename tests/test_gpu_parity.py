@@ -66,22 +66,38 @@ def test_tap_gemm_bitexact(shape, layout):
     assert (m.cpu().numpy().astype(np.int64) == ref).all()
 
 
+VARIANTS = [W.SPLIT, W.FUSED]
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
 @pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("shape", SHAPES)
 @pytest.mark.parametrize("relu,out_shift", [(False, 9), (True, 12)])
-def test_conv_bitexact_random(shape, layout, relu, out_shift):
+def test_conv_bitexact_random(shape, layout, relu, out_shift, variant):
     n, cin, cout, h, w = shape
     x, f, b = workloads.random_case(5, n, cin, cout, h, w, signed=True)
     eb = tapwise.calibrate_input_exps(x)
     gp, op = _plan_pair(f, eb, b, out_shift, relu)
     assert W.wino_f4_plan_info(gp)["epilogue_bits"] == 32
-    y = run_conv(gp, x, layout)
+    y = run_conv(gp, x, layout, variant)
     ref = tapwise.conv_int8(x, op)
     assert (y == ref).all(), f"{(y != ref).sum()} mismatches"
 
 
+@pytest.mark.parametrize("variant", VARIANTS)
 @pytest.mark.parametrize("layout", LAYOUTS)
-def test_conv_int64_epilogue(layout):
+def test_fused_equals_split_unaligned_channels(layout, variant):
+    """Odd channel counts exercise the byte-wise loads of both variants."""
+    n, cin, cout, h, w = 1, 67, 33, 10, 13
+    x, f, b = workloads.random_case(11, n, cin, cout, h, w, signed=True)
+    eb = tapwise.calibrate_input_exps(x)
+    gp, op = _plan_pair(f, eb, b, 10, False)
+    assert (run_conv(gp, x, layout, variant) == tapwise.conv_int8(x, op)).all()
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_conv_int64_epilogue(layout, variant):
     """Large alignment shifts force the 64-bit output transform."""
     n, cin, cout, h, w = 1, 20, 24, 11, 10
     x, f, b = workloads.random_case(6, n, cin, cout, h, w, signed=True)
@@ -90,17 +106,18 @@ def test_conv_int64_epilogue(layout):
     eb[0] = 14
     gp, op = _plan_pair(f, eb, b, 20, False)
     assert W.wino_f4_plan_info(gp)["epilogue_bits"] == 64
-    y = run_conv(gp, x, layout)
+    y = run_conv(gp, x, layout, variant)
     assert (y == tapwise.conv_int8(x, op)).all()
 
 
-def test_conv_deterministic_repeat():
+@pytest.mark.parametrize("variant", VARIANTS)
+def test_conv_deterministic_repeat(variant):
     n, cin, cout, h, w = 2, 96, 96, 30, 30
     x, f, b = workloads.random_case(7, n, cin, cout, h, w, signed=False, zero_frac=0.5)
     eb = tapwise.calibrate_input_exps(x)
     gp = W.wino_f4_plan(f, eb, bias=b, out_shift=11)
-    y1 = run_conv(gp, x, W.NHWC)
-    y2 = run_conv(gp, x, W.NHWC)
+    y1 = run_conv(gp, x, W.NHWC, variant)
+    y2 = run_conv(gp, x, W.NHWC, variant)
     assert (y1 == y2).all()
 
 
