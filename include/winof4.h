@@ -61,6 +61,15 @@ typedef enum wino_variant { WINO_SPLIT = 0, WINO_FUSED = 1 } wino_variant;
 
 typedef struct wino_f4_plan_s* wino_f4_plan_t;   /* opaque, immutable after creation */
 
+/* Which kernel runs the tap GEMM of the SPLIT variant (both give the same,
+ * exact result).  RESIDENT keeps all 36 tap accumulators of a 64-channel x
+ * 32-tile block in registers and applies the output transform once at the
+ * end; ROWS streams the taps one row of the 6x6 tile at a time and folds
+ * each row into the output as it completes, which allows 64 x 64 blocks.
+ * AUTO picks ROWS when its blocks fill the device and the 32-bit epilogue
+ * applies, else RESIDENT.                                                  */
+typedef enum wino_tap_kernel { WINO_TAP_AUTO = 0, WINO_TAP_RESIDENT = 1, WINO_TAP_ROWS = 2 } wino_tap_kernel;
+
 /*
  * wino_f4_plan -- the offline step: weight transform U = G f G^T (Eq.
  * winograd), tap-wise power-of-two weight quantization (Sec. III-B,
@@ -108,6 +117,16 @@ wino_status wino_f4_plan(wino_f4_plan_t* out, const float* w_oihw, int32_t cin, 
 wino_status wino_f4_plan_tables(const float* w_oihw, int32_t cin, int32_t cout, const int8_t* in_exp,
                                 const int8_t* w_exp, const int32_t* bias, int32_t out_shift, int8_t* e_g,
                                 int8_t* sh, int32_t* e_o, int32_t* epilogue_bits, int8_t* uq);
+
+/*
+ * wino_f4_plan_set_tap_kernel -- choose the tap-GEMM kernel (wino_tap_kernel)
+ * for later SPLIT convolutions with this plan.  ROWS applies to output
+ * convolutions with the 32-bit epilogue; calibration, debug exports and the
+ * 64-bit epilogue always use RESIDENT.  Not to be called while a convolution
+ * with the plan is being enqueued on another thread.
+ * Errors: WINO_EINVAL (null plan, unknown kind).
+ */
+wino_status wino_f4_plan_set_tap_kernel(wino_f4_plan_t plan, int32_t kind);
 
 /* Releases a plan and its device memory.  NULL is ignored.  The caller must
  * ensure no convolution using the plan is still running. */

@@ -320,6 +320,12 @@ extern "C" void wino_f4_plan_destroy(wino_f4_plan_t p) {
     delete p;
 }
 
+extern "C" wino_status wino_f4_plan_set_tap_kernel(wino_f4_plan_t p, int32_t kind) {
+    if (!p || kind < WINO_TAP_AUTO || kind > WINO_TAP_ROWS) return WINO_EINVAL;
+    p->tap_kernel = kind;
+    return WINO_OK;
+}
+
 extern "C" wino_status wino_f4_plan_info(wino_f4_plan_t p, int8_t* e_g, int8_t* sh, int32_t* e_o,
                                          int32_t* epilogue_bits, int8_t* uq, int32_t* cin,
                                          int32_t* cout) {

@@ -100,6 +100,20 @@ __device__ __forceinline__ uint32_t requant_pack(v2s ev, v2s od, int e) {
     return __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, b), __builtin_bit_cast(uint32_t, a), 0x06020400u);
 }
 
+// median of three (clamp a to [lo, hi]) in one instruction
+__device__ __forceinline__ int med3_i32(int a, int lo, int hi) {
+    int r;
+    asm("v_med3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(lo), "v"(hi));
+    return r;
+}
+
+// word w with byte k replaced by the low byte of b
+template <int K>
+__device__ __forceinline__ uint32_t put_byte(uint32_t w, uint32_t b) {
+    constexpr uint32_t sel = K == 0 ? 0x07060500u : K == 1 ? 0x07060004u : K == 2 ? 0x07000504u : 0x00060504u;
+    return __builtin_amdgcn_perm(w, b, sel);
+}
+
 // One-dimensional A^T transform of a 6-vector (rows of A^T, Sec. II:
 // 1 1 1 1 1 0 / 0 1 -1 2 -2 0 / 0 1 1 4 4 0 / 0 1 -1 8 -8 1).
 template <class T>
@@ -141,6 +155,10 @@ __device__ __forceinline__ void ring_barrier() {
 // s_waitcnt vmcnt(n) leaving the other counters untouched (gfx9 encoding:
 // vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8]).
 #define WINO_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(0x0f70 | (n))
+// the same, and also every LDS read of this wave returned (lgkmcnt 0): a
+// ring stage's buffer is refilled right after the next barrier, so each wave
+// must be done reading it before it arrives there
+#define WINO_WAIT_VM_LDS(n) __builtin_amdgcn_s_waitcnt(0x0070 | (n))
 
 // Epilogue of a 16-channel x 16-tile MFMA block holding all 36 taps: the
 // accumulator of tap t, register r, lane l is M_t[co_base + 4*(l/16) + r]
@@ -224,10 +242,14 @@ __device__ __forceinline__ void tap_epilogue(const v4i (&acc)[kTaps], const G& g
         for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
-                acc_t v = yv[i][jj] >> s;
-                v = v < (acc_t)lo ? (acc_t)lo : v;
-                v = v > (acc_t)127 ? (acc_t)127 : v;
-                qv[i][jj] = (int)v;
+                if (EPI == 32) {
+                    qv[i][jj] = med3_i32((int)(yv[i][jj] >> s), lo, 127);
+                } else {
+                    acc_t v = yv[i][jj] >> s;
+                    v = v < (acc_t)lo ? (acc_t)lo : v;
+                    v = v > (acc_t)127 ? (acc_t)127 : v;
+                    qv[i][jj] = (int)v;
+                }
             }
         if (LAYOUT == WINO_NCHW) {
             if (!tile_ok || co >= g.cout) continue;
@@ -250,7 +272,12 @@ __device__ __forceinline__ void tap_epilogue(const v4i (&acc)[kTaps], const G& g
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int jj = 0; jj < 4; ++jj) packed[4 * i + jj] |= (uint32_t)(qv[i][jj] & 255) << (8 * r);
+                for (int jj = 0; jj < 4; ++jj) {
+                    uint32_t& pk = packed[4 * i + jj];
+                    const uint32_t q = (uint32_t)qv[i][jj];
+                    pk = r == 0 ? put_byte<0>(pk, q) : r == 1 ? put_byte<1>(pk, q) : r == 2 ? put_byte<2>(pk, q)
+                                                                                        : put_byte<3>(pk, q);
+                }
         }
     }
 

@@ -155,13 +155,15 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
 // Workgroup = 8 waves computing 64 output channels x 32 tiles for all 36
 // taps; wave w owns channels 16*(w%4).. and tiles 16*(w/4).. (one 16x16
 // int8 MFMA block per tap, 36 x 4 int32 accumulators per lane).  The k loop
-// runs over input channels in steps of 64; each step is split into six tap
-// groups ("stages").  A stage's Uq slice (6 taps x 64 rows x 64 B) and Vq
-// slice (6 taps x 32 rows x 64 B) are copied global -> LDS by the
-// direct-to-LDS load (no VGPR staging) into a ring of four stage buffers, so
-// three stages are in flight while one feeds the MFMAs.  (Measured on
-// gfx950: two 4-wave workgroups per CU with 32x32 tiles and three-stage
-// rings were 1.4x slower -- more L2 traffic, shallower rings.)  Every such load writes 1 KB of LDS
+// runs over input channels in steps of 64; each step is split into three tap
+// groups ("stages").  A stage's Uq slice (12 taps x 64 rows x 64 B) and Vq
+// slice (12 taps x 32 rows x 64 B) are copied global -> LDS by the
+// direct-to-LDS load (no VGPR staging), double buffered: the next stage
+// loads while this one feeds the MFMAs.  Measured on gfx950, the copy rate of
+// such a ring is set by the loads each wave issues per stage (one barrier
+// per stage): 3 per wave gave 26 B/clk per CU, 9 per wave 34 B/clk.  (Also
+// measured: two 4-wave workgroups per CU with 32x32 tiles were 1.4x slower
+// -- more L2 traffic, shallower rings.)  Every such load writes 1 KB of LDS
 // contiguously (16 bytes per lane); the 16-byte slot of a row holding input
 // bytes [16p, 16p+16) is p ^ ((row >> 1) & 3).  Measured on gfx950, this
 // swizzle lets the fragment reads (16 rows x one 16-byte part per 16 lanes)
@@ -170,12 +172,13 @@ constexpr int K2_CO = 64;               // output channels per workgroup
 constexpr int K2_TL = 32;               // tiles per workgroup
 constexpr int K2_THREADS = 512;         // waves: (K2_CO/16) x (K2_TL/16), each 16x16
 constexpr int K2_WAVES = K2_THREADS / 64;
-constexpr int K2_G = 6;                 // taps per stage
+constexpr int K2_G = 12;                // taps per stage
 constexpr int K2_A_BYTES = K2_G * K2_CO * 64;
 constexpr int K2_B_BYTES = K2_G * K2_TL * 64;
 constexpr int K2_STAGE = K2_A_BYTES + K2_B_BYTES;
 constexpr int K2_KB = K2_STAGE / 1024;          // 1-KB load instructions per stage
-constexpr int K2_NBUF = 4;                      // ring depth (3 stages in flight)
+constexpr int K2_NBUF = 2;                      // double buffer: the next stage loads during this one
+constexpr int K2_PF = 6;                        // taps whose LDS fragments are in flight ahead
 constexpr int K2_LPW = (K2_KB + K2_WAVES - 1) / K2_WAVES;   // load instructions per wave per stage
 static_assert((K2_CO / 16) * (K2_TL / 16) == K2_WAVES, "one 16x16 block per wave");
 static_assert(K2_NBUF * K2_STAGE <= 160 * 1024, "LDS");
@@ -216,22 +219,31 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
 
     // This wave's 1-KB load instructions of a stage: global source of this
     // lane (stage 0) and LDS destination offset within a stage buffer.
-    const int8_t* src[K2_LPW];
+    // Each load instruction covers 16 rows x 64 B; a lane's byte offset within
+    // those 1 KB is the same for every instruction of the wave (the swizzle
+    // depends on the row only through bits that are equal across the 16-row
+    // groups), so the addresses are a wave-uniform base (scalar registers)
+    // plus one 32-bit lane offset.
+    const int wv_id = __builtin_amdgcn_readfirstlane(wave);
+    const int rr = lane >> 2;
+    const int lane_off = rr * 64 + 16 * lds_slot(rr, lane & 3);
+    long long ubase[K2_LPW];
     int dst[K2_LPW];
+    bool isa[K2_LPW];
 #pragma unroll
     for (int i = 0; i < K2_LPW; ++i) {
         // when the stage's loads do not split evenly, the last round repeats
         // an earlier load (same bytes to the same place)
-        int j = wave + K2_WAVES * i;
+        int j = wv_id + K2_WAVES * i;
         if (j >= K2_KB) j -= K2_WAVES;
-        const int rr = lane >> 2, slot = lane & 3;
-        if (j < K2_A_BYTES / 1024) {
-            const int u = j / (K2_CO / 16), row = 16 * (j % (K2_CO / 16)) + rr;
-            src[i] = uq + u * sa + (long long)(co_blk + row) * kKStep + 16 * lds_slot(row, slot);
+        isa[i] = j < K2_A_BYTES / 1024;
+        if (isa[i]) {
+            const int u = j / (K2_CO / 16), q = j % (K2_CO / 16);
+            ubase[i] = u * sa + (long long)(co_blk + 16 * q) * kKStep;
         } else {
             const int jj = j - K2_A_BYTES / 1024;
-            const int u = jj / (K2_TL / 16), row = 16 * (jj % (K2_TL / 16)) + rr;
-            src[i] = vq + u * sb + (tl_blk + row) * kKStep + 16 * lds_slot(row, slot);
+            const int u = jj / (K2_TL / 16), q = jj % (K2_TL / 16);
+            ubase[i] = u * sb + (tl_blk + 16 * q) * kKStep;
         }
         dst[i] = j * 1024;
     }
@@ -242,15 +254,14 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
         uint8_t* base = lds + (st % K2_NBUF) * K2_STAGE;
 #pragma unroll
         for (int i = 0; i < K2_LPW; ++i) {
-            const bool is_a = dst[i] < K2_A_BYTES;
-            const long long off = (long long)(K2_G * grp) * (is_a ? sa : sb) + kc * (is_a ? ka : kb);
+            const long long off = ubase[i] + (long long)(K2_G * grp) * (isa[i] ? sa : sb) + kc * (isa[i] ? ka : kb);
             // Vq is streamed once per output-channel block: non-temporal, so it
             // does not push the small, hot Uq out of L2
-            if (is_a)
-                __builtin_amdgcn_global_load_lds((const void*)(src[i] + off),
+            if (isa[i])
+                __builtin_amdgcn_global_load_lds((const void*)(uq + off + lane_off),
                                                  (__attribute__((address_space(3))) void*)(base + dst[i]), 16, 0, 0);
             else
-                __builtin_amdgcn_global_load_lds((const void*)(src[i] + off),
+                __builtin_amdgcn_global_load_lds((const void*)(vq + off + lane_off),
                                                  (__attribute__((address_space(3))) void*)(base + dst[i]), 16, 0, 2);
         }
     };
@@ -270,20 +281,41 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
         for (int grp = 0; grp < kTaps / K2_G; ++grp) {
             const int st = kc * (kTaps / K2_G) + grp;
             const int ahead = nstage - 1 - st;        // stages issued after this one
-            static_assert(K2_NBUF == 4 && 2 * K2_LPW <= 15, "wait counts below assume two stages ahead");
-            if (ahead >= 2) WINO_WAIT_VM(2 * K2_LPW);
-            else if (ahead == 1) WINO_WAIT_VM(K2_LPW);
-            else WINO_WAIT_VM(0);
+            static_assert(K2_NBUF == 2, "stage st is the newest issued when it is waited for");
+            (void)ahead;
+            WINO_WAIT_VM_LDS(0);
             ring_barrier();                              // stage st visible; stage st-1 consumed
             if (st + K2_NBUF - 1 < nstage) issue(st + K2_NBUF - 1);
             const uint8_t* base = lds + (st % K2_NBUF) * K2_STAGE;
+            // software pipeline over the stage's taps: fragments of K2_PF taps
+            // are in flight ahead of the MFMA that consumes the oldest, so the
+            // LDS read latency hides behind MFMAs
+            v4i fa[K2_PF], fb[K2_PF];
+#pragma unroll
+            for (int u = 0; u < K2_PF; ++u) {
+                fa[u] = *(const v4i*)(base + frag_a + u * K2_CO * 64);
+                fb[u] = *(const v4i*)(base + frag_b + u * K2_TL * 64);
+            }
 #pragma unroll
             for (int u = 0; u < K2_G; ++u) {
-                v4i av = *(const v4i*)(base + frag_a + u * K2_CO * 64);
-                v4i bv = *(const v4i*)(base + frag_b + u * K2_TL * 64);
+                const int slot = u % K2_PF;
                 acc[K2_G * grp + u] =
-                    __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bv, acc[K2_G * grp + u], 0, 0, 0);
+                    __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[slot], fb[slot], acc[K2_G * grp + u], 0, 0, 0);
+                if (u + K2_PF < K2_G) {
+                    fa[slot] = *(const v4i*)(base + frag_a + (u + K2_PF) * K2_CO * 64);
+                    fb[slot] = *(const v4i*)(base + frag_b + (u + K2_PF) * K2_TL * 64);
+                }
             }
+            // keep that order: the scheduler would otherwise pull the reads
+            // next to their MFMAs to save registers (masks: 0x100 LDS read,
+            // 0x008 MFMA)
+            __builtin_amdgcn_sched_group_barrier(0x100, 2 * K2_PF, 0);
+#pragma unroll
+            for (int u = 0; u < K2_G - K2_PF; ++u) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, K2_PF, 0);
         }
     }
 
@@ -291,8 +323,276 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
 }
 
 // ---------------------------------------------------------------------------
+// K2R wino_tap_gemm_rows: the same contraction with the output transform
+// folded in row by row.
+//
+// Y = A^T M' A is linear in the taps, and its row pass only mixes the six
+// taps of one row a of the 6x6 tile: Y = sum_a A^T[:, a] (M'[a, :] A).  So the
+// GEMM can stream the taps row by row: accumulate the six M_t of row a over
+// all input channels, fold them into Y (row pass on the six values, then the
+// rank-one update with column a of A^T), and reuse the six accumulators for
+// the next row.  Per (tile, channel) pair that keeps 16 + 6 values live
+// instead of 36, which buys a 64 x 64 block per workgroup (half the L2 ->
+// LDS operand traffic per MAC of the 64 x 32 block above) and spreads the
+// output transform over the main loop instead of a serial epilogue.
+//
+// Ring stage = one row a and one 64-channel k-chunk: six (tap, chunk) slices
+// of 64 Uq rows + 64 Vq rows, 8 KB each; three stages rotate through 144 KB
+// of LDS, two in flight.  The 16 waves form 4 (channels) x 4 (tiles), one
+// 16x16x64 MFMA block each: 16 + 6 values per pair is 88 registers a lane,
+// which fits the 128 a wave has at four waves per SIMD.  (Two blocks per
+// wave at eight waves would need 176 of 256 and the compiler spills.)
+// A slice is 8 groups of 16 rows; wave w copies group w % 8 of the slices
+// b = w / 8, w / 8 + 2, w / 8 + 4 (groups 0-3: Uq, 4-7: Vq), so its loads
+// never branch.
+//
+// Integer arithmetic is exact: the int32 epilogue is only selected when the
+// plan bound, which also bounds every partial sum of the folds, is < 2^31.
+// ---------------------------------------------------------------------------
+constexpr int KR_CO = 64;
+constexpr int KR_TL = 64;
+constexpr int KR_THREADS = 1024;
+constexpr int KR_WAVES = KR_THREADS / 64;
+constexpr int KR_CHUNK = (KR_CO + KR_TL) * kKStep;      // one tap, one k-chunk
+constexpr int KR_STAGE = 6 * KR_CHUNK;                  // one row of taps
+constexpr int KR_NBUF = 3;
+constexpr int KR_LPW = KR_STAGE / 1024 / KR_WAVES;      // 1-KB loads per wave per stage
+static_assert(KR_LPW == 3, "each wave copies one 16-row group of three slices");
+static_assert((KR_CO + KR_TL) / 16 == 8 && KR_WAVES == 16, "wave -> (group, slice parity) map");
+static_assert((KR_CO / 16) * (KR_TL / 16) == KR_WAVES, "one 16x16 block per wave");
+static_assert(KR_NBUF * KR_STAGE <= 160 * 1024, "LDS");
+static_assert(KR_CO % kCoutPad == 0 || kCoutPad % KR_CO == 0, "channel blocks tile the padded channels");
+static_assert(kTilePad % KR_TL == 0, "tile blocks tile the padded tiles");
+
+// Requantize and store the 4 channels x 16 pixels of one tile held by a lane:
+// q[r][4i+j] is Y + bias + rounding constant of channel co0 + r at pixel
+// (i, j) of the tile.
+template <int LAYOUT, class G>
+__device__ __forceinline__ void store_tile(const int (&q)[4][16], const G& g, int8_t* __restrict__ y, int co0,
+                                           long long tile) {
+    if (tile >= g.ntiles) return;
+    const int img = (int)(tile / ((long long)g.th * g.tw));
+    const int trem = (int)(tile - (long long)img * g.th * g.tw);
+    const int ty = trem / g.tw, tx = trem - ty * g.tw;
+    const int s = g.out_shift;
+    const int lo = g.relu ? 0 : -128;
+    int v[4][16];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int p = 0; p < 16; ++p) v[r][p] = med3_i32(q[r][p] >> s, lo, 127);
+    if (LAYOUT == WINO_NCHW) {
+        const bool full_cols = (4 * tx + 3 < g.w) && ((g.w & 3) == 0);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int co = co0 + r;
+            if (co >= g.cout) continue;
+            int8_t* base = y + (((long long)img * g.cout + co) * g.h + 4 * ty) * g.w + 4 * tx;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                if (4 * ty + i >= g.h) continue;
+                if (full_cols) {
+                    const uint32_t wv = __builtin_amdgcn_perm((uint32_t)v[r][4 * i + 1], (uint32_t)v[r][4 * i], 0x0c0c0400u) |
+                                        (__builtin_amdgcn_perm((uint32_t)v[r][4 * i + 3], (uint32_t)v[r][4 * i + 2],
+                                                               0x0c0c0400u) << 16);
+                    *(uint32_t*)(base + (long long)i * g.w) = wv;
+                } else {
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        if (4 * tx + j < g.w) base[(long long)i * g.w + j] = (int8_t)v[r][4 * i + j];
+                }
+            }
+        }
+    } else {
+        const long long rs = (long long)g.w * g.cout;
+        int8_t* ob = y + (((long long)img * g.h + 4 * ty) * g.w + 4 * tx) * g.cout + co0;
+        const bool full = (co0 + 3 < g.cout) && ((g.cout & 3) == 0) && (4 * ty + 3 < g.h) && (4 * tx + 3 < g.w);
+        if (full) {
+#pragma unroll
+            for (int p = 0; p < 16; ++p) {
+                uint32_t pk = put_byte<0>(0u, (uint32_t)v[0][p]);
+                pk = put_byte<1>(pk, (uint32_t)v[1][p]);
+                pk = put_byte<2>(pk, (uint32_t)v[2][p]);
+                pk = put_byte<3>(pk, (uint32_t)v[3][p]);
+                *(uint32_t*)(ob + (p >> 2) * rs + (p & 3) * g.cout) = pk;
+            }
+        } else {
+#pragma unroll
+            for (int p = 0; p < 16; ++p) {
+                if (4 * ty + (p >> 2) >= g.h || 4 * tx + (p & 3) >= g.w) continue;
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (co0 + r < g.cout) ob[(p >> 2) * rs + (p & 3) * g.cout + r] = (int8_t)v[r][p];
+            }
+        }
+    }
+}
+
+template <int LAYOUT>
+__global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* __restrict__ uq,
+                                                                 const int8_t* __restrict__ vq,
+                                                                 const int32_t* __restrict__ bias,
+                                                                 int8_t* __restrict__ y, K2Args g) {
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[KR_NBUF * KR_STAGE];
+    const int lbid = xcd_remap(blockIdx.x, g.nblocks);
+    const int bco = lbid % g.nbco, btl = lbid / g.nbco;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int cw = wave & 3, tw = wave >> 2;
+    const int co_blk = bco * KR_CO;
+    const long long tl_blk = (long long)btl * KR_TL;
+    const int lr = lane & 15, lk = lane >> 4;
+    const int nkc = g.cin_pad / kKStep;
+    const int nstage = 6 * nkc;
+
+    // copy side: k-blocked operands Uq[36][cin_pad/64][cout_pad][64] and
+    // Vq[36][cin_pad/64][t_pad][64]; this wave's 16 rows, this lane's 16 bytes
+    const int grp = wave & 7, b0 = wave >> 3;
+    const bool copies_u = grp < 4;
+    const int rr = lane >> 2;
+    const uint32_t lane_off = (uint32_t)(rr * 64 + 16 * lds_slot(rr, lane & 3));
+    const long long tap_stride = copies_u ? (long long)g.cout_pad * g.cin_pad : g.t_pad * g.cin_pad;
+    const long long kc_stride = copies_u ? (long long)g.cout_pad * kKStep : g.t_pad * kKStep;
+    const int8_t* const src = (copies_u ? uq + (long long)(co_blk + 16 * grp) * kKStep
+                                        : vq + (tl_blk + 16 * (grp - 4)) * kKStep) +
+                              b0 * tap_stride;
+    uint8_t* const dst = lds + 1024 * grp + b0 * KR_CHUNK;
+    int next_a = 0, next_kc = 0, next_buf = 0;
+    auto issue_next = [&]() {
+        const int8_t* p = src + (long long)(6 * next_a) * tap_stride + next_kc * kc_stride;
+        uint8_t* d = dst + next_buf * KR_STAGE;
+        // Vq is read by each channel block once: non-temporal, so it does not
+        // push the small, hot Uq out of L2
+        if (copies_u) {
+#pragma unroll
+            for (int i = 0; i < KR_LPW; ++i)
+                __builtin_amdgcn_global_load_lds((const void*)(p + 2 * i * tap_stride + lane_off),
+                                                 (__attribute__((address_space(3))) void*)(d + 2 * i * KR_CHUNK), 16,
+                                                 0, 0);
+        } else {
+#pragma unroll
+            for (int i = 0; i < KR_LPW; ++i)
+                __builtin_amdgcn_global_load_lds((const void*)(p + 2 * i * tap_stride + lane_off),
+                                                 (__attribute__((address_space(3))) void*)(d + 2 * i * KR_CHUNK), 16,
+                                                 0, 2);
+        }
+        if (++next_kc == nkc) {
+            next_kc = 0;
+            ++next_a;
+        }
+        next_buf = next_buf == KR_NBUF - 1 ? 0 : next_buf + 1;
+    };
+
+    // compute side: fragment offsets within a slice
+    const int row_a = 16 * cw + lr, row_b = KR_CO + 16 * tw + lr;
+    const int frag_a = row_a * 64 + 16 * lds_slot(row_a, lk);
+    const int frag_b = row_b * 64 + 16 * lds_slot(row_b, lk);
+
+    // the lane's four channels; the rounding constant of the final shift
+    const int co0 = co_blk + 16 * cw + 4 * lk;
+    const int rnd = g.out_shift > 0 ? 1 << (g.out_shift - 1) : 0;
+
+    // Y of the lane's tile x 4 channels, 4x4 each
+    int yv[4][16];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int p = 0; p < 16; ++p) yv[r][p] = 0;
+
+    issue_next();
+    if (nstage > 1) issue_next();
+    int s = 0, buf = 0;
+#pragma unroll
+    for (int a = 0; a < 6; ++a) {
+        // bias plus rounding constant, injected through tap (1,1): its row
+        // and column of A^T are all ones, so it reaches every output of the
+        // tile once.  Loaded in the row that uses it.
+        v4i bias_rnd = (v4i){0, 0, 0, 0};
+        if (a == 1) bias_rnd = *(const v4i*)(bias + co0) + rnd;
+        v4i m[6];
+        // one stage: the six taps of row a, 64 input channels; the first
+        // k-chunk of the row starts the accumulators from zero
+        auto stage = [&](bool first) {
+            // stage s has landed once only the next stage's loads are pending
+            if (s + 1 < nstage)
+                WINO_WAIT_VM_LDS(KR_LPW);
+            else
+                WINO_WAIT_VM_LDS(0);
+            ring_barrier();   // stage s visible; stage s-1 (same buffer as s+2) consumed
+            if (s + 2 < nstage) issue_next();
+            const uint8_t* base = lds + buf * KR_STAGE;
+            buf = buf == KR_NBUF - 1 ? 0 : buf + 1;
+            ++s;
+            // fragments of two taps in flight ahead of the MFMAs
+            v4i fa[2], fb[2];
+            auto frag = [&](int b) {
+                fa[b & 1] = *(const v4i*)(base + b * KR_CHUNK + frag_a);
+                fb[b & 1] = *(const v4i*)(base + b * KR_CHUNK + frag_b);
+            };
+            frag(0);
+            frag(1);
+            const v4i zero = (v4i){0, 0, 0, 0};
+#pragma unroll
+            for (int b = 0; b < 6; ++b) {
+                m[b] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[b & 1], fb[b & 1], first ? zero : m[b], 0, 0, 0);
+                if (b + 2 < 6) frag(b + 2);
+            }
+            // keep that order (masks: 0x100 LDS read, 0x008 MFMA)
+            __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        };
+        stage(true);
+        for (int kc = 1; kc < nkc; ++kc) stage(false);
+
+        // fold row a: z = (M'[a, :]) A, then Y += A^T[:, a] z
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            int mv[6], z[4];
+#pragma unroll
+            for (int b = 0; b < 6; ++b) mv[b] = m[b][r] << g.tab.sh[6 * a + b];
+            if (a == 1) mv[1] += bias_rnd[r];
+            at_1d(mv, z);
+            int* yr = yv[r];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                // column a of A^T: 1 1 1 1 1 0 / 0 1 -1 2 -2 0 / 0 1 1 4 4 0 / 0 1 -1 8 -8 1
+                if (a < 5) yr[j] += z[j];
+                if (a == 1) { yr[4 + j] += z[j]; yr[8 + j] += z[j]; yr[12 + j] += z[j]; }
+                if (a == 2) { yr[4 + j] -= z[j]; yr[8 + j] += z[j]; yr[12 + j] -= z[j]; }
+                if (a == 3) { yr[4 + j] += z[j] << 1; yr[8 + j] += z[j] << 2; yr[12 + j] += z[j] << 3; }
+                if (a == 4) { yr[4 + j] -= z[j] << 1; yr[8 + j] += z[j] << 2; yr[12 + j] -= z[j] << 3; }
+                if (a == 5) yr[12 + j] += z[j];
+            }
+        }
+        // materialize Y here: Y is only read at the very end, and the
+        // compiler would otherwise sink the folds past the later rows and keep
+        // every row's accumulators live at once
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int p = 0; p < 16; ++p) asm volatile("" : "+v"(yv[r][p]));
+    }
+
+    store_tile<LAYOUT>(yv, g, y, co0, tl_blk + 16 * tw + lr);
+}
+
+// ---------------------------------------------------------------------------
 // host-side helpers
 // ---------------------------------------------------------------------------
+// compute units of the current device (the launch heuristics use it)
+int num_cus() {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+        return 256;
+    return n;
+}
+
 struct Geometry {
     int n, h, w, th, tw;
     long long ntiles, t_pad;
@@ -382,6 +682,21 @@ wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout la
     a.out_shift = p->out_shift;
     a.relu = p->relu;
     a.tab = tables_of(p);
+    if (MODE == 0 && p->epi_bits == 32 && p->tap_kernel != WINO_TAP_RESIDENT) {
+        const long long rblocks = (long long)(p->cout_pad / KR_CO) * (g.t_pad / KR_TL);
+        if (p->tap_kernel == WINO_TAP_ROWS || rblocks >= num_cus()) {
+            if (rblocks > 0x7fffffffll) return WINO_EUNSUPPORTED;
+            a.nbco = p->cout_pad / KR_CO;
+            a.nblocks = (int)rblocks;
+            if (layout == WINO_NHWC)
+                hipLaunchKernelGGL(wino_tap_gemm_rows<WINO_NHWC>, dim3((unsigned)rblocks), dim3(KR_THREADS), 0,
+                                   stream, p->uq_dev, vq, p->bias_dev, y, a);
+            else
+                hipLaunchKernelGGL(wino_tap_gemm_rows<WINO_NCHW>, dim3((unsigned)rblocks), dim3(KR_THREADS), 0,
+                                   stream, p->uq_dev, vq, p->bias_dev, y, a);
+            return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
+        }
+    }
     dim3 grid((unsigned)blocks), block(K2_THREADS);
 #define K2_LAUNCH(L, E)                                                                              \
     hipLaunchKernelGGL((wino_tap_gemm<L, E, MODE>), grid, block, 0, stream, p->uq_dev, vq, p->bias_dev, \

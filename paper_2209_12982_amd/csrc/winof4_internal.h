@@ -17,11 +17,13 @@ constexpr int kTilePad = 64;
 
 inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
-// Per-tap tables passed by value to the kernels (they land in the kernarg
-// segment and are read through scalar loads).
+// Per-tap tables passed by value to the kernels.  They land in the kernarg
+// segment; 32-bit entries keep every element 4-byte aligned, so the kernels
+// read them with scalar loads into scalar registers (byte entries are read
+// with vector loads and then occupy vector registers).
 struct TapTables {
-    int8_t eb[kTaps];   // input tap exponents e_B
-    int8_t sh[kTaps];   // alignment shifts e_B + e_G - e_o
+    int32_t eb[kTaps];   // input tap exponents e_B
+    int32_t sh[kTaps];   // alignment shifts e_B + e_G - e_o
 };
 
 }  // namespace winof4
@@ -32,6 +34,7 @@ struct wino_f4_plan_s {
     int32_t e_o;
     int32_t out_shift, relu;
     int32_t epi_bits;                 // 32 or 64
+    int32_t tap_kernel = WINO_TAP_AUTO;
     int32_t device;
     int8_t* uq_dev;                   // [36][cin_pad/64][cout_pad][64], zero padded
     int32_t* bias_dev;                // [cout_pad], zero padded

@@ -20,7 +20,7 @@ pytestmark = pytest.mark.gpu
 GOLDEN = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "configs.json")))
 
 
-def _run_layer(x, f, b, spec, rec, layout, variant=W.SPLIT):
+def _run_layer(x, f, b, spec, rec, layout, variant=W.SPLIT, tap_kernel=W.TAP_AUTO):
     torch = torch_dev()
     n, cin, h, w = x.shape
     xd = to_device(x, layout)
@@ -35,6 +35,7 @@ def _run_layer(x, f, b, spec, rec, layout, variant=W.SPLIT):
     else:
         s = spec.out_shift
     plan = W.wino_f4_plan(f, eb, bias=b, out_shift=s, relu=spec.relu)
+    W.wino_f4_plan_set_tap_kernel(plan, tap_kernel)
     shape = (n, spec.cout, h, w) if layout == W.NCHW else (n, h, w, spec.cout)
     y = torch.full(shape, 77, dtype=torch.int8, device="cuda")
     ws = workspace(plan, n, h, w, variant) if variant == W.SPLIT else None
@@ -47,16 +48,20 @@ def _run_layer(x, f, b, spec, rec, layout, variant=W.SPLIT):
     return yn
 
 
-@pytest.mark.parametrize("layout,variant", [(W.NHWC, W.SPLIT), (W.NCHW, W.SPLIT), (W.NHWC, W.FUSED)])
+RUNS = [(W.NHWC, W.SPLIT, W.TAP_AUTO), (W.NCHW, W.SPLIT, W.TAP_AUTO), (W.NHWC, W.FUSED, W.TAP_AUTO),
+        (W.NHWC, W.SPLIT, W.TAP_RESIDENT), (W.NCHW, W.SPLIT, W.TAP_ROWS)]
+
+
+@pytest.mark.parametrize("layout,variant,tap_kernel", RUNS)
 @pytest.mark.parametrize("name", ["C4", "C5"])
-def test_full_size_layer_bitexact(name, layout, variant):
+def test_full_size_layer_bitexact(name, layout, variant, tap_kernel):
     x, layers = workloads.generate(name)
     f, b, spec = layers[0]
-    _run_layer(x, f, b, spec, GOLDEN[name]["layers"][0], layout, variant)
+    _run_layer(x, f, b, spec, GOLDEN[name]["layers"][0], layout, variant, tap_kernel)
 
 
-@pytest.mark.parametrize("layout,variant", [(W.NHWC, W.SPLIT), (W.NCHW, W.SPLIT), (W.NHWC, W.FUSED)])
-def test_c3_chain_bitexact(layout, variant):
+@pytest.mark.parametrize("layout,variant,tap_kernel", RUNS)
+def test_c3_chain_bitexact(layout, variant, tap_kernel):
     """Four chained layers; each layer's input is the GPU's own previous
     output (max-pooled where the stage halves the image), and every layer
     must match the oracle's chain byte for byte."""
@@ -65,4 +70,4 @@ def test_c3_chain_bitexact(layout, variant):
     for k, (f, b, spec) in enumerate(layers):
         if k > 0:
             cur = workloads.next_layer_input(cur, spec)
-        cur = _run_layer(cur, f, b, spec, GOLDEN["C3"]["layers"][k], layout, variant)
+        cur = _run_layer(cur, f, b, spec, GOLDEN["C3"]["layers"][k], layout, variant, tap_kernel)

@@ -84,6 +84,45 @@ def test_conv_bitexact_random(shape, layout, relu, out_shift, variant):
     assert (y == ref).all(), f"{(y != ref).sum()} mismatches"
 
 
+# shapes for the row-streamed tap GEMM: 1..5 k-chunks of 64 input channels,
+# ragged tile counts and channel counts that leave partial 64-blocks
+ROWS_SHAPES = SHAPES + [
+    (1, 256, 200, 21, 26),
+    (2, 192, 64, 9, 40),
+    (1, 320, 128, 16, 16),
+    (3, 128, 72, 14, 14),
+]
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("shape", ROWS_SHAPES)
+@pytest.mark.parametrize("relu,out_shift", [(False, 9), (True, 12), (False, 0)])
+def test_conv_rows_kernel_bitexact(shape, layout, relu, out_shift):
+    """The row-streamed tap GEMM, forced on shapes the automatic choice
+    would give to the tap-resident kernel."""
+    n, cin, cout, h, w = shape
+    x, f, b = workloads.random_case(5, n, cin, cout, h, w, signed=True)
+    eb = tapwise.calibrate_input_exps(x)
+    gp, op = _plan_pair(f, eb, b, out_shift, relu)
+    W.wino_f4_plan_set_tap_kernel(gp, W.TAP_ROWS)
+    y = run_conv(gp, x, layout, W.SPLIT)
+    ref = tapwise.conv_int8(x, op)
+    assert (y == ref).all(), f"{(y != ref).sum()} mismatches"
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_tap_kernels_agree(layout):
+    """Both tap-GEMM kernels on one plan, two calls each, equal to the oracle."""
+    n, cin, cout, h, w = 2, 128, 128, 40, 36
+    x, f, b = workloads.random_case(8, n, cin, cout, h, w, signed=False, zero_frac=0.5)
+    eb = tapwise.calibrate_input_exps(x)
+    gp, op = _plan_pair(f, eb, b, 11, False)
+    ref = tapwise.conv_int8(x, op)
+    for kind in (W.TAP_ROWS, W.TAP_RESIDENT, W.TAP_ROWS, W.TAP_AUTO):
+        W.wino_f4_plan_set_tap_kernel(gp, kind)
+        assert (run_conv(gp, x, layout, W.SPLIT) == ref).all(), f"tap kernel {kind}"
+
+
 @pytest.mark.parametrize("variant", VARIANTS)
 @pytest.mark.parametrize("layout", LAYOUTS)
 def test_fused_equals_split_unaligned_channels(layout, variant):

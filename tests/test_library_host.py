@@ -103,6 +103,7 @@ def test_invalid_arguments_return_status():
     assert lib.wino_f4_conv_int8(None, None, None, 1, 4, 4, 0, 0, None, 0, None) == -1
     assert lib.wino_f4_workspace_bytes(None, 1, 4, 4, 0) == 0
     assert lib.wino_f4_plan_info(None, None, None, None, None, None, None, None) == -1
+    assert lib.wino_f4_plan_set_tap_kernel(None, 0) == -1
     assert lib.direct_conv_int8(None, None, None, None, 1, 1, 1, 1, 1, 0, 0, 0, None) == -1
     x = np.zeros(16, np.int8)
     # bad layout / shift / relu / sizes are rejected before any launch
