@@ -189,6 +189,7 @@ struct K2Args {
     long long ntiles, t_pad;
     int nbco, nblocks;
     int out_shift, relu;
+    int y_staged;              // row-streamed kernel: stage NHWC output through LDS
     TapTables tab;
 };
 
@@ -351,15 +352,15 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
 // ---------------------------------------------------------------------------
 constexpr int KR_CO = 64;
 constexpr int KR_TL = 64;
-constexpr int KR_THREADS = 1024;
-constexpr int KR_WAVES = KR_THREADS / 64;
 constexpr int KR_CHUNK = (KR_CO + KR_TL) * kKStep;      // one tap, one k-chunk
 constexpr int KR_STAGE = 6 * KR_CHUNK;                  // one row of taps
 constexpr int KR_NBUF = 3;
+constexpr int KR_TB = 1;                                // 16x16 tile blocks per wave
+constexpr int KR_WAVES = 16 / KR_TB;
+constexpr int KR_THREADS = 64 * KR_WAVES;
 constexpr int KR_LPW = KR_STAGE / 1024 / KR_WAVES;      // 1-KB loads per wave per stage
-static_assert(KR_LPW == 3, "each wave copies one 16-row group of three slices");
-static_assert((KR_CO + KR_TL) / 16 == 8 && KR_WAVES == 16, "wave -> (group, slice parity) map");
-static_assert((KR_CO / 16) * (KR_TL / 16) == KR_WAVES, "one 16x16 block per wave");
+static_assert((KR_CO + KR_TL) / 16 == 8 && KR_WAVES % 8 == 0, "wave -> (row group, slices) map");
+static_assert((KR_CO / 16) * (KR_TL / 16) == KR_WAVES * KR_TB, "the waves' blocks tile the workgroup block");
 static_assert(KR_NBUF * KR_STAGE <= 160 * 1024, "LDS");
 static_assert(KR_CO % kCoutPad == 0 || kCoutPad % KR_CO == 0, "channel blocks tile the padded channels");
 static_assert(kTilePad % KR_TL == 0, "tile blocks tile the padded tiles");
@@ -447,6 +448,8 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
 
     // copy side: k-blocked operands Uq[36][cin_pad/64][cout_pad][64] and
     // Vq[36][cin_pad/64][t_pad][64]; this wave's 16 rows, this lane's 16 bytes
+    // of slices b0, b0 + step, ...
+    constexpr int step = KR_WAVES / 8;
     const int grp = wave & 7, b0 = wave >> 3;
     const bool copies_u = grp < 4;
     const int rr = lane >> 2;
@@ -461,21 +464,15 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
     auto issue_next = [&]() {
         const int8_t* p = src + (long long)(6 * next_a) * tap_stride + next_kc * kc_stride;
         uint8_t* d = dst + next_buf * KR_STAGE;
-        // Vq is read by each channel block once: non-temporal, so it does not
-        // push the small, hot Uq out of L2
-        if (copies_u) {
+        // plain (temporal) loads for Vq too: the four channel blocks of one
+        // tile block run side by side on one XCD (consecutive logical ids)
+        // and share that L2's copy; measured, a non-temporal hint on Vq made
+        // the later readers go back to memory and cost 8%
 #pragma unroll
-            for (int i = 0; i < KR_LPW; ++i)
-                __builtin_amdgcn_global_load_lds((const void*)(p + 2 * i * tap_stride + lane_off),
-                                                 (__attribute__((address_space(3))) void*)(d + 2 * i * KR_CHUNK), 16,
-                                                 0, 0);
-        } else {
-#pragma unroll
-            for (int i = 0; i < KR_LPW; ++i)
-                __builtin_amdgcn_global_load_lds((const void*)(p + 2 * i * tap_stride + lane_off),
-                                                 (__attribute__((address_space(3))) void*)(d + 2 * i * KR_CHUNK), 16,
-                                                 0, 2);
-        }
+        for (int i = 0; i < KR_LPW; ++i)
+            __builtin_amdgcn_global_load_lds((const void*)(p + step * i * tap_stride + lane_off),
+                                             (__attribute__((address_space(3))) void*)(d + step * i * KR_CHUNK), 16,
+                                             0, 0);
         if (++next_kc == nkc) {
             next_kc = 0;
             ++next_a;
@@ -484,20 +481,22 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
     };
 
     // compute side: fragment offsets within a slice
-    const int row_a = 16 * cw + lr, row_b = KR_CO + 16 * tw + lr;
+    const int row_a = 16 * cw + lr, row_b = KR_CO + 16 * KR_TB * tw + lr;
     const int frag_a = row_a * 64 + 16 * lds_slot(row_a, lk);
-    const int frag_b = row_b * 64 + 16 * lds_slot(row_b, lk);
+    const int frag_b = row_b * 64 + 16 * lds_slot(row_b, lk);   // block tb: + 16 tb rows
 
     // the lane's four channels; the rounding constant of the final shift
     const int co0 = co_blk + 16 * cw + 4 * lk;
     const int rnd = g.out_shift > 0 ? 1 << (g.out_shift - 1) : 0;
 
-    // Y of the lane's tile x 4 channels, 4x4 each
-    int yv[4][16];
+    // Y of the lane's KR_TB tiles x 4 channels, 4x4 each
+    int yv[KR_TB][4][16];
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+    for (int tb = 0; tb < KR_TB; ++tb)
 #pragma unroll
-        for (int p = 0; p < 16; ++p) yv[r][p] = 0;
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int p = 0; p < 16; ++p) yv[tb][r][p] = 0;
 
     issue_next();
     if (nstage > 1) issue_next();
@@ -509,7 +508,7 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
         // tile once.  Loaded in the row that uses it.
         v4i bias_rnd = (v4i){0, 0, 0, 0};
         if (a == 1) bias_rnd = *(const v4i*)(bias + co0) + rnd;
-        v4i m[6];
+        v4i m[6][KR_TB];
         // one stage: the six taps of row a, 64 input channels; the first
         // k-chunk of the row starts the accumulators from zero
         auto stage = [&](bool first) {
@@ -524,40 +523,47 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
             buf = buf == KR_NBUF - 1 ? 0 : buf + 1;
             ++s;
             // fragments of two taps in flight ahead of the MFMAs
-            v4i fa[2], fb[2];
+            v4i fa[2], fb[2][KR_TB];
             auto frag = [&](int b) {
                 fa[b & 1] = *(const v4i*)(base + b * KR_CHUNK + frag_a);
-                fb[b & 1] = *(const v4i*)(base + b * KR_CHUNK + frag_b);
+#pragma unroll
+                for (int tb = 0; tb < KR_TB; ++tb)
+                    fb[b & 1][tb] = *(const v4i*)(base + b * KR_CHUNK + frag_b + 16 * 64 * tb);
             };
             frag(0);
             frag(1);
             const v4i zero = (v4i){0, 0, 0, 0};
 #pragma unroll
             for (int b = 0; b < 6; ++b) {
-                m[b] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[b & 1], fb[b & 1], first ? zero : m[b], 0, 0, 0);
+#pragma unroll
+                for (int tb = 0; tb < KR_TB; ++tb)
+                    m[b][tb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[b & 1], fb[b & 1][tb], first ? zero : m[b][tb],
+                                                                     0, 0, 0);
                 if (b + 2 < 6) frag(b + 2);
             }
             // keep that order (masks: 0x100 LDS read, 0x008 MFMA)
-            __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 2 * (1 + KR_TB), 0);
 #pragma unroll
             for (int b = 0; b < 4; ++b) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, KR_TB, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1 + KR_TB, 0);
             }
-            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 2 * KR_TB, 0);
         };
         stage(true);
         for (int kc = 1; kc < nkc; ++kc) stage(false);
 
         // fold row a: z = (M'[a, :]) A, then Y += A^T[:, a] z
 #pragma unroll
+        for (int tb = 0; tb < KR_TB; ++tb)
+#pragma unroll
         for (int r = 0; r < 4; ++r) {
             int mv[6], z[4];
 #pragma unroll
-            for (int b = 0; b < 6; ++b) mv[b] = m[b][r] << g.tab.sh[6 * a + b];
+            for (int b = 0; b < 6; ++b) mv[b] = m[b][tb][r] << g.tab.sh[6 * a + b];
             if (a == 1) mv[1] += bias_rnd[r];
             at_1d(mv, z);
-            int* yr = yv[r];
+            int* yr = yv[tb][r];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 // column a of A^T: 1 1 1 1 1 0 / 0 1 -1 2 -2 0 / 0 1 1 4 4 0 / 0 1 -1 8 -8 1
@@ -573,12 +579,53 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
         // compiler would otherwise sink the folds past the later rows and keep
         // every row's accumulators live at once
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
+        for (int tb = 0; tb < KR_TB; ++tb)
 #pragma unroll
-            for (int p = 0; p < 16; ++p) asm volatile("" : "+v"(yv[r][p]));
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int p = 0; p < 16; ++p) asm volatile("" : "+v"(yv[tb][r][p]));
     }
 
-    store_tile<LAYOUT>(yv, g, y, co0, tl_blk + 16 * tw + lr);
+    if (LAYOUT == WINO_NHWC && g.y_staged) {
+        // NHWC with whole 64-channel blocks: gather the block's output in
+        // LDS (the ring is idle now) so every pixel's 64 channel bytes leave
+        // as four 16-byte stores of adjacent lanes -- 64-byte write requests
+        // instead of 16-byte pieces scattered over 16 lines per instruction
+        constexpr int PITCH = 16 * 64 + 16;   // bytes per tile; the pad spreads lanes over banks
+        static_assert(KR_TL * PITCH <= KR_NBUF * KR_STAGE, "output staging fits the ring");
+        const int s = g.out_shift, lo = g.relu ? 0 : -128;
+        __syncthreads();                      // every wave is done reading the ring
+#pragma unroll
+        for (int tb = 0; tb < KR_TB; ++tb) {
+            uint8_t* ot = lds + (16 * (KR_TB * tw + tb) + lr) * PITCH + 16 * cw + 4 * lk;
+#pragma unroll
+            for (int p = 0; p < 16; ++p) {
+                uint32_t pk = put_byte<0>(0u, (uint32_t)med3_i32(yv[tb][0][p] >> s, lo, 127));
+                pk = put_byte<1>(pk, (uint32_t)med3_i32(yv[tb][1][p] >> s, lo, 127));
+                pk = put_byte<2>(pk, (uint32_t)med3_i32(yv[tb][2][p] >> s, lo, 127));
+                pk = put_byte<3>(pk, (uint32_t)med3_i32(yv[tb][3][p] >> s, lo, 127));
+                *(uint32_t*)(ot + 64 * p) = pk;
+            }
+        }
+        __syncthreads();
+        // wave w copies tiles w, w + 16, ...: lane = 16-byte quarter q of pixel p
+        const int p = lane >> 2, q = lane & 3;
+        for (int tl = wave; tl < KR_TL; tl += KR_WAVES) {
+            const long long tile = tl_blk + tl;   // wave-uniform
+            if (tile >= g.ntiles) break;
+            const int img = (int)(tile / ((long long)g.th * g.tw));
+            const int trem = (int)(tile - (long long)img * g.th * g.tw);
+            const int ty = trem / g.tw, tx = trem - ty * g.tw;
+            const int yy = 4 * ty + (p >> 2), xx = 4 * tx + (p & 3);
+            if (yy < g.h && xx < g.w) {
+                const uint4 v = *(const uint4*)(lds + tl * PITCH + 64 * p + 16 * q);
+                *(uint4*)(y + (((long long)img * g.h + yy) * g.w + xx) * g.cout + co_blk + 16 * q) = v;
+            }
+        }
+        return;
+    }
+#pragma unroll
+    for (int tb = 0; tb < KR_TB; ++tb) store_tile<LAYOUT>(yv[tb], g, y, co0, tl_blk + 16 * (KR_TB * tw + tb) + lr);
 }
 
 // ---------------------------------------------------------------------------
@@ -681,6 +728,7 @@ wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout la
     a.nblocks = (int)blocks;
     a.out_shift = p->out_shift;
     a.relu = p->relu;
+    a.y_staged = layout == WINO_NHWC && p->cout % KR_CO == 0 && ((uintptr_t)y & 15) == 0;
     a.tab = tables_of(p);
     if (MODE == 0 && p->epi_bits == 32 && p->tap_kernel != WINO_TAP_RESIDENT) {
         const long long rblocks = (long long)(p->cout_pad / KR_CO) * (g.t_pad / KR_TL);
