@@ -157,6 +157,12 @@ def main():
     # launches
     th, tw = (h + 3) // 4, (w + 3) // 4
     T = n * th * tw
+    lay = 1 if layout == W.NHWC else 0
+    rows = W.wino_f4_tap_kernel_choice(plan, n, h, w) == W.TAP_ROWS
+    # kernel names as the profiler shows them (template arguments included)
+    k1_name, k1_inst = "wino_input_xform", f"wino_input_xform<{lay},0>"
+    k2_name = "wino_tap_gemm_rows" if rows else "wino_tap_gemm"
+    k2_inst = f"wino_tap_gemm_rows<{lay}>" if rows else f"wino_tap_gemm<{lay},{info['epilogue_bits']},0>"
     k1_ms = k2_ms = None
     if variant == W.SPLIT:
         k1_ms = time_loop(torch, lambda: W.wino_f4_input_transform(plan, xd, n, h, w, layout, ws), args.steps)
@@ -169,28 +175,23 @@ def main():
     k2_bytes = 36 * T * cin + 36 * cin * cout + n * h * w * cout + 4 * cout
     kernels = {}
     if k1_ms is not None:
-        kernels["wino_input_xform"] = {"ms": k1_ms, "bound": "hbm", "bytes": k1_bytes,
-                                       "GB/s": k1_bytes / (k1_ms * 1e-3) / 1e9,
-                                       "frac": k1_bytes / (k1_ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
-        kernels["wino_tap_gemm"] = {"ms": k2_ms, "bound": "mfma", "ops": tap_ops,
-                                    "TOP/s": tap_ops / (k2_ms * 1e-3) / 1e12,
-                                    "frac": tap_ops / (k2_ms * 1e-3) / 1e12 / PEAK_INT8_TOPS,
-                                    "GB/s_algorithmic": k2_bytes / (k2_ms * 1e-3) / 1e9}
-        dom = "wino_tap_gemm" if k2_ms >= k1_ms else "wino_input_xform"
-        # template arguments of the timed instantiation: <layout, epilogue bits, mode 0>
-        inst = f"{dom}<{1 if layout == W.NHWC else 0},{info['epilogue_bits']},0>" if dom == "wino_tap_gemm" \
-            else f"{dom}<{1 if layout == W.NHWC else 0},0>"
-        traffic = counter_traffic(args.config, args.layout, inst)
-        for name in kernels:
-            ik = f"{name}<{1 if layout == W.NHWC else 0},{info['epilogue_bits']},0>" if name == "wino_tap_gemm" \
-                else f"{name}<{1 if layout == W.NHWC else 0},0>"
-            kernels[name]["traffic_bytes"] = counter_traffic(args.config, args.layout, ik)
-        if dom == "wino_tap_gemm":
-            roofline = {"kernel": dom, "bound": "mfma", "achieved": kernels[dom]["TOP/s"],
-                        "peak": PEAK_INT8_TOPS, "unit": "TOP/s", "frac": kernels[dom]["frac"], "traffic": traffic}
+        kernels[k1_name] = {"ms": k1_ms, "bound": "hbm", "bytes": k1_bytes,
+                            "GB/s": k1_bytes / (k1_ms * 1e-3) / 1e9,
+                            "frac": k1_bytes / (k1_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                            "traffic_bytes": counter_traffic(args.config, args.layout, k1_inst)}
+        kernels[k2_name] = {"ms": k2_ms, "bound": "mfma", "ops": tap_ops,
+                            "TOP/s": tap_ops / (k2_ms * 1e-3) / 1e12,
+                            "frac": tap_ops / (k2_ms * 1e-3) / 1e12 / PEAK_INT8_TOPS,
+                            "GB/s_algorithmic": k2_bytes / (k2_ms * 1e-3) / 1e9,
+                            "traffic_bytes": counter_traffic(args.config, args.layout, k2_inst)}
+        if k2_ms >= k1_ms:
+            roofline = {"kernel": k2_name, "bound": "mfma", "achieved": kernels[k2_name]["TOP/s"],
+                        "peak": PEAK_INT8_TOPS, "unit": "TOP/s", "frac": kernels[k2_name]["frac"],
+                        "traffic": kernels[k2_name]["traffic_bytes"]}
         else:
-            roofline = {"kernel": dom, "bound": "hbm", "achieved": kernels[dom]["GB/s"],
-                        "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": kernels[dom]["frac"], "traffic": traffic}
+            roofline = {"kernel": k1_name, "bound": "hbm", "achieved": kernels[k1_name]["GB/s"],
+                        "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": kernels[k1_name]["frac"],
+                        "traffic": kernels[k1_name]["traffic_bytes"]}
     else:
         roofline = {"kernel": "wino_fused", "bound": "mfma", "achieved": tap_ops / (ms * 1e-3) / 1e12,
                     "peak": PEAK_INT8_TOPS, "unit": "TOP/s",

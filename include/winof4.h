@@ -128,6 +128,16 @@ wino_status wino_f4_plan_tables(const float* w_oihw, int32_t cin, int32_t cout, 
  */
 wino_status wino_f4_plan_set_tap_kernel(wino_f4_plan_t plan, int32_t kind);
 
+/*
+ * wino_f4_tap_kernel_choice -- the tap-GEMM kernel (WINO_TAP_RESIDENT or
+ * WINO_TAP_ROWS) that a SPLIT wino_f4_conv_int8 with this plan runs for an
+ * n x h x w input, under the plan's wino_f4_plan_set_tap_kernel setting.
+ * Host only, no device work.  kind: host int32 out.
+ * Errors: WINO_EINVAL (null plan or kind, negative sizes), WINO_EUNSUPPORTED
+ * (sizes beyond the library's limits).
+ */
+wino_status wino_f4_tap_kernel_choice(wino_f4_plan_t plan, int32_t n, int32_t h, int32_t w, int32_t* kind);
+
 /* Releases a plan and its device memory.  NULL is ignored.  The caller must
  * ensure no convolution using the plan is still running. */
 void wino_f4_plan_destroy(wino_f4_plan_t plan);

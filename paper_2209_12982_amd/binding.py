@@ -16,8 +16,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB = None
 
 EXPORTS = [
-    "wino_f4_plan", "wino_f4_plan_tables", "wino_f4_plan_destroy", "wino_f4_plan_info", "wino_f4_plan_set_tap_kernel",
-    "wino_f4_workspace_bytes",
+    "wino_f4_plan", "wino_f4_plan_tables", "wino_f4_plan_destroy", "wino_f4_plan_info",
+    "wino_f4_plan_set_tap_kernel", "wino_f4_tap_kernel_choice", "wino_f4_workspace_bytes",
     "wino_f4_conv_int8", "wino_f4_input_transform", "wino_f4_tap_gemm", "wino_f4_calibrate_input", "wino_f4_calibrate_output",
     "wino_f4_debug_input_transform", "wino_f4_debug_tap_gemm",
     "direct_conv_quantize_weights", "direct_conv_int8", "wino_strerror",
@@ -54,6 +54,7 @@ def load_library():
         "wino_f4_plan_destroy": (None, [P]),
         "wino_f4_plan_info": (I32, [P, P, P, P, P, P, P, P]),
         "wino_f4_plan_set_tap_kernel": (I32, [P, I32]),
+        "wino_f4_tap_kernel_choice": (I32, [P, I32, I32, I32, P]),
         "wino_f4_workspace_bytes": (SZ, [P, I32, I32, I32, I32]),
         "wino_f4_conv_int8": (I32, [P, P, P, I32, I32, I32, I32, I32, P, SZ, P]),
         "wino_f4_input_transform": (I32, [P, P, I32, I32, I32, I32, P, SZ, P]),
@@ -193,6 +194,14 @@ def wino_f4_plan_set_tap_kernel(plan, kind):
     """TAP_AUTO, TAP_RESIDENT or TAP_ROWS: the tap-GEMM kernel of later SPLIT
     convolutions with this plan."""
     _check(load_library().wino_f4_plan_set_tap_kernel(plan.handle, int(kind)), "wino_f4_plan_set_tap_kernel")
+
+
+def wino_f4_tap_kernel_choice(plan, n, h, w):
+    """TAP_RESIDENT or TAP_ROWS: the tap-GEMM kernel a SPLIT convolution runs."""
+    kind = ctypes.c_int32()
+    _check(load_library().wino_f4_tap_kernel_choice(plan.handle, n, h, w, ctypes.byref(kind)),
+           "wino_f4_tap_kernel_choice")
+    return kind.value
 
 
 def wino_f4_workspace_bytes(plan, n, h, w, variant=SPLIT):

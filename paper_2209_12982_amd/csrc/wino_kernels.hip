@@ -23,6 +23,7 @@
 // runs in 32-bit integers when the plan's bound proves every partial sum fits,
 // otherwise in 64-bit.
 #include <algorithm>
+#include <atomic>
 #include "wino_device.h"
 
 using namespace winof4;
@@ -631,12 +632,15 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
 // ---------------------------------------------------------------------------
 // host-side helpers
 // ---------------------------------------------------------------------------
-// compute units of the current device (the launch heuristics use it)
+// compute units of the current device (the launch heuristics use it),
+// queried once per device
 int num_cus() {
+    static std::atomic<int> cached[64] = {};
     int dev = 0, n = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-        return 256;
+    if (hipGetDevice(&dev) != hipSuccess) return 256;
+    if (dev >= 0 && dev < 64 && (n = cached[dev].load(std::memory_order_relaxed)) > 0) return n;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 256;
+    if (dev >= 0 && dev < 64) cached[dev].store(n, std::memory_order_relaxed);
     return n;
 }
 
@@ -706,6 +710,16 @@ wino_status launch_k1(const K1Args& a, wino_layout layout, const int8_t* x, int8
     return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
 }
 
+// Whether an output convolution (MODE 0) runs the row-streamed tap GEMM: it
+// needs the 32-bit epilogue; AUTO takes it when its 64x64 blocks fill the
+// device (below that the 64x32 blocks of the tap-resident kernel spread the
+// work over more compute units).
+bool use_rows(const wino_f4_plan_s* p, const Geometry& g) {
+    if (p->epi_bits != 32 || p->tap_kernel == WINO_TAP_RESIDENT) return false;
+    if (p->tap_kernel == WINO_TAP_ROWS) return true;
+    return (long long)(p->cout_pad / KR_CO) * (g.t_pad / KR_TL) >= num_cus();
+}
+
 template <int MODE>
 wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout layout, const int8_t* vq,
                       int8_t* y, void* aux, hipStream_t stream) {
@@ -730,9 +744,9 @@ wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout la
     a.relu = p->relu;
     a.y_staged = layout == WINO_NHWC && p->cout % KR_CO == 0 && ((uintptr_t)y & 15) == 0;
     a.tab = tables_of(p);
-    if (MODE == 0 && p->epi_bits == 32 && p->tap_kernel != WINO_TAP_RESIDENT) {
+    if (MODE == 0 && use_rows(p, g)) {
         const long long rblocks = (long long)(p->cout_pad / KR_CO) * (g.t_pad / KR_TL);
-        if (p->tap_kernel == WINO_TAP_ROWS || rblocks >= num_cus()) {
+        {
             if (rblocks > 0x7fffffffll) return WINO_EUNSUPPORTED;
             a.nbco = p->cout_pad / KR_CO;
             a.nblocks = (int)rblocks;
@@ -785,6 +799,16 @@ extern "C" size_t wino_f4_workspace_bytes(wino_f4_plan_t p, int32_t n, int32_t h
 // FUSED is served by the kernel in wino_fused.hip.
 wino_status wino_f4_conv_fused(const wino_f4_plan_s* p, const int8_t* x, int8_t* y, int n, int h, int w,
                                wino_layout layout, hipStream_t stream);
+
+extern "C" wino_status wino_f4_tap_kernel_choice(wino_f4_plan_t p, int32_t n, int32_t h, int32_t w,
+                                                 int32_t* kind) {
+    if (!p || !kind) return WINO_EINVAL;
+    Geometry g;
+    const wino_status st = geometry(n, h, w, g);
+    if (st != WINO_OK) return st;
+    *kind = use_rows(p, g) ? WINO_TAP_ROWS : WINO_TAP_RESIDENT;
+    return WINO_OK;
+}
 
 extern "C" wino_status wino_f4_conv_int8(wino_f4_plan_t p, const int8_t* x, int8_t* y, int32_t n,
                                          int32_t h, int32_t w, wino_layout layout, wino_variant variant,

@@ -110,6 +110,28 @@ def test_conv_rows_kernel_bitexact(shape, layout, relu, out_shift):
     assert (y == ref).all(), f"{(y != ref).sum()} mismatches"
 
 
+def test_tap_kernel_choice():
+    torch_dev()
+    f = np.random.default_rng(9).normal(0, 0.05, (256, 256, 3, 3)).astype(np.float32)
+    plan = W.wino_f4_plan(f, [4] * 36, bias=None, out_shift=11)
+    # 4 x 160 x 160: 400 blocks of 64 x 64 fill the device; 1 x 56 x 56: 4 do not
+    assert W.wino_f4_tap_kernel_choice(plan, 4, 160, 160) == W.TAP_ROWS
+    assert W.wino_f4_tap_kernel_choice(plan, 1, 56, 56) == W.TAP_RESIDENT
+    W.wino_f4_plan_set_tap_kernel(plan, W.TAP_RESIDENT)
+    assert W.wino_f4_tap_kernel_choice(plan, 4, 160, 160) == W.TAP_RESIDENT
+    W.wino_f4_plan_set_tap_kernel(plan, W.TAP_ROWS)
+    assert W.wino_f4_tap_kernel_choice(plan, 1, 56, 56) == W.TAP_ROWS
+    with pytest.raises(W.WinoError):
+        W.wino_f4_tap_kernel_choice(plan, -1, 8, 8)
+    # the 64-bit epilogue always runs the tap-resident kernel
+    eb = [0] * 36
+    eb[35], eb[0] = 15, 14
+    p64 = W.wino_f4_plan(f[:24, :20], eb, bias=None, out_shift=20)
+    assert W.wino_f4_plan_info(p64)["epilogue_bits"] == 64
+    W.wino_f4_plan_set_tap_kernel(p64, W.TAP_ROWS)
+    assert W.wino_f4_tap_kernel_choice(p64, 4, 160, 160) == W.TAP_RESIDENT
+
+
 @pytest.mark.parametrize("layout", LAYOUTS)
 def test_tap_kernels_agree(layout):
     """Both tap-GEMM kernels on one plan, two calls each, equal to the oracle."""
