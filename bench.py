@@ -87,6 +87,31 @@ def time_loop(torch, fn, steps):
     return s.elapsed_time(e) / steps
 
 
+def time_calls(torch, fn, calls):
+    """Per-call GPU duration: an event pair on the launch stream around each
+    call, so host-side call overhead between calls is not counted (it is for
+    short kernels in a back-to-back loop).  Returns (median, p10, p90) ms."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(calls)]
+    torch.cuda.synchronize()
+    for s, e in ev:
+        s.record()
+        fn()
+        e.record()
+    torch.cuda.synchronize()
+    t = sorted(s.elapsed_time(e) for s, e in ev)
+    q = lambda f: t[min(len(t) - 1, int(f * (len(t) - 1) + 0.5))]
+    return q(0.5), q(0.1), q(0.9)
+
+
+def kernel_ms(torch, fn, calls):
+    """A single-kernel call's duration: the smaller of the back-to-back loop
+    average (exact for long kernels, host-bound for short ones) and the
+    per-call event-pair median (exact for short kernels, plus the events' own
+    overhead for long ones); with the per-call p10 and p90."""
+    med, p10, p90 = time_calls(torch, fn, calls)
+    return min(med, time_loop(torch, fn, calls)), p10, p90
+
+
 def cpu_baseline(x, layers_plan, n_img, spec):
     """The oracle's online path (a-1 .. a-6, plan excluded) on the first
     n_img images of the same workload."""
@@ -151,10 +176,8 @@ def main():
     torch.cuda.synchronize()
     ms = time_loop(torch, step, args.steps)
 
-    # per-kernel durations: each of the two launches of a step timed in a
-    # back-to-back loop of its own (HIP events on the launch stream), so the
-    # average is the kernel's duration plus only the gap between identical
-    # launches
+    # per-kernel durations: each of the two launches of a step timed on its
+    # own (HIP events on the launch stream), see kernel_ms
     th, tw = (h + 3) // 4, (w + 3) // 4
     T = n * th * tw
     lay = 1 if layout == W.NHWC else 0
@@ -165,8 +188,10 @@ def main():
     k2_inst = f"wino_tap_gemm_rows<{lay}>" if rows else f"wino_tap_gemm<{lay},{info['epilogue_bits']},0>"
     k1_ms = k2_ms = None
     if variant == W.SPLIT:
-        k1_ms = time_loop(torch, lambda: W.wino_f4_input_transform(plan, xd, n, h, w, layout, ws), args.steps)
-        k2_ms = time_loop(torch, lambda: W.wino_f4_tap_gemm(plan, ws, y, n, h, w, layout), args.steps)
+        k1 = lambda: W.wino_f4_input_transform(plan, xd, n, h, w, layout, ws)
+        k2 = lambda: W.wino_f4_tap_gemm(plan, ws, y, n, h, w, layout)
+        k1_ms, k1_p10, k1_p90 = kernel_ms(torch, k1, args.steps)
+        k2_ms, k2_p10, k2_p90 = kernel_ms(torch, k2, args.steps)
 
     direct_ops = 2.0 * 9 * n * h * w * cin * cout
     tap_ops = 2.0 * 36 * T * cin * cout
@@ -175,11 +200,11 @@ def main():
     k2_bytes = 36 * T * cin + 36 * cin * cout + n * h * w * cout + 4 * cout
     kernels = {}
     if k1_ms is not None:
-        kernels[k1_name] = {"ms": k1_ms, "bound": "hbm", "bytes": k1_bytes,
+        kernels[k1_name] = {"ms": k1_ms, "p10_ms": k1_p10, "p90_ms": k1_p90, "bound": "hbm", "bytes": k1_bytes,
                             "GB/s": k1_bytes / (k1_ms * 1e-3) / 1e9,
                             "frac": k1_bytes / (k1_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
                             "traffic_bytes": counter_traffic(args.config, args.layout, k1_inst)}
-        kernels[k2_name] = {"ms": k2_ms, "bound": "mfma", "ops": tap_ops,
+        kernels[k2_name] = {"ms": k2_ms, "p10_ms": k2_p10, "p90_ms": k2_p90, "bound": "mfma", "ops": tap_ops,
                             "TOP/s": tap_ops / (k2_ms * 1e-3) / 1e12,
                             "frac": tap_ops / (k2_ms * 1e-3) / 1e12 / PEAK_INT8_TOPS,
                             "GB/s_algorithmic": k2_bytes / (k2_ms * 1e-3) / 1e9,
@@ -209,8 +234,8 @@ def main():
 
         for _ in range(max(2, args.warmup // 2)):
             dstep()
-        dms = time_loop(torch, dstep, max(5, args.steps // 2))
-        direct = {"ms": dms, "TOPS": direct_ops / (dms * 1e-3) / 1e12, "speedup": dms / ms,
+        dms, d10, d90 = kernel_ms(torch, dstep, max(5, args.steps // 2))
+        direct = {"ms": dms, "p10_ms": d10, "p90_ms": d90, "TOPS": direct_ops / (dms * 1e-3) / 1e12, "speedup": dms / ms,
                   "mfma_frac": direct_ops / (dms * 1e-3) / 1e12 / PEAK_INT8_TOPS}
 
     cpu = None
