@@ -61,14 +61,22 @@ typedef enum wino_variant { WINO_SPLIT = 0, WINO_FUSED = 1 } wino_variant;
 
 typedef struct wino_f4_plan_s* wino_f4_plan_t;   /* opaque, immutable after creation */
 
-/* Which kernel runs the tap GEMM of the SPLIT variant (both give the same,
- * exact result).  RESIDENT keeps all 36 tap accumulators of a 64-channel x
- * 32-tile block in registers and applies the output transform once at the
- * end; ROWS streams the taps one row of the 6x6 tile at a time and folds
- * each row into the output as it completes, which allows 64 x 64 blocks.
- * AUTO picks ROWS when its blocks fill the device and the 32-bit epilogue
- * applies, else RESIDENT.                                                  */
-typedef enum wino_tap_kernel { WINO_TAP_AUTO = 0, WINO_TAP_RESIDENT = 1, WINO_TAP_ROWS = 2 } wino_tap_kernel;
+/* Which kernel runs the tap GEMM of the SPLIT variant (all give the same,
+ * exact result).  RESIDENT keeps all 36 tap accumulators of its block in
+ * registers and applies the output transform once at the end, with blocks of
+ * 64 channels x 32 tiles (RESIDENT, RESIDENT_64X32), 32 x 32 or 16 x 16 (the
+ * _NxM values force a shape).  ROWS streams the taps one row of the 6x6 tile
+ * at a time and folds each row into the output as it completes, which allows
+ * 64 x 64 blocks.  AUTO picks ROWS when its blocks fill the device and the
+ * 32-bit epilogue applies, else RESIDENT_64X32.                             */
+typedef enum wino_tap_kernel {
+    WINO_TAP_AUTO = 0,
+    WINO_TAP_RESIDENT = 1,
+    WINO_TAP_ROWS = 2,
+    WINO_TAP_RESIDENT_64X32 = 3,
+    WINO_TAP_RESIDENT_32X32 = 4,
+    WINO_TAP_RESIDENT_16X16 = 5
+} wino_tap_kernel;
 
 /*
  * wino_f4_plan -- the offline step: weight transform U = G f G^T (Eq.
@@ -121,16 +129,17 @@ wino_status wino_f4_plan_tables(const float* w_oihw, int32_t cin, int32_t cout, 
 /*
  * wino_f4_plan_set_tap_kernel -- choose the tap-GEMM kernel (wino_tap_kernel)
  * for later SPLIT convolutions with this plan.  ROWS applies to output
- * convolutions with the 32-bit epilogue; calibration, debug exports and the
- * 64-bit epilogue always use RESIDENT.  Not to be called while a convolution
- * with the plan is being enqueued on another thread.
+ * convolutions with the 32-bit epilogue (else the RESIDENT choice is made);
+ * calibration and debug exports always use the 64 x 32 RESIDENT shape.  Not
+ * to be called while a convolution with the plan is being enqueued on
+ * another thread.
  * Errors: WINO_EINVAL (null plan, unknown kind).
  */
 wino_status wino_f4_plan_set_tap_kernel(wino_f4_plan_t plan, int32_t kind);
 
 /*
- * wino_f4_tap_kernel_choice -- the tap-GEMM kernel (WINO_TAP_RESIDENT or
- * WINO_TAP_ROWS) that a SPLIT wino_f4_conv_int8 with this plan runs for an
+ * wino_f4_tap_kernel_choice -- the tap-GEMM kernel (WINO_TAP_ROWS or one of
+ * the WINO_TAP_RESIDENT_* shapes) that a SPLIT wino_f4_conv_int8 runs for an
  * n x h x w input, under the plan's wino_f4_plan_set_tap_kernel setting.
  * Host only, no device work.  kind: host int32 out.
  * Errors: WINO_EINVAL (null plan or kind, negative sizes), WINO_EUNSUPPORTED

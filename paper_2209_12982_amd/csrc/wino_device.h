@@ -152,13 +152,15 @@ __device__ __forceinline__ void ring_barrier() {
     asm volatile("" ::: "memory");
 }
 
-// s_waitcnt vmcnt(n) leaving the other counters untouched (gfx9 encoding:
-// vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8]).
-#define WINO_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(0x0f70 | (n))
+// s_waitcnt vmcnt(n), 0 <= n <= 63, leaving the other counters untouched
+// (gfx9 encoding: vmcnt[3:0] and vmcnt[5:4] at bits 15:14, expcnt[6:4],
+// lgkmcnt[11:8]).
+#define WINO_VMCNT_BITS(n) ((((n) & 15)) | ((((n) >> 4) & 3) << 14))
+#define WINO_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(0x0f70 | WINO_VMCNT_BITS(n))
 // the same, and also every LDS read of this wave returned (lgkmcnt 0): a
 // ring stage's buffer is refilled right after the next barrier, so each wave
 // must be done reading it before it arrives there
-#define WINO_WAIT_VM_LDS(n) __builtin_amdgcn_s_waitcnt(0x0070 | (n))
+#define WINO_WAIT_VM_LDS(n) __builtin_amdgcn_s_waitcnt(0x0070 | WINO_VMCNT_BITS(n))
 
 // Epilogue of a 16-channel x 16-tile MFMA block holding all 36 taps: the
 // accumulator of tap t, register r, lane l is M_t[co_base + 4*(l/16) + r]

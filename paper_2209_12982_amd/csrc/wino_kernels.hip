@@ -153,36 +153,42 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
 // ---------------------------------------------------------------------------
 // K2: tap GEMM with fused output transform
 // ---------------------------------------------------------------------------
-// Workgroup = 8 waves computing 64 output channels x 32 tiles for all 36
-// taps; wave w owns channels 16*(w%4).. and tiles 16*(w/4).. (one 16x16
-// int8 MFMA block per tap, 36 x 4 int32 accumulators per lane).  The k loop
-// runs over input channels in steps of 64; each step is split into three tap
-// groups ("stages").  A stage's Uq slice (12 taps x 64 rows x 64 B) and Vq
-// slice (12 taps x 32 rows x 64 B) are copied global -> LDS by the
-// direct-to-LDS load (no VGPR staging), double buffered: the next stage
-// loads while this one feeds the MFMAs.  Measured on gfx950, the copy rate of
-// such a ring is set by the loads each wave issues per stage (one barrier
-// per stage): 3 per wave gave 26 B/clk per CU, 9 per wave 34 B/clk.  (Also
-// measured: two 4-wave workgroups per CU with 32x32 tiles were 1.4x slower
-// -- more L2 traffic, shallower rings.)  Every such load writes 1 KB of LDS
-// contiguously (16 bytes per lane); the 16-byte slot of a row holding input
-// bytes [16p, 16p+16) is p ^ ((row >> 1) & 3).  Measured on gfx950, this
-// swizzle lets the fragment reads (16 rows x one 16-byte part per 16 lanes)
-// run at the full 256 B/clk per CU; unswizzled or padded rows run 1.5x slower.
-constexpr int K2_CO = 64;               // output channels per workgroup
-constexpr int K2_TL = 32;               // tiles per workgroup
-constexpr int K2_THREADS = 512;         // waves: (K2_CO/16) x (K2_TL/16), each 16x16
-constexpr int K2_WAVES = K2_THREADS / 64;
-constexpr int K2_G = 12;                // taps per stage
-constexpr int K2_A_BYTES = K2_G * K2_CO * 64;
-constexpr int K2_B_BYTES = K2_G * K2_TL * 64;
-constexpr int K2_STAGE = K2_A_BYTES + K2_B_BYTES;
-constexpr int K2_KB = K2_STAGE / 1024;          // 1-KB load instructions per stage
-constexpr int K2_NBUF = 2;                      // double buffer: the next stage loads during this one
-constexpr int K2_PF = 6;                        // taps whose LDS fragments are in flight ahead
-constexpr int K2_LPW = (K2_KB + K2_WAVES - 1) / K2_WAVES;   // load instructions per wave per stage
-static_assert((K2_CO / 16) * (K2_TL / 16) == K2_WAVES, "one 16x16 block per wave");
-static_assert(K2_NBUF * K2_STAGE <= 160 * 1024, "LDS");
+// Workgroup = CW x TW waves computing 16*CW output channels x 16*TW tiles for
+// all 36 taps; wave w owns channels 16*(w%CW).. and tiles 16*(w/CW).. (one
+// 16x16 int8 MFMA block per tap, 36 x 4 int32 accumulators per lane).  The k
+// loop runs over input channels in steps of 64; each step is split into
+// three tap groups ("stages").  A stage's Uq slice (12 taps x 16*CW rows x
+// 64 B) and Vq slice (12 taps x 16*TW rows x 64 B) are copied global -> LDS
+// by the direct-to-LDS load (no VGPR staging) into a ring of NBUF stages, so
+// NBUF - 1 stages load while one feeds the MFMAs.  Every such load writes
+// 1 KB of LDS contiguously (16 bytes per lane); the 16-byte slot of a row
+// holding input bytes [16p, 16p+16) is p ^ ((row >> 1) & 3).  Measured on
+// gfx950, this swizzle lets the fragment reads (16 rows x one 16-byte part
+// per 16 lanes) run at the full 256 B/clk per CU; unswizzled or padded rows
+// run 1.5x slower.
+//
+// Three block shapes: 64x32 (8 waves, double buffer), the default; 32x32
+// (4 waves) and 16x16 (one wave) with 6-tap stages and rings small enough for
+// two and four workgroups per CU, selectable for small layers.
+template <int CW_, int TW_, int G_, int NBUF_>
+struct K2Cfg {
+    static constexpr int CW = CW_, TW = TW_, G = G_, NBUF = NBUF_;   // G: taps per stage
+    static constexpr int CO = 16 * CW, TL = 16 * TW;
+    static constexpr int WAVES = CW * TW, THREADS = 64 * WAVES;
+    static constexpr int A_BYTES = G * CO * 64, B_BYTES = G * TL * 64;
+    static constexpr int STAGE = A_BYTES + B_BYTES;
+    static constexpr int KB = STAGE / 1024;              // 1-KB load instructions per stage
+    static constexpr int LPW = (KB + WAVES - 1) / WAVES; // load instructions per wave per stage
+    static constexpr int PF = G / 2;                     // taps whose LDS fragments are in flight ahead
+    static_assert(NBUF * STAGE <= 160 * 1024, "LDS");
+    static_assert((NBUF - 2) * LPW <= 63, "vmcnt range");
+    static_assert(kTaps % G == 0 && G > PF, "stage shape");
+};
+// 64 x 32, one workgroup per CU; 32 x 32 and 16 x 16 with rings small
+// enough for two and four workgroups per CU
+using K2Big = K2Cfg<4, 2, 12, 2>;
+using K2Mid = K2Cfg<2, 2, 6, 3>;
+using K2Small = K2Cfg<1, 1, 6, 3>;
 
 struct K2Args {
     int cin_pad, cout, cout_pad;
@@ -196,20 +202,20 @@ struct K2Args {
 
 // MODE 0: store y.  MODE 1: max |Y + bias| into *zmax (calibration).
 // MODE 2: store raw M (debug export).
-template <int LAYOUT, int EPI, int MODE>
-__global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __restrict__ uq,
+template <class C, int LAYOUT, int EPI, int MODE>
+__global__ __launch_bounds__(C::THREADS) void wino_tap_gemm(const int8_t* __restrict__ uq,
                                                             const int8_t* __restrict__ vq,
                                                             const int32_t* __restrict__ bias,
                                                             int8_t* __restrict__ y,
                                                             void* __restrict__ aux, K2Args g) {
-    __shared__ __attribute__((aligned(1024))) uint8_t lds[K2_NBUF * K2_STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[C::NBUF * C::STAGE];
     const int lbid = xcd_remap(blockIdx.x, g.nblocks);
     const int bco = lbid % g.nbco, btl = lbid / g.nbco;
     const int tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
-    const int cw = wave % (K2_CO / 16), tw = wave / (K2_CO / 16);
-    const int co_blk = bco * K2_CO;
-    const long long tl_blk = (long long)btl * K2_TL;
+    const int cw = wave % C::CW, tw = wave / C::CW;
+    const int co_blk = bco * C::CO;
+    const long long tl_blk = (long long)btl * C::TL;
     const int co_base = co_blk + 16 * cw;
     const long long tl_base = tl_blk + 16 * tw;
     const int lr = lane & 15, lk = lane >> 4;
@@ -229,34 +235,35 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
     const int wv_id = __builtin_amdgcn_readfirstlane(wave);
     const int rr = lane >> 2;
     const int lane_off = rr * 64 + 16 * lds_slot(rr, lane & 3);
-    long long ubase[K2_LPW];
-    int dst[K2_LPW];
-    bool isa[K2_LPW];
+    long long ubase[C::LPW];
+    int dst[C::LPW];
+    bool isa[C::LPW];
 #pragma unroll
-    for (int i = 0; i < K2_LPW; ++i) {
+    for (int i = 0; i < C::LPW; ++i) {
         // when the stage's loads do not split evenly, the last round repeats
         // an earlier load (same bytes to the same place)
-        int j = wv_id + K2_WAVES * i;
-        if (j >= K2_KB) j -= K2_WAVES;
-        isa[i] = j < K2_A_BYTES / 1024;
+        int j = wv_id + C::WAVES * i;
+        if (j >= C::KB) j -= C::WAVES;
+        isa[i] = j < C::A_BYTES / 1024;
         if (isa[i]) {
-            const int u = j / (K2_CO / 16), q = j % (K2_CO / 16);
+            const int u = j / C::CW, q = j % C::CW;
             ubase[i] = u * sa + (long long)(co_blk + 16 * q) * kKStep;
         } else {
-            const int jj = j - K2_A_BYTES / 1024;
-            const int u = jj / (K2_TL / 16), q = jj % (K2_TL / 16);
+            const int jj = j - C::A_BYTES / 1024;
+            const int u = jj / C::TW, q = jj % C::TW;
             ubase[i] = u * sb + (tl_blk + 16 * q) * kKStep;
         }
         dst[i] = j * 1024;
     }
+    constexpr int GPS = kTaps / C::G;                  // stages per k-chunk
     const int nkc = g.cin_pad / kKStep;
-    const int nstage = nkc * (kTaps / K2_G);
+    const int nstage = nkc * GPS;
     auto issue = [&](int st) {
-        const int kc = st / (kTaps / K2_G), grp = st - kc * (kTaps / K2_G);
-        uint8_t* base = lds + (st % K2_NBUF) * K2_STAGE;
+        const int kc = st / GPS, grp = st - kc * GPS;
+        uint8_t* base = lds + (st % C::NBUF) * C::STAGE;
 #pragma unroll
-        for (int i = 0; i < K2_LPW; ++i) {
-            const long long off = ubase[i] + (long long)(K2_G * grp) * (isa[i] ? sa : sb) + kc * (isa[i] ? ka : kb);
+        for (int i = 0; i < C::LPW; ++i) {
+            const long long off = ubase[i] + (long long)(C::G * grp) * (isa[i] ? sa : sb) + kc * (isa[i] ? ka : kb);
             // Vq is streamed once per output-channel block: non-temporal, so it
             // does not push the small, hot Uq out of L2
             if (isa[i])
@@ -275,49 +282,54 @@ __global__ __launch_bounds__(K2_THREADS) void wino_tap_gemm(const int8_t* __rest
     // fragment offsets within a stage buffer (tap u adds u * rows * 64)
     const int row_a = 16 * cw + lr, row_b = 16 * tw + lr;
     const int frag_a = row_a * 64 + 16 * lds_slot(row_a, lk);
-    const int frag_b = K2_A_BYTES + row_b * 64 + 16 * lds_slot(row_b, lk);
+    const int frag_b = C::A_BYTES + row_b * 64 + 16 * lds_slot(row_b, lk);
 
-    for (int st = 0; st < K2_NBUF - 1 && st < nstage; ++st) issue(st);
+    for (int st = 0; st < C::NBUF - 1 && st < nstage; ++st) issue(st);
     for (int kc = 0; kc < nkc; ++kc) {
 #pragma unroll
-        for (int grp = 0; grp < kTaps / K2_G; ++grp) {
-            const int st = kc * (kTaps / K2_G) + grp;
-            const int ahead = nstage - 1 - st;        // stages issued after this one
-            static_assert(K2_NBUF == 2, "stage st is the newest issued when it is waited for");
-            (void)ahead;
-            WINO_WAIT_VM_LDS(0);
+        for (int grp = 0; grp < GPS; ++grp) {
+            const int st = kc * GPS + grp;
+            // stage st has landed once only the stages issued after it are
+            // pending: min(NBUF - 2, nstage - 1 - st) of them, LPW loads each
+            const int ahead = min(C::NBUF - 2, nstage - 1 - st);
+            if (C::NBUF >= 4 && ahead >= 2)
+                WINO_WAIT_VM_LDS(2 * C::LPW);
+            else if (C::NBUF >= 3 && ahead >= 1)
+                WINO_WAIT_VM_LDS(C::LPW);
+            else
+                WINO_WAIT_VM_LDS(0);
             ring_barrier();                              // stage st visible; stage st-1 consumed
-            if (st + K2_NBUF - 1 < nstage) issue(st + K2_NBUF - 1);
-            const uint8_t* base = lds + (st % K2_NBUF) * K2_STAGE;
-            // software pipeline over the stage's taps: fragments of K2_PF taps
+            if (st + C::NBUF - 1 < nstage) issue(st + C::NBUF - 1);
+            const uint8_t* base = lds + (st % C::NBUF) * C::STAGE;
+            // software pipeline over the stage's taps: fragments of PF taps
             // are in flight ahead of the MFMA that consumes the oldest, so the
             // LDS read latency hides behind MFMAs
-            v4i fa[K2_PF], fb[K2_PF];
+            v4i fa[C::PF], fb[C::PF];
 #pragma unroll
-            for (int u = 0; u < K2_PF; ++u) {
-                fa[u] = *(const v4i*)(base + frag_a + u * K2_CO * 64);
-                fb[u] = *(const v4i*)(base + frag_b + u * K2_TL * 64);
+            for (int u = 0; u < C::PF; ++u) {
+                fa[u] = *(const v4i*)(base + frag_a + u * C::CO * 64);
+                fb[u] = *(const v4i*)(base + frag_b + u * C::TL * 64);
             }
 #pragma unroll
-            for (int u = 0; u < K2_G; ++u) {
-                const int slot = u % K2_PF;
-                acc[K2_G * grp + u] =
-                    __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[slot], fb[slot], acc[K2_G * grp + u], 0, 0, 0);
-                if (u + K2_PF < K2_G) {
-                    fa[slot] = *(const v4i*)(base + frag_a + (u + K2_PF) * K2_CO * 64);
-                    fb[slot] = *(const v4i*)(base + frag_b + (u + K2_PF) * K2_TL * 64);
+            for (int u = 0; u < C::G; ++u) {
+                const int slot = u % C::PF;
+                acc[C::G * grp + u] =
+                    __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[slot], fb[slot], acc[C::G * grp + u], 0, 0, 0);
+                if (u + C::PF < C::G) {
+                    fa[slot] = *(const v4i*)(base + frag_a + (u + C::PF) * C::CO * 64);
+                    fb[slot] = *(const v4i*)(base + frag_b + (u + C::PF) * C::TL * 64);
                 }
             }
             // keep that order: the scheduler would otherwise pull the reads
             // next to their MFMAs to save registers (masks: 0x100 LDS read,
             // 0x008 MFMA)
-            __builtin_amdgcn_sched_group_barrier(0x100, 2 * K2_PF, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::PF, 0);
 #pragma unroll
-            for (int u = 0; u < K2_G - K2_PF; ++u) {
+            for (int u = 0; u < C::G - C::PF; ++u) {
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
                 __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
             }
-            __builtin_amdgcn_sched_group_barrier(0x008, K2_PF, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, C::PF, 0);
         }
     }
 
@@ -710,19 +722,54 @@ wino_status launch_k1(const K1Args& a, wino_layout layout, const int8_t* x, int8
     return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
 }
 
-// Whether an output convolution (MODE 0) runs the row-streamed tap GEMM: it
-// needs the 32-bit epilogue; AUTO takes it when its 64x64 blocks fill the
-// device (below that the 64x32 blocks of the tap-resident kernel spread the
-// work over more compute units).
-bool use_rows(const wino_f4_plan_s* p, const Geometry& g) {
-    if (p->epi_bits != 32 || p->tap_kernel == WINO_TAP_RESIDENT) return false;
-    if (p->tap_kernel == WINO_TAP_ROWS) return true;
-    return (long long)(p->cout_pad / KR_CO) * (g.t_pad / KR_TL) >= num_cus();
+template <class C>
+long long resident_blocks(const wino_f4_plan_s* p, const Geometry& g) {
+    return (long long)(p->cout_pad / C::CO) * ((g.ntiles + C::TL - 1) / C::TL);
+}
+
+// The tap-GEMM kernel of a convolution (a wino_tap_kernel value other than
+// AUTO and RESIDENT).  The row-streamed kernel needs the 32-bit epilogue and
+// an output convolution; AUTO takes it when its 64x64 blocks fill the device.
+// Otherwise the 64x32 tap-resident shape: on the small layers where too few
+// blocks exist the smaller shapes were measured no faster (C1-C3: 14-16 us
+// against 11-14 us), as the time there is the serial chain of ring-stage
+// latencies and the epilogue inside each block, not the block count.
+// Calibration and debug exports (MODE 1, 2) always use the 64x32 shape.
+int tap_kernel_for(const wino_f4_plan_s* p, const Geometry& g, int mode) {
+    const int k = p->tap_kernel;
+    if (mode != 0) return WINO_TAP_RESIDENT_64X32;
+    if (k == WINO_TAP_RESIDENT_64X32 || k == WINO_TAP_RESIDENT_32X32 || k == WINO_TAP_RESIDENT_16X16) return k;
+    if (p->epi_bits == 32 && k != WINO_TAP_RESIDENT &&
+        (k == WINO_TAP_ROWS || (long long)(p->cout_pad / KR_CO) * (g.t_pad / KR_TL) >= num_cus()))
+        return WINO_TAP_ROWS;
+    return WINO_TAP_RESIDENT_64X32;
+}
+
+template <class C, int MODE>
+wino_status launch_resident(const wino_f4_plan_s* p, const Geometry& g, wino_layout layout, const int8_t* vq,
+                            int8_t* y, void* aux, K2Args a, hipStream_t stream) {
+    const long long blocks = resident_blocks<C>(p, g);
+    if (blocks == 0) return WINO_OK;
+    if (blocks > 0x7fffffffll) return WINO_EUNSUPPORTED;
+    a.nbco = p->cout_pad / C::CO;
+    a.nblocks = (int)blocks;
+    dim3 grid((unsigned)blocks), block(C::THREADS);
+#define K2_LAUNCH(L, E)                                                                              \
+    hipLaunchKernelGGL((wino_tap_gemm<C, L, E, MODE>), grid, block, 0, stream, p->uq_dev, vq, p->bias_dev, \
+                       y, aux, a)
+    if (layout == WINO_NHWC) {
+        if (p->epi_bits == 32) K2_LAUNCH(WINO_NHWC, 32); else K2_LAUNCH(WINO_NHWC, 64);
+    } else {
+        if (p->epi_bits == 32) K2_LAUNCH(WINO_NCHW, 32); else K2_LAUNCH(WINO_NCHW, 64);
+    }
+#undef K2_LAUNCH
+    return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
 }
 
 template <int MODE>
 wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout layout, const int8_t* vq,
                       int8_t* y, void* aux, hipStream_t stream) {
+    if (g.ntiles == 0) return WINO_OK;
     K2Args a;
     a.cin_pad = p->cin_pad;
     a.cout = p->cout;
@@ -734,19 +781,13 @@ wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout la
     a.tw = g.tw;
     a.ntiles = g.ntiles;
     a.t_pad = g.t_pad;
-    a.nbco = p->cout_pad / K2_CO;
-    long long nbtl = (g.ntiles + K2_TL - 1) / K2_TL;
-    long long blocks = nbtl * a.nbco;
-    if (blocks == 0) return WINO_OK;
-    if (blocks > 0x7fffffffll) return WINO_EUNSUPPORTED;
-    a.nblocks = (int)blocks;
     a.out_shift = p->out_shift;
     a.relu = p->relu;
     a.y_staged = layout == WINO_NHWC && p->cout % KR_CO == 0 && ((uintptr_t)y & 15) == 0;
     a.tab = tables_of(p);
-    if (MODE == 0 && use_rows(p, g)) {
-        const long long rblocks = (long long)(p->cout_pad / KR_CO) * (g.t_pad / KR_TL);
-        {
+    switch (tap_kernel_for(p, g, MODE)) {
+        case WINO_TAP_ROWS: {
+            const long long rblocks = (long long)(p->cout_pad / KR_CO) * (g.t_pad / KR_TL);
             if (rblocks > 0x7fffffffll) return WINO_EUNSUPPORTED;
             a.nbco = p->cout_pad / KR_CO;
             a.nblocks = (int)rblocks;
@@ -758,18 +799,16 @@ wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout la
                                    stream, p->uq_dev, vq, p->bias_dev, y, a);
             return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
         }
+        case WINO_TAP_RESIDENT_32X32:
+            if constexpr (MODE == 0) return launch_resident<K2Mid, MODE>(p, g, layout, vq, y, aux, a, stream);
+            break;
+        case WINO_TAP_RESIDENT_16X16:
+            if constexpr (MODE == 0) return launch_resident<K2Small, MODE>(p, g, layout, vq, y, aux, a, stream);
+            break;
+        default:
+            break;
     }
-    dim3 grid((unsigned)blocks), block(K2_THREADS);
-#define K2_LAUNCH(L, E)                                                                              \
-    hipLaunchKernelGGL((wino_tap_gemm<L, E, MODE>), grid, block, 0, stream, p->uq_dev, vq, p->bias_dev, \
-                       y, aux, a)
-    if (layout == WINO_NHWC) {
-        if (p->epi_bits == 32) K2_LAUNCH(WINO_NHWC, 32); else K2_LAUNCH(WINO_NHWC, 64);
-    } else {
-        if (p->epi_bits == 32) K2_LAUNCH(WINO_NCHW, 32); else K2_LAUNCH(WINO_NCHW, 64);
-    }
-#undef K2_LAUNCH
-    return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
+    return launch_resident<K2Big, MODE>(p, g, layout, vq, y, aux, a, stream);
 }
 
 wino_status check_common(const wino_f4_plan_s* p, const void* x, int32_t n, int32_t h, int32_t w,
@@ -806,7 +845,7 @@ extern "C" wino_status wino_f4_tap_kernel_choice(wino_f4_plan_t p, int32_t n, in
     Geometry g;
     const wino_status st = geometry(n, h, w, g);
     if (st != WINO_OK) return st;
-    *kind = use_rows(p, g) ? WINO_TAP_ROWS : WINO_TAP_RESIDENT;
+    *kind = tap_kernel_for(p, g, 0);
     return WINO_OK;
 }
 

@@ -116,11 +116,14 @@ def test_tap_kernel_choice():
     plan = W.wino_f4_plan(f, [4] * 36, bias=None, out_shift=11)
     # 4 x 160 x 160: 400 blocks of 64 x 64 fill the device; 1 x 56 x 56: 4 do not
     assert W.wino_f4_tap_kernel_choice(plan, 4, 160, 160) == W.TAP_ROWS
-    assert W.wino_f4_tap_kernel_choice(plan, 1, 56, 56) == W.TAP_RESIDENT
+    assert W.wino_f4_tap_kernel_choice(plan, 1, 56, 56) == W.TAP_RESIDENT_64X32
     W.wino_f4_plan_set_tap_kernel(plan, W.TAP_RESIDENT)
-    assert W.wino_f4_tap_kernel_choice(plan, 4, 160, 160) == W.TAP_RESIDENT
+    assert W.wino_f4_tap_kernel_choice(plan, 4, 160, 160) == W.TAP_RESIDENT_64X32
     W.wino_f4_plan_set_tap_kernel(plan, W.TAP_ROWS)
     assert W.wino_f4_tap_kernel_choice(plan, 1, 56, 56) == W.TAP_ROWS
+    for kind in (W.TAP_RESIDENT_64X32, W.TAP_RESIDENT_32X32, W.TAP_RESIDENT_16X16):
+        W.wino_f4_plan_set_tap_kernel(plan, kind)
+        assert W.wino_f4_tap_kernel_choice(plan, 4, 160, 160) == kind
     with pytest.raises(W.WinoError):
         W.wino_f4_tap_kernel_choice(plan, -1, 8, 8)
     # the 64-bit epilogue always runs the tap-resident kernel
@@ -129,7 +132,36 @@ def test_tap_kernel_choice():
     p64 = W.wino_f4_plan(f[:24, :20], eb, bias=None, out_shift=20)
     assert W.wino_f4_plan_info(p64)["epilogue_bits"] == 64
     W.wino_f4_plan_set_tap_kernel(p64, W.TAP_ROWS)
-    assert W.wino_f4_tap_kernel_choice(p64, 4, 160, 160) == W.TAP_RESIDENT
+    assert W.wino_f4_tap_kernel_choice(p64, 4, 160, 160) == W.TAP_RESIDENT_64X32
+
+
+@pytest.mark.parametrize("kind", [W.TAP_RESIDENT_32X32, W.TAP_RESIDENT_16X16])
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("shape", SHAPES + [(1, 256, 200, 21, 26), (2, 192, 48, 9, 40)])
+@pytest.mark.parametrize("relu,out_shift", [(False, 9), (True, 0)])
+def test_conv_resident_shapes_bitexact(shape, layout, relu, out_shift, kind):
+    """The small-layer block shapes of the tap-resident kernel, forced."""
+    n, cin, cout, h, w = shape
+    x, f, b = workloads.random_case(5, n, cin, cout, h, w, signed=True)
+    eb = tapwise.calibrate_input_exps(x)
+    gp, op = _plan_pair(f, eb, b, out_shift, relu)
+    W.wino_f4_plan_set_tap_kernel(gp, kind)
+    y = run_conv(gp, x, layout, W.SPLIT)
+    ref = tapwise.conv_int8(x, op)
+    assert (y == ref).all(), f"{(y != ref).sum()} mismatches"
+
+
+@pytest.mark.parametrize("kind", [W.TAP_RESIDENT_32X32, W.TAP_RESIDENT_16X16])
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_conv_resident_shapes_int64(layout, kind):
+    n, cin, cout, h, w = 1, 20, 24, 11, 10
+    x, f, b = workloads.random_case(6, n, cin, cout, h, w, signed=True)
+    eb = [0] * 36
+    eb[35], eb[0] = 15, 14
+    gp, op = _plan_pair(f, eb, b, 20, False)
+    assert W.wino_f4_plan_info(gp)["epilogue_bits"] == 64
+    W.wino_f4_plan_set_tap_kernel(gp, kind)
+    assert (run_conv(gp, x, layout, W.SPLIT) == tapwise.conv_int8(x, op)).all()
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
@@ -140,7 +172,8 @@ def test_tap_kernels_agree(layout):
     eb = tapwise.calibrate_input_exps(x)
     gp, op = _plan_pair(f, eb, b, 11, False)
     ref = tapwise.conv_int8(x, op)
-    for kind in (W.TAP_ROWS, W.TAP_RESIDENT, W.TAP_ROWS, W.TAP_AUTO):
+    for kind in (W.TAP_ROWS, W.TAP_RESIDENT, W.TAP_RESIDENT_16X16, W.TAP_ROWS, W.TAP_RESIDENT_32X32,
+                 W.TAP_RESIDENT_64X32, W.TAP_AUTO):
         W.wino_f4_plan_set_tap_kernel(gp, kind)
         assert (run_conv(gp, x, layout, W.SPLIT) == ref).all(), f"tap kernel {kind}"
 
