@@ -147,6 +147,25 @@ wino_status wino_f4_plan_set_tap_kernel(wino_f4_plan_t plan, int32_t kind);
  */
 wino_status wino_f4_tap_kernel_choice(wino_f4_plan_t plan, int32_t n, int32_t h, int32_t w, int32_t* kind);
 
+/*
+ * wino_f2_plan, wino_f2_plan_tables -- the same offline step for Winograd
+ * F(2x2, 3x3) (Sec. II: B^T, G = Gint / 2 and A^T of the F2 algorithm; the
+ * tap-wise scheme of Sec. III with 16 taps, t = 4a + b).  Arguments, errors
+ * and exactness as for the F4 functions, except that in_exp, w_exp, e_g and
+ * sh have 16 entries and uq is [16][cin][cout].  The resulting plan runs 4x4
+ * input tiles at stride 2 and 2x2 output tiles through the same execution
+ * entry points (wino_f4_conv_int8 SPLIT, wino_f4_workspace_bytes,
+ * wino_f4_input_transform, wino_f4_tap_gemm, wino_f4_calibrate_output, the
+ * debug exports and wino_f4_plan_info, whose table arguments then hold 16
+ * entries); the FUSED variant returns WINO_EUNSUPPORTED for it.
+ */
+wino_status wino_f2_plan(wino_f4_plan_t* out, const float* w_oihw, int32_t cin, int32_t cout,
+                         const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                         int32_t out_shift, int32_t relu, hipStream_t stream);
+wino_status wino_f2_plan_tables(const float* w_oihw, int32_t cin, int32_t cout, const int8_t* in_exp,
+                                const int8_t* w_exp, const int32_t* bias, int32_t out_shift, int8_t* e_g,
+                                int8_t* sh, int32_t* e_o, int32_t* epilogue_bits, int8_t* uq);
+
 /* Releases a plan and its device memory.  NULL is ignored.  The caller must
  * ensure no convolution using the plan is still running. */
 void wino_f4_plan_destroy(wino_f4_plan_t plan);
@@ -221,6 +240,12 @@ wino_status wino_f4_tap_gemm(wino_f4_plan_t plan, const void* workspace, size_t 
  * Allocates and frees a small device buffer (an offline step).
  */
 wino_status wino_f4_calibrate_input(const int8_t* x, int32_t n, int32_t cin, int32_t h,
+                                    int32_t w, wino_layout layout, int32_t* absmax,
+                                    int8_t* e_b, hipStream_t stream);
+
+/* wino_f2_calibrate_input -- the same for F(2x2, 3x3): 4x4 tiles at stride
+ * 2, absmax and e_b with 16 entries. */
+wino_status wino_f2_calibrate_input(const int8_t* x, int32_t n, int32_t cin, int32_t h,
                                     int32_t w, wino_layout layout, int32_t* absmax,
                                     int8_t* e_b, hipStream_t stream);
 

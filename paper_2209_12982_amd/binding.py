@@ -18,6 +18,7 @@ _LIB = None
 
 EXPORTS = [
     "wino_f4_plan", "wino_f4_plan_tables", "wino_f4_plan_destroy", "wino_f4_plan_info",
+    "wino_f2_plan", "wino_f2_plan_tables", "wino_f2_calibrate_input",
     "wino_f4_plan_set_tap_kernel", "wino_f4_tap_kernel_choice", "wino_f4_workspace_bytes",
     "wino_f4_conv_int8", "wino_f4_input_transform", "wino_f4_tap_gemm", "wino_f4_calibrate_input", "wino_f4_calibrate_output",
     "wino_f4_debug_input_transform", "wino_f4_debug_tap_gemm",
@@ -52,6 +53,9 @@ def load_library():
     sig = {
         "wino_f4_plan": (I32, [P, P, I32, I32, P, P, P, I32, I32, P]),
         "wino_f4_plan_tables": (I32, [P, I32, I32, P, P, P, I32, P, P, P, P, P]),
+        "wino_f2_plan": (I32, [P, P, I32, I32, P, P, P, I32, I32, P]),
+        "wino_f2_plan_tables": (I32, [P, I32, I32, P, P, P, I32, P, P, P, P, P]),
+        "wino_f2_calibrate_input": (I32, [P, I32, I32, I32, I32, I32, P, P, P]),
         "wino_f4_plan_destroy": (None, [P]),
         "wino_f4_plan_info": (I32, [P, P, P, P, P, P, P, P]),
         "wino_f4_plan_set_tap_kernel": (I32, [P, I32]),
@@ -118,12 +122,15 @@ def _host(a, dtype, n=None):
 
 
 class WinoF4Plan:
-    """Owns a wino_f4_plan_t; destroyed with the object or by close()."""
+    """Owns a wino_f4_plan_t (from wino_f4_plan, m = 4, or wino_f2_plan,
+    m = 2); destroyed with the object or by close()."""
 
-    def __init__(self, handle, cin, cout):
+    def __init__(self, handle, cin, cout, m=4):
         self.handle = handle
         self.cin = cin
         self.cout = cout
+        self.m = m
+        self.ntap = (m + 2) * (m + 2)
 
     def close(self):
         if self.handle:
@@ -137,53 +144,71 @@ class WinoF4Plan:
             pass
 
 
-def wino_f4_plan(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0, relu=False, stream=None):
-    lib = load_library()
+def _make_plan(fn, m, w_oihw, in_exp, w_exp, bias, out_shift, relu, stream):
+    ntap = (m + 2) * (m + 2)
     w = _host(w_oihw, np.float32)
     cout, cin = w.shape[:2]
-    eb = _host(in_exp, np.int8, TAPS)
-    eg = None if w_exp is None else _host(w_exp, np.int8, TAPS)
+    eb = _host(in_exp, np.int8, ntap)
+    eg = None if w_exp is None else _host(w_exp, np.int8, ntap)
     b = None if bias is None else _host(bias, np.int32, cout)
     h = ctypes.c_void_p()
-    st = lib.wino_f4_plan(ctypes.byref(h), w.ctypes.data, cin, cout, eb.ctypes.data,
-                          None if eg is None else eg.ctypes.data,
-                          None if b is None else b.ctypes.data, int(out_shift), int(bool(relu)),
-                          _stream(stream))
-    _check(st, "wino_f4_plan")
-    return WinoF4Plan(h, cin, cout)
+    st = getattr(load_library(), fn)(ctypes.byref(h), w.ctypes.data, cin, cout, eb.ctypes.data,
+                                     None if eg is None else eg.ctypes.data,
+                                     None if b is None else b.ctypes.data, int(out_shift), int(bool(relu)),
+                                     _stream(stream))
+    _check(st, fn)
+    return WinoF4Plan(h, cin, cout, m)
+
+
+def wino_f4_plan(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0, relu=False, stream=None):
+    return _make_plan("wino_f4_plan", 4, w_oihw, in_exp, w_exp, bias, out_shift, relu, stream)
+
+
+def wino_f2_plan(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0, relu=False, stream=None):
+    """F(2x2, 3x3) plan: 16-entry in_exp / w_exp."""
+    return _make_plan("wino_f2_plan", 2, w_oihw, in_exp, w_exp, bias, out_shift, relu, stream)
+
+
+def _plan_tables(fn, m, w_oihw, in_exp, w_exp, bias, out_shift):
+    ntap = (m + 2) * (m + 2)
+    w = _host(w_oihw, np.float32)
+    cout, cin = w.shape[:2]
+    eb = _host(in_exp, np.int8, ntap)
+    eg_in = None if w_exp is None else _host(w_exp, np.int8, ntap)
+    b = None if bias is None else _host(bias, np.int32, cout)
+    eg = np.zeros(ntap, np.int8)
+    sh = np.zeros(ntap, np.int8)
+    eo = ctypes.c_int32()
+    bits = ctypes.c_int32()
+    uq = np.zeros((ntap, cin, cout), np.int8)
+    st = getattr(load_library(), fn)(w.ctypes.data, cin, cout, eb.ctypes.data,
+                                     None if eg_in is None else eg_in.ctypes.data,
+                                     None if b is None else b.ctypes.data, int(out_shift),
+                                     eg.ctypes.data, sh.ctypes.data, ctypes.byref(eo), ctypes.byref(bits),
+                                     uq.ctypes.data)
+    _check(st, fn)
+    return dict(e_g=eg.astype(int).tolist(), sh=sh.astype(int).tolist(), e_o=eo.value,
+                epilogue_bits=bits.value, uq=uq)
 
 
 def wino_f4_plan_tables(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0):
     """Host-only plan arithmetic (no GPU): dict with e_g, sh, e_o,
     epilogue_bits and uq [36][cin][cout]."""
-    lib = load_library()
-    w = _host(w_oihw, np.float32)
-    cout, cin = w.shape[:2]
-    eb = _host(in_exp, np.int8, TAPS)
-    eg_in = None if w_exp is None else _host(w_exp, np.int8, TAPS)
-    b = None if bias is None else _host(bias, np.int32, cout)
-    eg = np.zeros(TAPS, np.int8)
-    sh = np.zeros(TAPS, np.int8)
-    eo = ctypes.c_int32()
-    bits = ctypes.c_int32()
-    uq = np.zeros((TAPS, cin, cout), np.int8)
-    st = lib.wino_f4_plan_tables(w.ctypes.data, cin, cout, eb.ctypes.data,
-                                 None if eg_in is None else eg_in.ctypes.data,
-                                 None if b is None else b.ctypes.data, int(out_shift),
-                                 eg.ctypes.data, sh.ctypes.data, ctypes.byref(eo), ctypes.byref(bits),
-                                 uq.ctypes.data)
-    _check(st, "wino_f4_plan_tables")
-    return dict(e_g=eg.astype(int).tolist(), sh=sh.astype(int).tolist(), e_o=eo.value,
-                epilogue_bits=bits.value, uq=uq)
+    return _plan_tables("wino_f4_plan_tables", 4, w_oihw, in_exp, w_exp, bias, out_shift)
+
+
+def wino_f2_plan_tables(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0):
+    """The same for F(2x2, 3x3): 16 taps."""
+    return _plan_tables("wino_f2_plan_tables", 2, w_oihw, in_exp, w_exp, bias, out_shift)
 
 
 def wino_f4_plan_info(plan, with_uq=False):
     lib = load_library()
-    eg = np.zeros(TAPS, np.int8)
-    sh = np.zeros(TAPS, np.int8)
+    eg = np.zeros(plan.ntap, np.int8)
+    sh = np.zeros(plan.ntap, np.int8)
     eo = ctypes.c_int32()
     bits = ctypes.c_int32()
-    uq = np.zeros((TAPS, plan.cin, plan.cout), np.int8) if with_uq else None
+    uq = np.zeros((plan.ntap, plan.cin, plan.cout), np.int8) if with_uq else None
     st = lib.wino_f4_plan_info(plan.handle, eg.ctypes.data, sh.ctypes.data, ctypes.byref(eo),
                                ctypes.byref(bits), None if uq is None else uq.ctypes.data, None, None)
     _check(st, "wino_f4_plan_info")
@@ -231,14 +256,22 @@ def wino_f4_tap_gemm(plan, workspace, y, n, h, w, layout, stream=None):
                                 _stream(stream)), "wino_f4_tap_gemm")
 
 
-def wino_f4_calibrate_input(x, n, cin, h, w, layout=NCHW, stream=None):
-    lib = load_library()
-    amax = np.zeros(TAPS, np.int32)
-    eb = np.zeros(TAPS, np.int8)
-    st = lib.wino_f4_calibrate_input(_ptr(x), n, cin, h, w, layout, amax.ctypes.data, eb.ctypes.data,
+def _calibrate_input(fn, m, x, n, cin, h, w, layout, stream):
+    ntap = (m + 2) * (m + 2)
+    amax = np.zeros(ntap, np.int32)
+    eb = np.zeros(ntap, np.int8)
+    st = getattr(load_library(), fn)(_ptr(x), n, cin, h, w, layout, amax.ctypes.data, eb.ctypes.data,
                                      _stream(stream))
-    _check(st, "wino_f4_calibrate_input")
+    _check(st, fn)
     return eb.astype(int).tolist(), amax.astype(int).tolist()
+
+
+def wino_f4_calibrate_input(x, n, cin, h, w, layout=NCHW, stream=None):
+    return _calibrate_input("wino_f4_calibrate_input", 4, x, n, cin, h, w, layout, stream)
+
+
+def wino_f2_calibrate_input(x, n, cin, h, w, layout=NCHW, stream=None):
+    return _calibrate_input("wino_f2_calibrate_input", 2, x, n, cin, h, w, layout, stream)
 
 
 def wino_f4_calibrate_output(plan, x, n, h, w, layout=NCHW, workspace=None, stream=None):

@@ -1,15 +1,17 @@
 // Offline plan: exact weight transform, tap-wise power-of-two quantization
-// and the alignment / epilogue-width decisions (Sec. III, Sec. III-B).
+// and the alignment / epilogue-width decisions (Sec. III, Sec. III-B), for
+// F(4x4,3x3) and F(2x2,3x3).
 //
-// U = G f G^T with G = G24 / 24 (G24 integral, Sec. II).  For one tap (a, b)
-// 576 * U = sum_{i,j} G24[a][i] G24[b][j] f[i][j]; every term is an integer
-// of magnitude <= 576 times an fp32 value, hence exact in double.  The sum of
-// the nine terms is kept exact as a non-overlapping floating-point expansion
-// (Shewchuk, "Adaptive Precision Floating-Point Arithmetic and Fast Robust
-// Geometric Predicates", 1997: TwoSum and GROW-EXPANSION), which decides
-// every comparison against a power-of-two range or a rounding threshold
-// without error.  A double approximation of each sum drives the search; the
-// exact expansion is consulted only near a decision boundary.
+// U = G f G^T with G = Gint / d (Gint integral, Sec. II: d = 24 for F4, 2 for
+// F2).  For one tap (a, b), d^2 U = sum_{i,j} Gint[a][i] Gint[b][j] f[i][j];
+// every term is an integer of magnitude <= 576 times an fp32 value, hence
+// exact in double.  The sum of the nine terms is kept exact as a
+// non-overlapping floating-point expansion (Shewchuk, "Adaptive Precision
+// Floating-Point Arithmetic and Fast Robust Geometric Predicates", 1997:
+// TwoSum and GROW-EXPANSION), which decides every comparison against a
+// power-of-two range or a rounding threshold without error.  A double
+// approximation of each sum drives the search; the exact expansion is
+// consulted only near a decision boundary.
 #include <algorithm>
 #include <cmath>
 #include <cstring>
@@ -21,8 +23,19 @@ using namespace winof4;
 
 namespace {
 
-const int G24[6][3] = {{6, 0, 0}, {-4, -4, -4}, {-4, 4, -4}, {1, 2, 4}, {1, -2, 4}, {0, 0, 24}};
-const int AT[4][6] = {{1, 1, 1, 1, 1, 0}, {0, 1, -1, 2, -2, 0}, {0, 1, 1, 4, 4, 0}, {0, 1, -1, 8, -8, 1}};
+// One transform F(m x m, 3 x 3): n = m + 2 input rows, n^2 taps, Gint = d G,
+// den2 = d^2, A^T (m x n).
+struct Xform {
+    int m, n, ntap, den2;
+    int gint[6][3];
+    int at[4][6];
+};
+const Xform kF4 = {4, 6, 36, 576,
+                   {{6, 0, 0}, {-4, -4, -4}, {-4, 4, -4}, {1, 2, 4}, {1, -2, 4}, {0, 0, 24}},
+                   {{1, 1, 1, 1, 1, 0}, {0, 1, -1, 2, -2, 0}, {0, 1, 1, 4, 4, 0}, {0, 1, -1, 8, -8, 1}}};
+const Xform kF2 = {2, 4, 16, 4,
+                   {{2, 0, 0}, {1, 1, 1}, {1, -1, 1}, {0, 0, 2}},
+                   {{1, 1, 1, 0}, {0, 1, -1, -1}}};
 
 // Knuth's TwoSum: s + e == a + b exactly, s = fl(a + b).
 inline void two_sum(double a, double b, double& s, double& e) {
@@ -63,19 +76,20 @@ int exact_sign_minus(const double* terms, double thr) {
     return ex[len - 1] > 0 ? 1 : -1;   // the largest component carries the sign
 }
 
-// The nine exact terms of 576 * U[a][b] for one 3x3 kernel.
-void tap_terms(const float* f9, int a, int b, double* terms) {
+// The nine exact terms of d^2 * U[a][b] for one 3x3 kernel.
+void tap_terms(const Xform& X, const float* f9, int a, int b, double* terms) {
     int k = 0;
     for (int i = 0; i < 3; ++i)
         for (int j = 0; j < 3; ++j)
-            terms[k++] = (double)(G24[a][i] * G24[b][j]) * (double)f9[i * 3 + j];
+            terms[k++] = (double)(X.gint[a][i] * X.gint[b][j]) * (double)f9[i * 3 + j];
 }
 
-// Smallest integer e with |S| <= 73728 * 2^e (73728 = 128 * 576) over a set
-// of sums, decided exactly.  `approx` holds the double approximation of each
-// sum; `terms_of(k, t9)` regenerates the exact terms of sum k.
+// Smallest integer e with |S| <= 128 d^2 2^e over a set of sums S = d^2 U,
+// decided exactly.  `approx` holds the double approximation of each sum;
+// `terms_of(k, t9)` regenerates the exact terms of sum k.
 template <class TermsOf>
-int exact_cexp_of_max(const std::vector<double>& approx, TermsOf terms_of) {
+int exact_cexp_of_max(const Xform& X, const std::vector<double>& approx, TermsOf terms_of) {
+    const double unit = 128.0 * X.den2;
     double amax = 0.0;
     for (double v : approx) amax = std::max(amax, std::fabs(v));
     if (amax == 0.0) {
@@ -84,15 +98,15 @@ int exact_cexp_of_max(const std::vector<double>& approx, TermsOf terms_of) {
         return 0;
     }
     int e;
-    std::frexp(amax / 73728.0, &e);     // 2^(e-1) <= amax/73728 < 2^e
+    std::frexp(amax / unit, &e);     // 2^(e-1) <= amax/unit < 2^e
     e = e - 1;
-    if (std::ldexp(73728.0, e) < amax) e += 1;
+    if (std::ldexp(unit, e) < amax) e += 1;
     const double rel = 1e-9;
     double t9[9];
     for (int iter = 0; iter < 8; ++iter) {
         bool changed = false;
-        // (1) every |S| <= 73728 * 2^e ?
-        double thr = std::ldexp(73728.0, e);
+        // (1) every |S| <= unit * 2^e ?
+        double thr = std::ldexp(unit, e);
         for (size_t k = 0; k < approx.size() && !changed; ++k) {
             if (std::fabs(approx[k]) < thr * (1 - rel)) continue;
             terms_of(k, t9);
@@ -102,8 +116,8 @@ int exact_cexp_of_max(const std::vector<double>& approx, TermsOf terms_of) {
             }
         }
         if (changed) continue;
-        // (2) some |S| > 73728 * 2^(e-1) ?
-        double lo = std::ldexp(73728.0, e - 1);
+        // (2) some |S| > unit * 2^(e-1) ?
+        double lo = std::ldexp(unit, e - 1);
         bool found = false;
         for (size_t k = 0; k < approx.size() && !found; ++k) {
             double v = std::fabs(approx[k]);
@@ -118,9 +132,9 @@ int exact_cexp_of_max(const std::vector<double>& approx, TermsOf terms_of) {
     return e;
 }
 
-// clamp(R(S / (576 * 2^e)), -128, 127) for the exact sum S of `t9`.
-int8_t exact_quantize(const double* t9, double approx, int e) {
-    double scale = std::ldexp(576.0, e);
+// clamp(R(S / (d^2 2^e)), -128, 127) for the exact sum S of `t9`.
+int8_t exact_quantize(const Xform& X, const double* t9, double approx, int e) {
+    double scale = std::ldexp((double)X.den2, e);
     double u = approx / scale;
     if (!(u < 200.0)) return 127;       // also catches +inf
     if (!(u > -200.0)) return -128;
@@ -140,9 +154,10 @@ int8_t exact_quantize(const double* t9, double approx, int e) {
 
 // Host part of the plan: validates the arguments and fills every table of
 // `p` (cin, cout, paddings, e_b, e_g, sh, e_o, epi_bits, uq_host, bias_host).
-static wino_status compute_tables(wino_f4_plan_s* p, const float* w_oihw, int32_t cin, int32_t cout,
-                                  const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+static wino_status compute_tables(const Xform& X, wino_f4_plan_s* p, const float* w_oihw, int32_t cin,
+                                  int32_t cout, const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
                                   int32_t out_shift, int32_t relu) {
+    const int kTaps = X.ntap, n = X.n;
     if (!w_oihw || !in_exp) return WINO_EINVAL;
     if (cin < 1 || cout < 1) return WINO_EINVAL;
     if (cin > 65536 || cout > 65536) return WINO_EUNSUPPORTED;
@@ -154,6 +169,8 @@ static wino_status compute_tables(wino_f4_plan_s* p, const float* w_oihw, int32_
     for (int64_t i = 0; i < (int64_t)cout * cin * 9; ++i)
         if (!std::isfinite(w_oihw[i])) return WINO_EINVAL;
 
+    p->m = X.m;
+    p->ntap = X.ntap;
     p->cin = cin;
     p->cout = cout;
     p->cin_pad = (int32_t)round_up(cin, kKStep);
@@ -162,7 +179,7 @@ static wino_status compute_tables(wino_f4_plan_s* p, const float* w_oihw, int32_
     p->relu = relu;
 
     const int64_t nblk = (int64_t)cout * cin;
-    // double approximations of 576 * U for every (block, tap)
+    // double approximations of d^2 U for every (block, tap)
     std::vector<double> approx;
     try {
         approx.resize(nblk * kTaps);
@@ -175,7 +192,7 @@ static wino_status compute_tables(wino_f4_plan_s* p, const float* w_oihw, int32_
     for (int64_t k = 0; k < nblk; ++k) {
         const float* f9 = w_oihw + k * 9;
         for (int t = 0; t < kTaps; ++t) {
-            tap_terms(f9, t / 6, t % 6, t9);
+            tap_terms(X, f9, t / n, t % n, t9);
             int len = exact_sum(t9, 9, ex);
             double s = 0.0;
             for (int i = 0; i < len; ++i) s += ex[i];   // small to large
@@ -190,8 +207,8 @@ static wino_status compute_tables(wino_f4_plan_s* p, const float* w_oihw, int32_
             continue;
         }
         for (int64_t k = 0; k < nblk; ++k) col[k] = approx[k * kTaps + t];
-        int e = exact_cexp_of_max(col, [&](size_t kk, double* tt) {
-            tap_terms(w_oihw + kk * 9, t / 6, t % 6, tt);
+        int e = exact_cexp_of_max(X, col, [&](size_t kk, double* tt) {
+            tap_terms(X, w_oihw + kk * 9, t / n, t % n, tt);
         });
         if (e < -126 || e > 126) return WINO_ERANGE;
         p->e_g[t] = (int8_t)e;
@@ -200,9 +217,9 @@ static wino_status compute_tables(wino_f4_plan_s* p, const float* w_oihw, int32_
     for (int64_t k = 0; k < nblk; ++k) {
         int co = (int)(k / cin), ci = (int)(k % cin);
         for (int t = 0; t < kTaps; ++t) {
-            tap_terms(w_oihw + k * 9, t / 6, t % 6, t9);
+            tap_terms(X, w_oihw + k * 9, t / n, t % n, t9);
             p->uq_host[((size_t)t * cin + ci) * cout + co] =
-                exact_quantize(t9, approx[k * kTaps + t], p->e_g[t]);
+                exact_quantize(X, t9, approx[k * kTaps + t], p->e_g[t]);
         }
     }
     // exponents and alignment
@@ -235,11 +252,11 @@ static wino_status compute_tables(wino_f4_plan_s* p, const float* w_oihw, int32_
             for (int ci = 0; ci < cin; ++ci) s += std::abs((int)p->uq_host[((size_t)t * cin + ci) * cout + co]);
             colsum[t] = s;
         }
-        for (int i = 0; i < 4; ++i)
-            for (int j = 0; j < 4; ++j) {
+        for (int i = 0; i < X.m; ++i)
+            for (int j = 0; j < X.m; ++j) {
                 unsigned __int128 tot = 0;
                 for (int t = 0; t < kTaps; ++t) {
-                    int c = std::abs(AT[i][t / 6] * AT[j][t % 6]);
+                    int c = std::abs(X.at[i][t / n] * X.at[j][t % n]);
                     tot += (unsigned __int128)c * colsum[t] * 128u * ((unsigned __int128)1 << p->sh[t]);
                 }
                 worst = std::max(worst, tot);
@@ -253,41 +270,39 @@ static wino_status compute_tables(wino_f4_plan_s* p, const float* w_oihw, int32_
     return WINO_OK;
 }
 
-extern "C" wino_status wino_f4_plan_tables(const float* w_oihw, int32_t cin, int32_t cout,
-                                           const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
-                                           int32_t out_shift, int8_t* e_g, int8_t* sh, int32_t* e_o,
-                                           int32_t* epilogue_bits, int8_t* uq) {
+static wino_status plan_tables(const Xform& X, const float* w_oihw, int32_t cin, int32_t cout,
+                               const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias, int32_t out_shift,
+                               int8_t* e_g, int8_t* sh, int32_t* e_o, int32_t* epilogue_bits, int8_t* uq) {
     wino_f4_plan_s* p = new (std::nothrow) wino_f4_plan_s();
     if (!p) return WINO_ENOMEM;
     p->uq_dev = nullptr;
     p->bias_dev = nullptr;
-    wino_status st = compute_tables(p, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, 0);
+    wino_status st = compute_tables(X, p, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, 0);
     if (st == WINO_OK) st = wino_f4_plan_info(p, e_g, sh, e_o, epilogue_bits, uq, nullptr, nullptr);
     delete p;
     return st;
 }
 
-extern "C" wino_status wino_f4_plan(wino_f4_plan_t* out, const float* w_oihw, int32_t cin,
-                                    int32_t cout, const int8_t* in_exp, const int8_t* w_exp,
-                                    const int32_t* bias, int32_t out_shift, int32_t relu,
-                                    hipStream_t stream) {
+static wino_status make_plan(const Xform& X, wino_f4_plan_t* out, const float* w_oihw, int32_t cin, int32_t cout,
+                             const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias, int32_t out_shift,
+                             int32_t relu, hipStream_t stream) {
     if (!out) return WINO_EINVAL;
     *out = nullptr;
     wino_f4_plan_s* p = new (std::nothrow) wino_f4_plan_s();
     if (!p) return WINO_ENOMEM;
     p->uq_dev = nullptr;
     p->bias_dev = nullptr;
-    wino_status st = compute_tables(p, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, relu);
+    wino_status st = compute_tables(X, p, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, relu);
     if (st != WINO_OK) {
         delete p;
         return st;
     }
-    // device upload: Uq k-blocked as [36][cin_pad/64][cout_pad][64] (GEMM A
+    // device upload: Uq k-blocked as [ntap][cin_pad/64][cout_pad][64] (GEMM A
     // operand: rows = output channels, 64 input channels contiguous per row,
     // so one k step of one tap is a single contiguous block), bias [cout_pad]
-    std::vector<int8_t> dev_layout((size_t)kTaps * p->cout_pad * p->cin_pad, 0);
+    std::vector<int8_t> dev_layout((size_t)X.ntap * p->cout_pad * p->cin_pad, 0);
     const int nkb = p->cin_pad / kKStep;
-    for (int t = 0; t < kTaps; ++t)
+    for (int t = 0; t < X.ntap; ++t)
         for (int ci = 0; ci < cin; ++ci)
             for (int co = 0; co < cout; ++co)
                 dev_layout[(((size_t)t * nkb + ci / kKStep) * p->cout_pad + co) * kKStep + ci % kKStep] =
@@ -313,6 +328,34 @@ extern "C" wino_status wino_f4_plan(wino_f4_plan_t* out, const float* w_oihw, in
     return WINO_OK;
 }
 
+extern "C" wino_status wino_f4_plan_tables(const float* w_oihw, int32_t cin, int32_t cout,
+                                           const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                                           int32_t out_shift, int8_t* e_g, int8_t* sh, int32_t* e_o,
+                                           int32_t* epilogue_bits, int8_t* uq) {
+    return plan_tables(kF4, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, e_g, sh, e_o, epilogue_bits, uq);
+}
+
+extern "C" wino_status wino_f2_plan_tables(const float* w_oihw, int32_t cin, int32_t cout,
+                                           const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                                           int32_t out_shift, int8_t* e_g, int8_t* sh, int32_t* e_o,
+                                           int32_t* epilogue_bits, int8_t* uq) {
+    return plan_tables(kF2, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, e_g, sh, e_o, epilogue_bits, uq);
+}
+
+extern "C" wino_status wino_f4_plan(wino_f4_plan_t* out, const float* w_oihw, int32_t cin,
+                                    int32_t cout, const int8_t* in_exp, const int8_t* w_exp,
+                                    const int32_t* bias, int32_t out_shift, int32_t relu,
+                                    hipStream_t stream) {
+    return make_plan(kF4, out, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, relu, stream);
+}
+
+extern "C" wino_status wino_f2_plan(wino_f4_plan_t* out, const float* w_oihw, int32_t cin,
+                                    int32_t cout, const int8_t* in_exp, const int8_t* w_exp,
+                                    const int32_t* bias, int32_t out_shift, int32_t relu,
+                                    hipStream_t stream) {
+    return make_plan(kF2, out, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, relu, stream);
+}
+
 extern "C" void wino_f4_plan_destroy(wino_f4_plan_t p) {
     if (!p) return;
     if (p->uq_dev) hipFree(p->uq_dev);
@@ -330,8 +373,8 @@ extern "C" wino_status wino_f4_plan_info(wino_f4_plan_t p, int8_t* e_g, int8_t* 
                                          int32_t* epilogue_bits, int8_t* uq, int32_t* cin,
                                          int32_t* cout) {
     if (!p) return WINO_EINVAL;
-    if (e_g) std::memcpy(e_g, p->e_g, kTaps);
-    if (sh) std::memcpy(sh, p->sh, kTaps);
+    if (e_g) std::memcpy(e_g, p->e_g, p->ntap);
+    if (sh) std::memcpy(sh, p->sh, p->ntap);
     if (e_o) *e_o = p->e_o;
     if (epilogue_bits) *epilogue_bits = p->epi_bits;
     if (uq) std::memcpy(uq, p->uq_host.data(), p->uq_host.size());

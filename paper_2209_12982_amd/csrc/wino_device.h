@@ -40,52 +40,6 @@ __device__ __forceinline__ void bt_1d(const T* v, T* r, T two, T four) {
     r[5] = four * d + f;
 }
 
-// V = B^T d B for four channels of one 6x6 tile.  wv[r][c] holds the int8
-// values of the four channels at tile pixel (r, c), channel k in byte k.
-// On return ev[r][c] holds V[r][c] of channels (0, 2) and od[r][c] of
-// channels (1, 3), as 16-bit lanes: |V| <= 12768 for int8 inputs and the
-// row-pass intermediates are at most 1278, so 16 bits hold everything.
-__device__ __forceinline__ void input_tile_transform(const uint32_t (&wv)[6][6], v2s (&ev)[6][6],
-                                                     v2s (&od)[6][6]) {
-#pragma unroll
-    for (int r = 0; r < 6; ++r)
-#pragma unroll
-        for (int c = 0; c < 6; ++c) {
-            ev[r][c] = lanes_even(wv[r][c]);
-            od[r][c] = lanes_odd(wv[r][c]);
-        }
-    const v2s two = splat(2), four = splat(4);
-    // columns: T1 = B^T d
-#pragma unroll
-    for (int c = 0; c < 6; ++c) {
-        v2s ve[6], vo[6], re[6], ro[6];
-#pragma unroll
-        for (int r = 0; r < 6; ++r) {
-            ve[r] = ev[r][c];
-            vo[r] = od[r][c];
-        }
-        bt_1d(ve, re, two, four);
-        bt_1d(vo, ro, two, four);
-#pragma unroll
-        for (int r = 0; r < 6; ++r) {
-            ev[r][c] = re[r];
-            od[r][c] = ro[r];
-        }
-    }
-    // rows: V = T1 B
-#pragma unroll
-    for (int r = 0; r < 6; ++r) {
-        v2s re[6], ro[6];
-        bt_1d(ev[r], re, two, four);
-        bt_1d(od[r], ro, two, four);
-#pragma unroll
-        for (int c = 0; c < 6; ++c) {
-            ev[r][c] = re[c];
-            od[r][c] = ro[c];
-        }
-    }
-}
-
 // Tap-wise requantization of tap t (Sec. III, power-of-two scale 2^e_B):
 // clamp(R(V / 2^e), -128, 127) with R(v) = floor(v + 1/2), for the four
 // channels, packed back into one word (channel k in byte k).
@@ -125,6 +79,92 @@ __device__ __forceinline__ void at_1d(const T* v, T* y) {
     y[3] = m + (r << 3) + v[5];
 }
 
+// One-dimensional B^T and A^T transforms of F(2x2,3x3) (Sec. II: rows of
+// B^T 1 0 -1 0 / 0 1 1 0 / 0 -1 1 0 / 0 1 0 -1, rows of A^T 1 1 1 0 /
+// 0 1 -1 -1).
+template <class T>
+__device__ __forceinline__ void bt2_1d(const T* v, T* r) {
+    r[0] = v[0] - v[2];
+    r[1] = v[1] + v[2];
+    r[2] = v[2] - v[1];
+    r[3] = v[1] - v[3];
+}
+template <class T>
+__device__ __forceinline__ void at2_1d(const T* v, T* y) {
+    y[0] = v[0] + v[1] + v[2];
+    y[1] = v[1] - v[2] - v[3];
+}
+
+// F(M x M, 3 x 3): N = M + 2 input rows per tile, NTAP = N^2 taps; bt / at
+// are the one-dimensional transforms above.  Tap (1,1), t = N + 1, has an
+// all-ones row and column of A^T for both, so a constant added to it reaches
+// every output of the tile once (used for bias and the rounding constant).
+template <int M>
+struct Wino;
+template <>
+struct Wino<4> {
+    static constexpr int N = 6, NTAP = 36;
+    template <class T>
+    __device__ static __forceinline__ void bt(const T* v, T* r, T two, T four) { bt_1d(v, r, two, four); }
+    template <class T>
+    __device__ static __forceinline__ void at(const T* v, T* y) { at_1d(v, y); }
+};
+template <>
+struct Wino<2> {
+    static constexpr int N = 4, NTAP = 16;
+    template <class T>
+    __device__ static __forceinline__ void bt(const T* v, T* r, T, T) { bt2_1d(v, r); }
+    template <class T>
+    __device__ static __forceinline__ void at(const T* v, T* y) { at2_1d(v, y); }
+};
+
+// V = B^T d B for four channels of one N x N tile.  wv[r][c] holds the int8
+// values of the four channels at tile pixel (r, c), channel k in byte k.
+// On return ev[r][c] holds V[r][c] of channels (0, 2) and od[r][c] of
+// channels (1, 3), as 16-bit lanes: |V| <= 12768 for int8 inputs (F4; 512
+// for F2) and the row-pass intermediates are at most 1278, so 16 bits hold
+// everything.
+template <int M, int N = Wino<M>::N>
+__device__ __forceinline__ void input_tile_transform(const uint32_t (&wv)[N][N], v2s (&ev)[N][N], v2s (&od)[N][N]) {
+#pragma unroll
+    for (int r = 0; r < N; ++r)
+#pragma unroll
+        for (int c = 0; c < N; ++c) {
+            ev[r][c] = lanes_even(wv[r][c]);
+            od[r][c] = lanes_odd(wv[r][c]);
+        }
+    const v2s two = splat(2), four = splat(4);
+    // columns: T1 = B^T d
+#pragma unroll
+    for (int c = 0; c < N; ++c) {
+        v2s ve[N], vo[N], re[N], ro[N];
+#pragma unroll
+        for (int r = 0; r < N; ++r) {
+            ve[r] = ev[r][c];
+            vo[r] = od[r][c];
+        }
+        Wino<M>::bt(ve, re, two, four);
+        Wino<M>::bt(vo, ro, two, four);
+#pragma unroll
+        for (int r = 0; r < N; ++r) {
+            ev[r][c] = re[r];
+            od[r][c] = ro[r];
+        }
+    }
+    // rows: V = T1 B
+#pragma unroll
+    for (int r = 0; r < N; ++r) {
+        v2s re[N], ro[N];
+        Wino<M>::bt(ev[r], re, two, four);
+        Wino<M>::bt(od[r], ro, two, four);
+#pragma unroll
+        for (int c = 0; c < N; ++c) {
+            ev[r][c] = re[c];
+            od[r][c] = ro[c];
+        }
+    }
+}
+
 // Consecutive workgroup ids are dispatched round robin over the 8 XCDs
 // (workgroup i runs on XCD i % 8).  Remap so that each XCD works through one
 // contiguous range of logical block ids, i.e. blocks with neighbouring ids
@@ -162,20 +202,22 @@ __device__ __forceinline__ void ring_barrier() {
 // must be done reading it before it arrives there
 #define WINO_WAIT_VM_LDS(n) __builtin_amdgcn_s_waitcnt(0x0070 | WINO_VMCNT_BITS(n))
 
-// Epilogue of a 16-channel x 16-tile MFMA block holding all 36 taps: the
-// accumulator of tap t, register r, lane l is M_t[co_base + 4*(l/16) + r]
-// [tile tl_base + l%16].  Per output channel: align taps by 2^sh (exact), add
-// bias and the rounding constant once through tap (1,1) (its column of A^T is
-// all ones, so A^T (c e_7 e_7^T) A adds c to every output of the tile), apply
-// Y = A^T M A in two separable passes, then shift, clamp, ReLU, crop, store.
+// Epilogue of a 16-channel x 16-tile MFMA block holding all NTAP taps of
+// F(M x M, 3 x 3): the accumulator of tap t, register r, lane l is
+// M_t[co_base + 4*(l/16) + r][tile tl_base + l%16].  Per output channel: align
+// taps by 2^sh (exact), add bias and the rounding constant once through tap
+// (1,1) (its row and column of A^T are all ones, so they reach every output
+// of the tile once), apply Y = A^T M A in two separable passes, then shift,
+// clamp, ReLU, crop, store.
 // MODE 0: store y.  MODE 1: max |Y + bias| into *aux (calibration).
-// MODE 2: store raw M to aux [36][ntiles][cout] (debug export).
+// MODE 2: store raw M to aux [NTAP][ntiles][cout] (debug export).
 // G provides cout, h, w, th, tw, ntiles, out_shift, relu, tab.
-template <int LAYOUT, int EPI, int MODE, class G>
-__device__ __forceinline__ void tap_epilogue(const v4i (&acc)[kTaps], const G& g, const int32_t* __restrict__ bias,
-                                             int8_t* __restrict__ y, void* __restrict__ aux, int co_base,
-                                             long long tl_base, int lane) {
+template <int M, int LAYOUT, int EPI, int MODE, class G>
+__device__ __forceinline__ void tap_epilogue(const v4i (&acc)[Wino<M>::NTAP], const G& g,
+                                             const int32_t* __restrict__ bias, int8_t* __restrict__ y,
+                                             void* __restrict__ aux, int co_base, long long tl_base, int lane) {
     typedef typename std::conditional<EPI == 64, long long, int>::type acc_t;
+    constexpr int N = Wino<M>::N, NT = Wino<M>::NTAP;
     const int lr = lane & 15, lk = lane >> 4;
     const long long tile = tl_base + lr;
     const bool tile_ok = tile < g.ntiles;
@@ -188,7 +230,7 @@ __device__ __forceinline__ void tap_epilogue(const v4i (&acc)[kTaps], const G& g
             const int co = co_base + 4 * lk + r;
             if (co >= g.cout) continue;
 #pragma unroll
-            for (int t = 0; t < kTaps; ++t) m_out[((long long)t * g.ntiles + tile) * g.cout + co] = acc[t][r];
+            for (int t = 0; t < NT; ++t) m_out[((long long)t * g.ntiles + tile) * g.cout + co] = acc[t][r];
         }
         return;
     }
@@ -201,37 +243,37 @@ __device__ __forceinline__ void tap_epilogue(const v4i (&acc)[kTaps], const G& g
     const acc_t rnd = (MODE == 0 && s > 0) ? ((acc_t)1 << (s - 1)) : 0;
     const int lo = g.relu ? 0 : -128;
     unsigned long long zmax = 0;
-    uint32_t packed[16];  // NHWC: 4 output channels per pixel
+    uint32_t packed[M * M];  // NHWC: 4 output channels per pixel
 #pragma unroll
-    for (int p = 0; p < 16; ++p) packed[p] = 0;
+    for (int p = 0; p < M * M; ++p) packed[p] = 0;
 
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int co = co_base + 4 * lk + r;
-        acc_t mv[kTaps];
+        acc_t mv[NT];
 #pragma unroll
-        for (int t = 0; t < kTaps; ++t) mv[t] = (acc_t)acc[t][r] << g.tab.sh[t];
-        mv[7] += (acc_t)bias[co] + rnd;
-        acc_t rp[6][4];
+        for (int t = 0; t < NT; ++t) mv[t] = (acc_t)acc[t][r] << g.tab.sh[t];
+        mv[N + 1] += (acc_t)bias[co] + rnd;
+        acc_t rp[N][M];
 #pragma unroll
-        for (int a = 0; a < 6; ++a) at_1d(&mv[6 * a], rp[a]);
-        acc_t yv[4][4];
+        for (int a = 0; a < N; ++a) Wino<M>::at(&mv[N * a], rp[a]);
+        acc_t yv[M][M];
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-            acc_t col[6], o[4];
+        for (int jj = 0; jj < M; ++jj) {
+            acc_t col[N], o[M];
 #pragma unroll
-            for (int a = 0; a < 6; ++a) col[a] = rp[a][jj];
-            at_1d(col, o);
+            for (int a = 0; a < N; ++a) col[a] = rp[a][jj];
+            Wino<M>::at(col, o);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) yv[i][jj] = o[i];
+            for (int i = 0; i < M; ++i) yv[i][jj] = o[i];
         }
         if (MODE == 1) {
             if (tile_ok && co < g.cout) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
+                for (int i = 0; i < M; ++i)
 #pragma unroll
-                    for (int jj = 0; jj < 4; ++jj)
-                        if (4 * ty + i < g.h && 4 * tx + jj < g.w) {
+                    for (int jj = 0; jj < M; ++jj)
+                        if (M * ty + i < g.h && M * tx + jj < g.w) {
                             acc_t v = yv[i][jj];
                             unsigned long long av = (unsigned long long)(v < 0 ? -(long long)v : (long long)v);
                             zmax = av > zmax ? av : zmax;
@@ -239,11 +281,11 @@ __device__ __forceinline__ void tap_epilogue(const v4i (&acc)[kTaps], const G& g
             }
             continue;
         }
-        int qv[4][4];
+        int qv[M][M];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < M; ++i)
 #pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
+            for (int jj = 0; jj < M; ++jj) {
                 if (EPI == 32) {
                     qv[i][jj] = med3_i32((int)(yv[i][jj] >> s), lo, 127);
                 } else {
@@ -255,27 +297,33 @@ __device__ __forceinline__ void tap_epilogue(const v4i (&acc)[kTaps], const G& g
             }
         if (LAYOUT == WINO_NCHW) {
             if (!tile_ok || co >= g.cout) continue;
-            int8_t* base = y + (((long long)img * g.cout + co) * g.h + 4 * ty) * g.w + 4 * tx;
-            const bool full_cols = (4 * tx + 3 < g.w) && ((g.w & 3) == 0);
+            int8_t* base = y + (((long long)img * g.cout + co) * g.h + M * ty) * g.w + M * tx;
+            const bool full_cols = (M * tx + M - 1 < g.w) && (g.w % M == 0);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                if (4 * ty + i >= g.h) continue;
+            for (int i = 0; i < M; ++i) {
+                if (M * ty + i >= g.h) continue;
                 if (full_cols) {
-                    uint32_t wv = __builtin_amdgcn_perm((uint32_t)qv[i][1], (uint32_t)qv[i][0], 0x0c0c0400u) |
-                                  (__builtin_amdgcn_perm((uint32_t)qv[i][3], (uint32_t)qv[i][2], 0x0c0c0400u) << 16);
-                    *(uint32_t*)(base + (long long)i * g.w) = wv;
+                    if (M == 4) {
+                        uint32_t wv = __builtin_amdgcn_perm((uint32_t)qv[i][1], (uint32_t)qv[i][0], 0x0c0c0400u) |
+                                      (__builtin_amdgcn_perm((uint32_t)qv[i][M - 1], (uint32_t)qv[i][M - 2],
+                                                             0x0c0c0400u) << 16);
+                        *(uint32_t*)(base + (long long)i * g.w) = wv;
+                    } else {
+                        *(uint16_t*)(base + (long long)i * g.w) =
+                            (uint16_t)__builtin_amdgcn_perm((uint32_t)qv[i][1], (uint32_t)qv[i][0], 0x0c0c0400u);
+                    }
                 } else {
 #pragma unroll
-                    for (int jj = 0; jj < 4; ++jj)
-                        if (4 * tx + jj < g.w) base[(long long)i * g.w + jj] = (int8_t)qv[i][jj];
+                    for (int jj = 0; jj < M; ++jj)
+                        if (M * tx + jj < g.w) base[(long long)i * g.w + jj] = (int8_t)qv[i][jj];
                 }
             }
         } else {
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < M; ++i)
 #pragma unroll
-                for (int jj = 0; jj < 4; ++jj) {
-                    uint32_t& pk = packed[4 * i + jj];
+                for (int jj = 0; jj < M; ++jj) {
+                    uint32_t& pk = packed[M * i + jj];
                     const uint32_t q = (uint32_t)qv[i][jj];
                     pk = r == 0 ? put_byte<0>(pk, q) : r == 1 ? put_byte<1>(pk, q) : r == 2 ? put_byte<2>(pk, q)
                                                                                         : put_byte<3>(pk, q);
@@ -295,19 +343,23 @@ __device__ __forceinline__ void tap_epilogue(const v4i (&acc)[kTaps], const G& g
     if (LAYOUT == WINO_NHWC && tile_ok) {
         const int co0 = co_base + 4 * lk;
         const long long rs = (long long)g.w * g.cout;
-        int8_t* ob = y + (((long long)img * g.h + 4 * ty) * g.w + 4 * tx) * g.cout + co0;
-        const bool full = (co0 + 3 < g.cout) && ((g.cout & 3) == 0) && (4 * ty + 3 < g.h) && (4 * tx + 3 < g.w);
+        int8_t* ob = y + (((long long)img * g.h + M * ty) * g.w + M * tx) * g.cout + co0;
+        const bool full = (co0 + 3 < g.cout) && ((g.cout & 3) == 0) && (M * ty + M - 1 < g.h) &&
+                          (M * tx + M - 1 < g.w);
         if (full) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < M; ++i)
 #pragma unroll
-                for (int jj = 0; jj < 4; ++jj) *(uint32_t*)(ob + i * rs + jj * g.cout) = packed[4 * i + jj];
+                for (int jj = 0; jj < M; ++jj) *(uint32_t*)(ob + i * rs + jj * g.cout) = packed[M * i + jj];
         } else {
-            for (int i = 0; i < 4; ++i)
-                for (int jj = 0; jj < 4; ++jj) {
-                    if (4 * ty + i >= g.h || 4 * tx + jj >= g.w) continue;
+#pragma unroll
+            for (int i = 0; i < M; ++i)
+#pragma unroll
+                for (int jj = 0; jj < M; ++jj) {
+                    if (M * ty + i >= g.h || M * tx + jj >= g.w) continue;
+#pragma unroll
                     for (int r = 0; r < 4; ++r)
-                        if (co0 + r < g.cout) ob[i * rs + jj * g.cout + r] = (int8_t)(packed[4 * i + jj] >> (8 * r));
+                        if (co0 + r < g.cout) ob[i * rs + jj * g.cout + r] = (int8_t)(packed[M * i + jj] >> (8 * r));
                 }
         }
     }

@@ -192,7 +192,7 @@ __global__ __launch_bounds__(K4_THREADS) void wino_fused(const int8_t* __restric
         }
         __syncthreads();   // every wave is done with this Vq block
     }
-    tap_epilogue<LAYOUT, EPI, 0>(acc, g, bias, y, nullptr, co_blk + 16 * cw, tl_blk + 16 * tw, lane);
+    tap_epilogue<4, LAYOUT, EPI, 0>(acc, g, bias, y, nullptr, co_blk + 16 * cw, tl_blk + 16 * tw, lane);
 }
 
 }  // namespace

@@ -35,9 +35,13 @@ namespace {
 // ---------------------------------------------------------------------------
 constexpr int K1_TX = 16;               // tiles per block along x
 constexpr int K1_CG = 64;               // channels per block
-constexpr int K1_COLS = 4 * K1_TX + 2;  // band width in pixels
 constexpr int K1_CS = 20;               // LDS words per pixel (16 used, 4 pad)
 constexpr int K1_THREADS = 256;
+// halo band of a block: M + 2 rows x (M * K1_TX + 2) pixels
+template <int M>
+struct K1Band {
+    static constexpr int ROWS = M + 2, COLS = M * K1_TX + 2;
+};
 
 struct K1Args {
     int n, cin, h, w, th, tw, cin_pad;
@@ -48,17 +52,18 @@ struct K1Args {
 };
 
 // Stage the halo band of one block into LDS as [row][col][channel] bytes
-// (channel fastest, K1_CS words per pixel).  Rows 4ty-1 .. 4ty+4, columns
-// 4tx0-1 .. 4tx0+4*K1_TX, channels ci0 .. ci0+63; zero outside the image and
-// beyond Cin.
-template <int LAYOUT>
+// (channel fastest, K1_CS words per pixel).  Rows M ty - 1 .. M ty + M,
+// columns M tx0 - 1 .. M (tx0 + K1_TX), channels ci0 .. ci0+63; zero outside
+// the image and beyond Cin.
+template <int M, int LAYOUT>
 __device__ __forceinline__ void k1_stage_band(uint32_t* lds, const int8_t* __restrict__ x,
                                               const K1Args& g, int img, int ty, int tx0, int ci0) {
-    const int h0 = 4 * ty - 1, w0 = 4 * tx0 - 1;
+    constexpr int ROWS = K1Band<M>::ROWS, COLS = K1Band<M>::COLS;
+    const int h0 = M * ty - 1, w0 = M * tx0 - 1;
     if (LAYOUT == WINO_NHWC) {
-        for (int id = threadIdx.x; id < 6 * K1_COLS * 4; id += K1_THREADS) {
+        for (int id = threadIdx.x; id < ROWS * COLS * 4; id += K1_THREADS) {
             int pix = id >> 2, part = id & 3;
-            int r = pix / K1_COLS, c = pix - r * K1_COLS;
+            int r = pix / COLS, c = pix - r * COLS;
             int hh = h0 + r, ww = w0 + c, cb = ci0 + 16 * part;
             uint4 v = make_uint4(0, 0, 0, 0);
             if (hh >= 0 && hh < g.h && ww >= 0 && ww < g.w && cb < g.cin) {
@@ -76,26 +81,28 @@ __device__ __forceinline__ void k1_stage_band(uint32_t* lds, const int8_t* __res
         }
     } else {
         uint8_t* lb = (uint8_t*)lds;
-        for (int id = threadIdx.x; id < K1_CG * 6 * K1_COLS; id += K1_THREADS) {
-            int c = id % K1_COLS;
-            int rest = id / K1_COLS;
-            int r = rest % 6, ch = rest / 6;
+        for (int id = threadIdx.x; id < K1_CG * ROWS * COLS; id += K1_THREADS) {
+            int c = id % COLS;
+            int rest = id / COLS;
+            int r = rest % ROWS, ch = rest / ROWS;
             int hh = h0 + r, ww = w0 + c, ci = ci0 + ch;
             int8_t v = 0;
             if (hh >= 0 && hh < g.h && ww >= 0 && ww < g.w && ci < g.cin)
                 v = x[(((long long)img * g.cin + ci) * g.h + hh) * g.w + ww];
-            lb[(r * K1_COLS + c) * K1_CS * 4 + ch] = (uint8_t)v;
+            lb[(r * COLS + c) * K1_CS * 4 + ch] = (uint8_t)v;
         }
     }
 }
 
-// MODE 0: write Vq.  MODE 1: per-tap max |V| into tapmax[36] (calibration).
-template <int LAYOUT, int MODE>
+// MODE 0: write Vq.  MODE 1: per-tap max |V| into tapmax[NTAP] (calibration).
+template <int M, int LAYOUT, int MODE>
 __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __restrict__ x,
                                                                int8_t* __restrict__ vq,
                                                                int* __restrict__ tapmax, K1Args g) {
-    __shared__ uint32_t band[6 * K1_COLS * K1_CS];
-    __shared__ int red[kTaps];
+    constexpr int N = Wino<M>::N, NT = Wino<M>::NTAP;
+    constexpr int COLS = K1Band<M>::COLS;
+    __shared__ uint32_t band[K1Band<M>::ROWS * COLS * K1_CS];
+    __shared__ int red[NT];
     // Logical block order: channel group fastest, then tile-column block,
     // then tile row; consecutive logical ids are kept on one XCD (its L2),
     // so the channel groups sharing each 128-byte line of an NHWC pixel and
@@ -107,9 +114,9 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
     const int row = bid / g.ntxb;         // img * th + ty
     const int img = row / g.th, ty = row - img * g.th;
     const int tx0 = txb * K1_TX, ci0 = cgi * K1_CG;
-    if (MODE == 1 && threadIdx.x < kTaps) red[threadIdx.x] = 0;
+    if (MODE == 1 && threadIdx.x < NT) red[threadIdx.x] = 0;
 
-    k1_stage_band<LAYOUT>(band, x, g, img, ty, tx0, ci0);
+    k1_stage_band<M, LAYOUT>(band, x, g, img, ty, tx0, ci0);
     __syncthreads();
 
     // thread -> (tile j, channel quad q): 16 quads x 16 tiles
@@ -118,13 +125,13 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
     const int tx = tx0 + j;
     const bool valid = tx < g.tw;
 
-    uint32_t wv[6][6];
+    uint32_t wv[N][N];
 #pragma unroll
-    for (int r = 0; r < 6; ++r)
+    for (int r = 0; r < N; ++r)
 #pragma unroll
-        for (int c = 0; c < 6; ++c) wv[r][c] = band[(r * K1_COLS + 4 * j + c) * K1_CS + q];
-    v2s ev[6][6], od[6][6];
-    input_tile_transform(wv, ev, od);
+        for (int c = 0; c < N; ++c) wv[r][c] = band[(r * COLS + M * j + c) * K1_CS + q];
+    v2s ev[N][N], od[N][N];
+    input_tile_transform<M>(wv, ev, od);
 
     if (MODE == 0) {
         if (!valid) return;
@@ -133,12 +140,12 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
         uint32_t* dst = (uint32_t*)(vq + ((long long)cgi * g.t_pad + tile) * K1_CG) + q;
         const long long plane = g.t_pad * g.cin_pad / 4;   // words per tap plane
 #pragma unroll
-        for (int t = 0; t < kTaps; ++t) dst[t * plane] = requant_pack(ev[t / 6][t % 6], od[t / 6][t % 6], g.tab.eb[t]);
+        for (int t = 0; t < NT; ++t) dst[t * plane] = requant_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t]);
     } else {
         if (valid) {
 #pragma unroll
-            for (int t = 0; t < kTaps; ++t) {
-                v2s a = ev[t / 6][t % 6], b = od[t / 6][t % 6];
+            for (int t = 0; t < NT; ++t) {
+                v2s a = ev[t / N][t % N], b = od[t / N][t % N];
                 a = __builtin_elementwise_max(a, -a);
                 b = __builtin_elementwise_max(b, -b);
                 int m = max(max((int)a.x, (int)a.y), max((int)b.x, (int)b.y));
@@ -146,7 +153,7 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
             }
         }
         __syncthreads();
-        if (threadIdx.x < kTaps) atomicMax(&tapmax[threadIdx.x], red[threadIdx.x]);
+        if (threadIdx.x < NT) atomicMax(&tapmax[threadIdx.x], red[threadIdx.x]);
     }
 }
 
@@ -182,13 +189,15 @@ struct K2Cfg {
     static constexpr int PF = G / 2;                     // taps whose LDS fragments are in flight ahead
     static_assert(NBUF * STAGE <= 160 * 1024, "LDS");
     static_assert((NBUF - 2) * LPW <= 63, "vmcnt range");
-    static_assert(kTaps % G == 0 && G > PF, "stage shape");
+    static_assert(G > PF, "stage shape");
 };
 // 64 x 32, one workgroup per CU; 32 x 32 and 16 x 16 with rings small
 // enough for two and four workgroups per CU
 using K2Big = K2Cfg<4, 2, 12, 2>;
 using K2Mid = K2Cfg<2, 2, 6, 3>;
 using K2Small = K2Cfg<1, 1, 6, 3>;
+// F(2x2,3x3): 16 taps in two 8-tap stages per k step, 64 x 32 blocks
+using K2F2 = K2Cfg<4, 2, 8, 3>;
 
 struct K2Args {
     int cin_pad, cout, cout_pad;
@@ -202,7 +211,7 @@ struct K2Args {
 
 // MODE 0: store y.  MODE 1: max |Y + bias| into *zmax (calibration).
 // MODE 2: store raw M (debug export).
-template <class C, int LAYOUT, int EPI, int MODE>
+template <class C, int M, int LAYOUT, int EPI, int MODE>
 __global__ __launch_bounds__(C::THREADS) void wino_tap_gemm(const int8_t* __restrict__ uq,
                                                             const int8_t* __restrict__ vq,
                                                             const int32_t* __restrict__ bias,
@@ -255,7 +264,9 @@ __global__ __launch_bounds__(C::THREADS) void wino_tap_gemm(const int8_t* __rest
         }
         dst[i] = j * 1024;
     }
-    constexpr int GPS = kTaps / C::G;                  // stages per k-chunk
+    constexpr int NT = Wino<M>::NTAP;
+    static_assert(NT % C::G == 0, "stages split the taps evenly");
+    constexpr int GPS = NT / C::G;                     // stages per k-chunk
     const int nkc = g.cin_pad / kKStep;
     const int nstage = nkc * GPS;
     auto issue = [&](int st) {
@@ -275,9 +286,9 @@ __global__ __launch_bounds__(C::THREADS) void wino_tap_gemm(const int8_t* __rest
         }
     };
 
-    v4i acc[kTaps];
+    v4i acc[NT];
 #pragma unroll
-    for (int t = 0; t < kTaps; ++t) acc[t] = (v4i){0, 0, 0, 0};
+    for (int t = 0; t < NT; ++t) acc[t] = (v4i){0, 0, 0, 0};
 
     // fragment offsets within a stage buffer (tap u adds u * rows * 64)
     const int row_a = 16 * cw + lr, row_b = 16 * tw + lr;
@@ -333,7 +344,7 @@ __global__ __launch_bounds__(C::THREADS) void wino_tap_gemm(const int8_t* __rest
         }
     }
 
-    tap_epilogue<LAYOUT, EPI, MODE>(acc, g, bias, y, aux, co_base, tl_base, lane);
+    tap_epilogue<M, LAYOUT, EPI, MODE>(acc, g, bias, y, aux, co_base, tl_base, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -661,14 +672,15 @@ struct Geometry {
     long long ntiles, t_pad;
 };
 
-wino_status geometry(int32_t n, int32_t h, int32_t w, Geometry& g) {
+// Tile grid of F(m x m, 3 x 3) over an n x h x w input.
+wino_status geometry(int32_t n, int32_t h, int32_t w, int m, Geometry& g) {
     if (n < 0 || h < 0 || w < 0) return WINO_EINVAL;
     if (h > 65536 || w > 65536) return WINO_EUNSUPPORTED;
     g.n = n;
     g.h = h;
     g.w = w;
-    g.th = (h + 3) / 4;
-    g.tw = (w + 3) / 4;
+    g.th = (h + m - 1) / m;
+    g.tw = (w + m - 1) / m;
     g.ntiles = (long long)n * g.th * g.tw;
     if (g.ntiles >= (1ll << 26)) return WINO_EUNSUPPORTED;
     g.t_pad = round_up(g.ntiles, kTilePad);
@@ -676,12 +688,12 @@ wino_status geometry(int32_t n, int32_t h, int32_t w, Geometry& g) {
 }
 
 size_t vq_bytes(const wino_f4_plan_s* p, const Geometry& g) {
-    return (size_t)kTaps * (size_t)g.t_pad * (size_t)p->cin_pad;
+    return (size_t)p->ntap * (size_t)g.t_pad * (size_t)p->cin_pad;
 }
 
 TapTables tables_of(const wino_f4_plan_s* p) {
-    TapTables t;
-    for (int i = 0; i < kTaps; ++i) {
+    TapTables t = {};
+    for (int i = 0; i < p->ntap; ++i) {
         t.eb[i] = p->e_b[i];
         t.sh[i] = p->sh[i];
     }
@@ -705,7 +717,7 @@ K1Args k1_args(const Geometry& g, int cin, int cin_pad, const TapTables& tab) {
     return a;
 }
 
-template <int MODE>
+template <int M, int MODE>
 wino_status launch_k1(const K1Args& a, wino_layout layout, const int8_t* x, int8_t* vq, int* tapmax,
                       hipStream_t stream) {
     long long blocks = (long long)a.ntxb * a.ncg * a.n * a.th;
@@ -714,10 +726,10 @@ wino_status launch_k1(const K1Args& a, wino_layout layout, const int8_t* x, int8
     K1Args args = a;
     args.x_vec = (a.cin % 16 == 0) && (((uintptr_t)x & 15) == 0);
     if (layout == WINO_NHWC)
-        hipLaunchKernelGGL((wino_input_xform<WINO_NHWC, MODE>), dim3((unsigned)blocks), dim3(K1_THREADS), 0,
+        hipLaunchKernelGGL((wino_input_xform<M, WINO_NHWC, MODE>), dim3((unsigned)blocks), dim3(K1_THREADS), 0,
                            stream, x, vq, tapmax, args);
     else
-        hipLaunchKernelGGL((wino_input_xform<WINO_NCHW, MODE>), dim3((unsigned)blocks), dim3(K1_THREADS), 0,
+        hipLaunchKernelGGL((wino_input_xform<M, WINO_NCHW, MODE>), dim3((unsigned)blocks), dim3(K1_THREADS), 0,
                            stream, x, vq, tapmax, args);
     return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
 }
@@ -737,7 +749,7 @@ long long resident_blocks(const wino_f4_plan_s* p, const Geometry& g) {
 // Calibration and debug exports (MODE 1, 2) always use the 64x32 shape.
 int tap_kernel_for(const wino_f4_plan_s* p, const Geometry& g, int mode) {
     const int k = p->tap_kernel;
-    if (mode != 0) return WINO_TAP_RESIDENT_64X32;
+    if (mode != 0 || p->m != 4) return WINO_TAP_RESIDENT_64X32;   // F2: its own 64x32 configuration
     if (k == WINO_TAP_RESIDENT_64X32 || k == WINO_TAP_RESIDENT_32X32 || k == WINO_TAP_RESIDENT_16X16) return k;
     if (p->epi_bits == 32 && k != WINO_TAP_RESIDENT &&
         (k == WINO_TAP_ROWS || (long long)(p->cout_pad / KR_CO) * (g.t_pad / KR_TL) >= num_cus()))
@@ -745,7 +757,7 @@ int tap_kernel_for(const wino_f4_plan_s* p, const Geometry& g, int mode) {
     return WINO_TAP_RESIDENT_64X32;
 }
 
-template <class C, int MODE>
+template <class C, int M, int MODE>
 wino_status launch_resident(const wino_f4_plan_s* p, const Geometry& g, wino_layout layout, const int8_t* vq,
                             int8_t* y, void* aux, K2Args a, hipStream_t stream) {
     const long long blocks = resident_blocks<C>(p, g);
@@ -755,7 +767,7 @@ wino_status launch_resident(const wino_f4_plan_s* p, const Geometry& g, wino_lay
     a.nblocks = (int)blocks;
     dim3 grid((unsigned)blocks), block(C::THREADS);
 #define K2_LAUNCH(L, E)                                                                              \
-    hipLaunchKernelGGL((wino_tap_gemm<C, L, E, MODE>), grid, block, 0, stream, p->uq_dev, vq, p->bias_dev, \
+    hipLaunchKernelGGL((wino_tap_gemm<C, M, L, E, MODE>), grid, block, 0, stream, p->uq_dev, vq, p->bias_dev, \
                        y, aux, a)
     if (layout == WINO_NHWC) {
         if (p->epi_bits == 32) K2_LAUNCH(WINO_NHWC, 32); else K2_LAUNCH(WINO_NHWC, 64);
@@ -785,6 +797,7 @@ wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout la
     a.relu = p->relu;
     a.y_staged = layout == WINO_NHWC && p->cout % KR_CO == 0 && ((uintptr_t)y & 15) == 0;
     a.tab = tables_of(p);
+    if (p->m == 2) return launch_resident<K2F2, 2, MODE>(p, g, layout, vq, y, aux, a, stream);
     switch (tap_kernel_for(p, g, MODE)) {
         case WINO_TAP_ROWS: {
             const long long rblocks = (long long)(p->cout_pad / KR_CO) * (g.t_pad / KR_TL);
@@ -800,22 +813,30 @@ wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout la
             return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
         }
         case WINO_TAP_RESIDENT_32X32:
-            if constexpr (MODE == 0) return launch_resident<K2Mid, MODE>(p, g, layout, vq, y, aux, a, stream);
+            if constexpr (MODE == 0) return launch_resident<K2Mid, 4, MODE>(p, g, layout, vq, y, aux, a, stream);
             break;
         case WINO_TAP_RESIDENT_16X16:
-            if constexpr (MODE == 0) return launch_resident<K2Small, MODE>(p, g, layout, vq, y, aux, a, stream);
+            if constexpr (MODE == 0) return launch_resident<K2Small, 4, MODE>(p, g, layout, vq, y, aux, a, stream);
             break;
         default:
             break;
     }
-    return launch_resident<K2Big, MODE>(p, g, layout, vq, y, aux, a, stream);
+    return launch_resident<K2Big, 4, MODE>(p, g, layout, vq, y, aux, a, stream);
 }
 
 wino_status check_common(const wino_f4_plan_s* p, const void* x, int32_t n, int32_t h, int32_t w,
                          wino_layout layout, Geometry& g) {
     if (!p || !x) return WINO_EINVAL;
     if (layout != WINO_NCHW && layout != WINO_NHWC) return WINO_EINVAL;
-    return geometry(n, h, w, g);
+    return geometry(n, h, w, p->m, g);
+}
+
+// K1 for the plan's transform
+template <int MODE>
+wino_status run_k1(int m, const K1Args& a, wino_layout layout, const int8_t* x, int8_t* vq, int* tapmax,
+                   hipStream_t stream) {
+    return m == 2 ? launch_k1<2, MODE>(a, layout, x, vq, tapmax, stream)
+                  : launch_k1<4, MODE>(a, layout, x, vq, tapmax, stream);
 }
 
 int cexp_int(unsigned long long a) {
@@ -830,7 +851,7 @@ int cexp_int(unsigned long long a) {
 extern "C" size_t wino_f4_workspace_bytes(wino_f4_plan_t p, int32_t n, int32_t h, int32_t w,
                                           wino_variant variant) {
     Geometry g;
-    if (!p || geometry(n, h, w, g) != WINO_OK) return 0;
+    if (!p || geometry(n, h, w, p->m, g) != WINO_OK) return 0;
     if (variant == WINO_FUSED) return 0;
     return vq_bytes(p, g);
 }
@@ -843,7 +864,7 @@ extern "C" wino_status wino_f4_tap_kernel_choice(wino_f4_plan_t p, int32_t n, in
                                                  int32_t* kind) {
     if (!p || !kind) return WINO_EINVAL;
     Geometry g;
-    const wino_status st = geometry(n, h, w, g);
+    const wino_status st = geometry(n, h, w, p->m, g);
     if (st != WINO_OK) return st;
     *kind = tap_kernel_for(p, g, 0);
     return WINO_OK;
@@ -858,10 +879,13 @@ extern "C" wino_status wino_f4_conv_int8(wino_f4_plan_t p, const int8_t* x, int8
     if (!y) return WINO_EINVAL;
     if (variant != WINO_SPLIT && variant != WINO_FUSED) return WINO_EINVAL;
     if (g.ntiles == 0) return WINO_OK;
-    if (variant == WINO_FUSED) return wino_f4_conv_fused(p, x, y, n, h, w, layout, stream);
+    if (variant == WINO_FUSED) {
+        if (p->m != 4) return WINO_EUNSUPPORTED;
+        return wino_f4_conv_fused(p, x, y, n, h, w, layout, stream);
+    }
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
     int8_t* vq = (int8_t*)ws;
-    st = launch_k1<0>(k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, vq, nullptr, stream);
+    st = run_k1<0>(p->m, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, vq, nullptr, stream);
     if (st != WINO_OK) return st;
     return launch_k2<0>(p, g, layout, vq, y, nullptr, stream);
 }
@@ -874,7 +898,7 @@ extern "C" wino_status wino_f4_input_transform(wino_f4_plan_t p, const int8_t* x
     if (st != WINO_OK) return st;
     if (g.ntiles == 0) return WINO_OK;
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
-    return launch_k1<0>(k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
+    return run_k1<0>(p->m, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
 }
 
 extern "C" wino_status wino_f4_tap_gemm(wino_f4_plan_t p, const void* ws, size_t ws_bytes, int8_t* y, int32_t n,
@@ -888,29 +912,30 @@ extern "C" wino_status wino_f4_tap_gemm(wino_f4_plan_t p, const void* ws, size_t
     return launch_k2<0>(p, g, layout, (const int8_t*)ws, y, nullptr, stream);
 }
 
-extern "C" wino_status wino_f4_calibrate_input(const int8_t* x, int32_t n, int32_t cin, int32_t h, int32_t w,
-                                               wino_layout layout, int32_t* absmax, int8_t* e_b,
-                                               hipStream_t stream) {
+// per-tap max |V| over the input and the exponents e_B = max(0, cexp(.))
+static wino_status calibrate_input(int m, const int8_t* x, int32_t n, int32_t cin, int32_t h, int32_t w,
+                                   wino_layout layout, int32_t* absmax, int8_t* e_b, hipStream_t stream) {
     if (!x || cin < 1) return WINO_EINVAL;
     if (cin > 65536) return WINO_EUNSUPPORTED;
     if (layout != WINO_NCHW && layout != WINO_NHWC) return WINO_EINVAL;
     Geometry g;
-    wino_status st = geometry(n, h, w, g);
+    wino_status st = geometry(n, h, w, m, g);
     if (st != WINO_OK) return st;
+    const int ntap = (m + 2) * (m + 2);
     int host[kTaps] = {0};
     if (g.ntiles > 0) {
         int* dmax = nullptr;
         if (hipMalloc(&dmax, sizeof(int) * kTaps) != hipSuccess) return WINO_ENOMEM;
         TapTables tab = {};
         bool ok = hipMemsetAsync(dmax, 0, sizeof(int) * kTaps, stream) == hipSuccess;
-        if (ok) ok = launch_k1<1>(k1_args(g, cin, (int)round_up(cin, kKStep), tab), layout, x, nullptr, dmax,
-                                  stream) == WINO_OK;
+        if (ok) ok = run_k1<1>(m, k1_args(g, cin, (int)round_up(cin, kKStep), tab), layout, x, nullptr, dmax,
+                               stream) == WINO_OK;
         if (ok) ok = hipMemcpyAsync(host, dmax, sizeof(int) * kTaps, hipMemcpyDeviceToHost, stream) == hipSuccess;
         if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
         hipFree(dmax);
         if (!ok) return WINO_EHIP;
     }
-    for (int t = 0; t < kTaps; ++t) {
+    for (int t = 0; t < ntap; ++t) {
         if (absmax) absmax[t] = host[t];
         if (e_b) {
             int e = cexp_int((unsigned long long)host[t]);
@@ -918,6 +943,18 @@ extern "C" wino_status wino_f4_calibrate_input(const int8_t* x, int32_t n, int32
         }
     }
     return WINO_OK;
+}
+
+extern "C" wino_status wino_f4_calibrate_input(const int8_t* x, int32_t n, int32_t cin, int32_t h, int32_t w,
+                                               wino_layout layout, int32_t* absmax, int8_t* e_b,
+                                               hipStream_t stream) {
+    return calibrate_input(4, x, n, cin, h, w, layout, absmax, e_b, stream);
+}
+
+extern "C" wino_status wino_f2_calibrate_input(const int8_t* x, int32_t n, int32_t cin, int32_t h, int32_t w,
+                                               wino_layout layout, int32_t* absmax, int8_t* e_b,
+                                               hipStream_t stream) {
+    return calibrate_input(2, x, n, cin, h, w, layout, absmax, e_b, stream);
 }
 
 extern "C" wino_status wino_f4_calibrate_output(wino_f4_plan_t p, const int8_t* x, int32_t n, int32_t h,
@@ -932,8 +969,8 @@ extern "C" wino_status wino_f4_calibrate_output(wino_f4_plan_t p, const int8_t* 
         unsigned long long* dmax = nullptr;
         if (hipMalloc(&dmax, sizeof(unsigned long long)) != hipSuccess) return WINO_ENOMEM;
         bool ok = hipMemsetAsync(dmax, 0, sizeof(unsigned long long), stream) == hipSuccess;
-        if (ok) ok = launch_k1<0>(k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr,
-                                  stream) == WINO_OK;
+        if (ok) ok = run_k1<0>(p->m, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws,
+                               nullptr, stream) == WINO_OK;
         if (ok) ok = launch_k2<1>(p, g, layout, (const int8_t*)ws, nullptr, dmax, stream) == WINO_OK;
         if (ok) ok = hipMemcpyAsync(&host, dmax, sizeof(host), hipMemcpyDeviceToHost, stream) == hipSuccess;
         if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
@@ -954,12 +991,12 @@ extern "C" wino_status wino_f4_debug_input_transform(wino_f4_plan_t p, const int
     if (!vq_out) return WINO_EINVAL;
     if (g.ntiles == 0) return WINO_OK;
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
-    st = launch_k1<0>(k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
+    st = run_k1<0>(p->m, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
     if (st != WINO_OK) return st;
-    // compact [36][cin_pad/64][t_pad][64] -> [36][ntiles][cin], one 2-D copy
-    // per (tap, k block)
+    // compact [ntap][cin_pad/64][t_pad][64] -> [ntap][ntiles][cin], one 2-D
+    // copy per (tap, k block)
     const int nkb = p->cin_pad / kKStep;
-    for (int t = 0; t < kTaps; ++t)
+    for (int t = 0; t < p->ntap; ++t)
         for (int b = 0; b < nkb; ++b) {
             const int width = std::min(kKStep, p->cin - b * kKStep);
             if (width <= 0) break;
@@ -980,7 +1017,7 @@ extern "C" wino_status wino_f4_debug_tap_gemm(wino_f4_plan_t p, const int8_t* x,
     if (!m_out) return WINO_EINVAL;
     if (g.ntiles == 0) return WINO_OK;
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
-    st = launch_k1<0>(k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
+    st = run_k1<0>(p->m, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
     if (st != WINO_OK) return st;
     return launch_k2<2>(p, g, layout, (const int8_t*)ws, nullptr, m_out, stream);
 }

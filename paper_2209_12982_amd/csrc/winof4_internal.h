@@ -29,6 +29,8 @@ struct TapTables {
 }  // namespace winof4
 
 struct wino_f4_plan_s {
+    int32_t m = 4;                    // output tile: F(m x m, 3 x 3), m = 4 or 2
+    int32_t ntap = 36;                // (m + 2)^2 taps
     int32_t cin, cout, cin_pad, cout_pad;
     int8_t e_b[winof4::kTaps], e_g[winof4::kTaps], sh[winof4::kTaps];
     int32_t e_o;
@@ -36,8 +38,8 @@ struct wino_f4_plan_s {
     int32_t epi_bits;                 // 32 or 64
     int32_t tap_kernel = WINO_TAP_AUTO;
     int32_t device;
-    int8_t* uq_dev;                   // [36][cin_pad/64][cout_pad][64], zero padded
+    int8_t* uq_dev;                   // [ntap][cin_pad/64][cout_pad][64], zero padded
     int32_t* bias_dev;                // [cout_pad], zero padded
-    std::vector<int8_t> uq_host;      // [36][cin][cout]
+    std::vector<int8_t> uq_host;      // [ntap][cin][cout]
     std::vector<int32_t> bias_host;   // [cout]
 };

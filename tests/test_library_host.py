@@ -87,6 +87,47 @@ def test_plan_tables_adversarial():
         assert (c["uq"] == o["uq"]).all()
 
 
+@pytest.mark.parametrize("name", ["C1", "C2", "C3"])
+def test_f2_plan_tables_match_oracle_on_configs(name):
+    _lib()
+    x, layers = workloads.generate(name)
+    for f, b, spec in layers:
+        eb = [int(v) for v in np.random.default_rng(spec.cin + 1).integers(0, 4, 16)]
+        for out_shift in (0, 9):
+            c = W.wino_f2_plan_tables(f, eb, bias=b, out_shift=out_shift)
+            o = tapwise.make_plan(f, eb, bias=b, out_shift=out_shift, m=2)
+            assert c["e_g"] == o["e_g"] and c["sh"] == o["sh"] and c["e_o"] == o["e_o"]
+            assert (c["uq"] == o["uq"]).all()
+            bits = 32 if tapwise.epilogue_bound(o) < 2 ** 31 else 64
+            assert c["epilogue_bits"] == bits
+
+
+def test_f2_plan_tables_adversarial():
+    """F2 (G = Gint / 2): exact ties, maxima exactly at 128 * 2^k, zero taps,
+    extreme magnitudes, explicit exponents."""
+    _lib()
+    rng = np.random.default_rng(5)
+    cases = []
+    f = np.zeros((2, 3, 3, 3), np.float32)
+    f[0, 0, 1, 1] = 4 * 2.0 ** -6 * 3              # U = 3 * 2^-6 * outer(Gint[:,1])
+    f[1, 2] = 1.0
+    cases.append((f, [-5] * 16))
+    f2 = np.zeros((3, 2, 3, 3), np.float32)
+    f2[:, :, 0, 0] = 4 * 2.0 ** -3 * 32 * rng.integers(-1, 2, (3, 2))   # |U| reaches 128 * 2^k
+    cases.append((f2, None))
+    f3 = rng.normal(0, 1, (4, 3, 3, 3)).astype(np.float32)
+    f3[0, 0, 0, 0] = np.float32(1e-38)
+    f3[1, 1, 2, 2] = np.float32(3e4)
+    cases.append((f3, None))
+    cases.append((np.zeros((1, 1, 3, 3), np.float32), None))
+    for f, eg in cases:
+        eb = [int(v) for v in rng.integers(0, 16, 16)]
+        c = W.wino_f2_plan_tables(f, eb, w_exp=eg, out_shift=3)
+        o = tapwise.make_plan(f, eb, e_g=eg, out_shift=3, m=2)
+        assert c["e_g"] == o["e_g"] and c["sh"] == o["sh"] and c["e_o"] == o["e_o"]
+        assert (c["uq"] == o["uq"]).all()
+
+
 def test_direct_weight_quantization_matches_oracle():
     _lib()
     rng = np.random.default_rng(4)
