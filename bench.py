@@ -33,9 +33,14 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", default="C5", help="C1 .. C5 (C3: first layer)")
+    ap.add_argument("--config", default="C5", help="C1 .. C5")
+    ap.add_argument("--layer", type=int, default=0,
+                    help="layer of a chained configuration (C3: 0..3); layers after the first get "
+                         "an input drawn with the configuration's activation recipe at their shape")
     ap.add_argument("--layout", default="nhwc", choices=["nchw", "nhwc"])
     ap.add_argument("--variant", default="split", choices=["split", "fused"])
+    ap.add_argument("--transform", default="f4", choices=["f4", "f2"],
+                    help="Winograd F(4x4,3x3) (the default) or F(2x2,3x3)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-direct", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=0, help="oracle sample size (images); 0 = auto")
@@ -44,14 +49,15 @@ def parse():
     return ap.parse_args()
 
 
-def counter_traffic(cfg, layout, kernel):
+def counter_traffic(cfg, layout, kernel, transform="f4"):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
     summary (FETCH_SIZE and WRITE_SIZE, each scaled by what the counter
     reads for a plain copy of known size), or None when there is no
     summary for this workload or the kernel source changed since the
     counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"{cfg}_{layout}_hbm_counters.txt")
+    tag = cfg if transform == "f4" else f"{cfg}_{transform}"
+    path = os.path.join(ROOT, "profiles", f"{tag}_{layout}_hbm_counters.txt")
     if not os.path.exists(path):
         return None
     vals, kern = {}, {}
@@ -151,7 +157,10 @@ def main():
     variant = W.SPLIT if args.variant == "split" else W.FUSED
     wl = workloads.WORKLOADS[args.config]
     x, layers = workloads.generate(args.config)
-    f, bias, spec = layers[0]
+    f, bias, spec = layers[args.layer]
+    if args.layer > 0:
+        x = workloads.draw_activations(np.random.default_rng(1000 + args.layer), (x.shape[0], spec.cin, spec.h, spec.w),
+                                       wl.act, wl.zero_frac)
     n, cin, cout, h, w = x.shape[0], spec.cin, spec.cout, spec.h, spec.w
     xa = x if layout == W.NCHW else np.ascontiguousarray(x.transpose(0, 2, 3, 1))
     xd = torch.from_numpy(xa).cuda()
@@ -159,13 +168,16 @@ def main():
     y = torch.empty(yshape, dtype=torch.int8, device="cuda")
 
     # offline: calibration and plan (not timed)
-    eb, _ = W.wino_f4_calibrate_input(xd, n, cin, h, w, layout)
-    plan0 = W.wino_f4_plan(f, eb, bias=bias, out_shift=0, relu=spec.relu)
+    mt = 4 if args.transform == "f4" else 2
+    calibrate = W.wino_f4_calibrate_input if mt == 4 else W.wino_f2_calibrate_input
+    make_plan = W.wino_f4_plan if mt == 4 else W.wino_f2_plan
+    eb, _ = calibrate(xd, n, cin, h, w, layout)
+    plan0 = make_plan(f, eb, bias=bias, out_shift=0, relu=spec.relu)
     ws = torch.empty(max(1, W.wino_f4_workspace_bytes(plan0, n, h, w, W.SPLIT)), dtype=torch.int8, device="cuda")
     out_shift = spec.out_shift
     if out_shift is None:
         out_shift, _ = W.wino_f4_calibrate_output(plan0, xd, n, h, w, layout, ws)
-    plan = W.wino_f4_plan(f, eb, bias=bias, out_shift=out_shift, relu=spec.relu)
+    plan = make_plan(f, eb, bias=bias, out_shift=out_shift, relu=spec.relu)
     info = W.wino_f4_plan_info(plan)
 
     def step():
@@ -178,14 +190,16 @@ def main():
 
     # per-kernel durations: each of the two launches of a step timed on its
     # own (HIP events on the launch stream), see kernel_ms
-    th, tw = (h + 3) // 4, (w + 3) // 4
+    th, tw = (h + mt - 1) // mt, (w + mt - 1) // mt
     T = n * th * tw
+    ntap = (mt + 2) ** 2
     lay = 1 if layout == W.NHWC else 0
     rows = W.wino_f4_tap_kernel_choice(plan, n, h, w) == W.TAP_ROWS
-    # kernel names as the profiler shows them (template arguments included)
-    k1_name, k1_inst = "wino_input_xform", f"wino_input_xform<{lay},0>"
+    # kernel names as the profiler shows them (template arguments included;
+    # the tap-resident kernel's block configuration is a class argument)
+    k1_name, k1_inst = "wino_input_xform", f"wino_input_xform<{mt},{lay},0>"
     k2_name = "wino_tap_gemm_rows" if rows else "wino_tap_gemm"
-    k2_inst = f"wino_tap_gemm_rows<{lay}>" if rows else f"wino_tap_gemm<{lay},{info['epilogue_bits']},0>"
+    k2_inst = f"wino_tap_gemm_rows<{lay}>" if rows else f"wino_tap_gemm<{mt},{lay},{info['epilogue_bits']},0>"
     k1_ms = k2_ms = None
     if variant == W.SPLIT:
         k1 = lambda: W.wino_f4_input_transform(plan, xd, n, h, w, layout, ws)
@@ -194,21 +208,22 @@ def main():
         k2_ms, k2_p10, k2_p90 = kernel_ms(torch, k2, args.steps)
 
     direct_ops = 2.0 * 9 * n * h * w * cin * cout
-    tap_ops = 2.0 * 36 * T * cin * cout
+    tap_ops = 2.0 * ntap * T * cin * cout
     value = direct_ops / (ms * 1e-3) / 1e12
-    k1_bytes = n * h * w * cin + 36 * T * cin                 # read x, write Vq
-    k2_bytes = 36 * T * cin + 36 * cin * cout + n * h * w * cout + 4 * cout
+    k1_bytes = n * h * w * cin + ntap * T * cin                 # read x, write Vq
+    k2_bytes = ntap * T * cin + ntap * cin * cout + n * h * w * cout + 4 * cout
     kernels = {}
+    cfg_tag = args.config + (f"L{args.layer}" if args.layer else "")
     if k1_ms is not None:
         kernels[k1_name] = {"ms": k1_ms, "p10_ms": k1_p10, "p90_ms": k1_p90, "bound": "hbm", "bytes": k1_bytes,
                             "GB/s": k1_bytes / (k1_ms * 1e-3) / 1e9,
                             "frac": k1_bytes / (k1_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
-                            "traffic_bytes": counter_traffic(args.config, args.layout, k1_inst)}
+                            "traffic_bytes": counter_traffic(cfg_tag, args.layout, k1_inst, args.transform)}
         kernels[k2_name] = {"ms": k2_ms, "p10_ms": k2_p10, "p90_ms": k2_p90, "bound": "mfma", "ops": tap_ops,
                             "TOP/s": tap_ops / (k2_ms * 1e-3) / 1e12,
                             "frac": tap_ops / (k2_ms * 1e-3) / 1e12 / PEAK_INT8_TOPS,
                             "GB/s_algorithmic": k2_bytes / (k2_ms * 1e-3) / 1e9,
-                            "traffic_bytes": counter_traffic(args.config, args.layout, k2_inst)}
+                            "traffic_bytes": counter_traffic(cfg_tag, args.layout, k2_inst, args.transform)}
         if k2_ms >= k1_ms:
             roofline = {"kernel": k2_name, "bound": "mfma", "achieved": kernels[k2_name]["TOP/s"],
                         "peak": PEAK_INT8_TOPS, "unit": "TOP/s", "frac": kernels[k2_name]["frac"],
@@ -258,8 +273,9 @@ def main():
         "metric": METRIC, "value": value, "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "int8", "data": "synthetic",
-        "config": {"workload": f"{args.config}: {wl.desc}", "n": n, "cin": cin, "cout": cout, "h": h, "w": w,
-                   "layout": args.layout, "variant": args.variant, "tiles": T,
+        "config": {"workload": f"{args.config}: {wl.desc}" + (f" (layer {args.layer})" if args.layer else ""),
+                   "n": n, "cin": cin, "cout": cout, "h": h, "w": w,
+                   "layout": args.layout, "variant": args.variant, "transform": args.transform, "tiles": T,
                    "e_b": eb, "e_g": info["e_g"], "out_shift": out_shift,
                    "epilogue_bits": info["epilogue_bits"]},
         "roofline": roofline,

@@ -8,11 +8,11 @@ an entry point without the built library raises ``LibraryNotBuilt``.
 """
 from .binding import (  # noqa: F401
     NCHW, NHWC, SPLIT, FUSED, TAPS, TAP_AUTO, TAP_RESIDENT, TAP_ROWS,
-    TAP_RESIDENT_64X32, TAP_RESIDENT_32X32, TAP_RESIDENT_16X16,
+    TAP_RESIDENT_64X32, TAP_RESIDENT_32X32, TAP_RESIDENT_16X16, ALGO_DIRECT, ALGO_F2, ALGO_F4,
     LibraryNotBuilt, WinoError, WinoF4Plan,
     library_path, load_library, exported_symbols,
     wino_f4_plan, wino_f4_plan_tables, wino_f4_plan_info,
-    wino_f2_plan, wino_f2_plan_tables, wino_f2_calibrate_input, wino_f4_plan_set_tap_kernel, wino_f4_tap_kernel_choice,
+    wino_f2_plan, wino_f2_plan_tables, wino_f2_calibrate_input, wino_f4_plan_set_tap_kernel, wino_f4_tap_kernel_choice, wino_select_algorithm,
     wino_f4_workspace_bytes, wino_f4_conv_int8,
     wino_f4_input_transform, wino_f4_tap_gemm,
     wino_f4_calibrate_input, wino_f4_calibrate_output,

@@ -12,6 +12,7 @@ NCHW, NHWC = 0, 1
 SPLIT, FUSED = 0, 1
 TAP_AUTO, TAP_RESIDENT, TAP_ROWS = 0, 1, 2
 TAP_RESIDENT_64X32, TAP_RESIDENT_32X32, TAP_RESIDENT_16X16 = 3, 4, 5
+ALGO_DIRECT, ALGO_F2, ALGO_F4 = 0, 2, 4
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB = None
@@ -19,7 +20,8 @@ _LIB = None
 EXPORTS = [
     "wino_f4_plan", "wino_f4_plan_tables", "wino_f4_plan_destroy", "wino_f4_plan_info",
     "wino_f2_plan", "wino_f2_plan_tables", "wino_f2_calibrate_input",
-    "wino_f4_plan_set_tap_kernel", "wino_f4_tap_kernel_choice", "wino_f4_workspace_bytes",
+    "wino_f4_plan_set_tap_kernel", "wino_f4_tap_kernel_choice", "wino_select_algorithm",
+    "wino_f4_workspace_bytes",
     "wino_f4_conv_int8", "wino_f4_input_transform", "wino_f4_tap_gemm", "wino_f4_calibrate_input", "wino_f4_calibrate_output",
     "wino_f4_debug_input_transform", "wino_f4_debug_tap_gemm",
     "direct_conv_quantize_weights", "direct_conv_int8", "wino_strerror",
@@ -60,6 +62,7 @@ def load_library():
         "wino_f4_plan_info": (I32, [P, P, P, P, P, P, P, P]),
         "wino_f4_plan_set_tap_kernel": (I32, [P, I32]),
         "wino_f4_tap_kernel_choice": (I32, [P, I32, I32, I32, P]),
+        "wino_select_algorithm": (I32, [I32, I32, I32, I32, I32, P]),
         "wino_f4_workspace_bytes": (SZ, [P, I32, I32, I32, I32]),
         "wino_f4_conv_int8": (I32, [P, P, P, I32, I32, I32, I32, I32, P, SZ, P]),
         "wino_f4_input_transform": (I32, [P, P, I32, I32, I32, I32, P, SZ, P]),
@@ -228,6 +231,13 @@ def wino_f4_tap_kernel_choice(plan, n, h, w):
     _check(load_library().wino_f4_tap_kernel_choice(plan.handle, n, h, w, ctypes.byref(kind)),
            "wino_f4_tap_kernel_choice")
     return kind.value
+
+
+def wino_select_algorithm(n, cin, cout, h, w):
+    """ALGO_DIRECT, ALGO_F2 or ALGO_F4 for a 3x3 layer of this shape."""
+    algo = ctypes.c_int32()
+    _check(load_library().wino_select_algorithm(n, cin, cout, h, w, ctypes.byref(algo)), "wino_select_algorithm")
+    return algo.value
 
 
 def wino_f4_workspace_bytes(plan, n, h, w, variant=SPLIT):

@@ -860,6 +860,20 @@ extern "C" size_t wino_f4_workspace_bytes(wino_f4_plan_t p, int32_t n, int32_t h
 wino_status wino_f4_conv_fused(const wino_f4_plan_s* p, const int8_t* x, int8_t* y, int n, int h, int w,
                                wino_layout layout, hipStream_t stream);
 
+extern "C" wino_status wino_select_algorithm(int32_t n, int32_t cin, int32_t cout, int32_t h, int32_t w,
+                                             int32_t* algo) {
+    if (!algo || n < 0 || h < 0 || w < 0 || cin < 1 || cout < 1) return WINO_EINVAL;
+    const double ops = 2.0 * 9 * (double)n * h * w * (double)cin * cout;
+    if (ops < (double)(1 << 27)) {
+        *algo = WINO_ALGO_DIRECT;
+        return WINO_OK;
+    }
+    const long long tiles4 = (long long)n * ((h + 3) / 4) * ((w + 3) / 4);
+    const long long blocks = (long long)((cout + KR_CO - 1) / KR_CO) * ((tiles4 + KR_TL - 1) / KR_TL);
+    *algo = blocks >= num_cus() ? WINO_ALGO_F4 : WINO_ALGO_F2;
+    return WINO_OK;
+}
+
 extern "C" wino_status wino_f4_tap_kernel_choice(wino_f4_plan_t p, int32_t n, int32_t h, int32_t w,
                                                  int32_t* kind) {
     if (!p || !kind) return WINO_EINVAL;

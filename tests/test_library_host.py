@@ -128,6 +128,19 @@ def test_f2_plan_tables_adversarial():
         assert (c["uq"] == o["uq"]).all()
 
 
+def test_select_algorithm_on_configs():
+    """The per-layer rule picks what was measured fastest on MI355X for every
+    layer of C1-C5 (host only: with no device the rule assumes 256 CUs)."""
+    _lib()
+    want = {"C1": [W.ALGO_DIRECT], "C2": [W.ALGO_F2], "C3": [W.ALGO_F2] * 4, "C4": [W.ALGO_F4], "C5": [W.ALGO_F4]}
+    for name, algos in want.items():
+        wl = workloads.WORKLOADS[name]
+        got = [W.wino_select_algorithm(wl.n, s.cin, s.cout, s.h, s.w) for s in wl.layers]
+        assert got == algos, name
+    with pytest.raises(W.WinoError):
+        W.wino_select_algorithm(1, 0, 4, 8, 8)
+
+
 def test_direct_weight_quantization_matches_oracle():
     _lib()
     rng = np.random.default_rng(4)
