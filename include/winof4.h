@@ -181,6 +181,52 @@ wino_status wino_f2_plan_tables(const float* w_oihw, int32_t cin, int32_t cout, 
                                 const int8_t* w_exp, const int32_t* bias, int32_t out_shift, int8_t* e_g,
                                 int8_t* sh, int32_t* e_o, int32_t* epilogue_bits, int8_t* uq);
 
+/*
+ * wino_f4_plan_device, wino_f2_plan_device -- the same plan with the weight
+ * transform, the tap calibration and the tap-wise quantization (Sec. III-B:
+ * U = G f G^T, e_G[t] the smallest e with max |U_t| <= 128 2^e, Uq =
+ * clamp(R(U / 2^e_G))) computed on the GPU.  The paper transforms weights
+ * inside the accelerator because Winograd-domain weights are four times the
+ * spatial ones (Sec. IV); here the transform is a plan-time pass on the
+ * device that writes Uq straight into the tap-GEMM layout.
+ *   w_oihw_dev  device fp32 [cout][cin][3][3], contiguous, finite; read on
+ *               `stream`, not retained.
+ * Every other argument is the host argument of wino_f4_plan / wino_f2_plan.
+ * Exact: the result is identical to wino_f4_plan / wino_f2_plan on the same
+ * weights (every rounding and range decision is taken on an exact
+ * floating-point expansion of d^2 U).  Allocates the plan's device memory
+ * and a temporary; synchronizes `stream` before returning.  Errors as for
+ * wino_f4_plan (WINO_EINVAL also for a NULL or non-finite weight tensor);
+ * on error *out is NULL.  wino_f4_plan_info(uq) of such a plan reads Uq back
+ * from the device.
+ */
+wino_status wino_f4_plan_device(wino_f4_plan_t* out, const float* w_oihw_dev, int32_t cin, int32_t cout,
+                                const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                                int32_t out_shift, int32_t relu, hipStream_t stream);
+wino_status wino_f2_plan_device(wino_f4_plan_t* out, const float* w_oihw_dev, int32_t cin, int32_t cout,
+                                const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                                int32_t out_shift, int32_t relu, hipStream_t stream);
+
+/*
+ * wino_f4_plan_int8, wino_f2_plan_int8 -- plan from int8 spatial weights
+ * f_hat = w_int8 * 2^w_scale_exp (the quantized weights that the tap-wise
+ * formula of Sec. III transforms; one power-of-two scale per layer, e.g. from
+ * direct_conv_quantize_weights after reordering to OIHW).  d^2 U = Gint w
+ * Gint^T is then an integer, so the transform and the tap-wise quantization
+ * run in integer arithmetic on the GPU.
+ *   w_oihw_dev    device int8 [cout][cin][3][3], contiguous; read on `stream`.
+ *   w_scale_exp   e_f in [-126, 120] (f_hat is then an exact fp32 value).
+ * Other arguments and errors as for wino_f4_plan_device.  The result is
+ * identical to wino_f4_plan / wino_f2_plan applied to the fp32 weights
+ * w_int8 * 2^w_scale_exp.
+ */
+wino_status wino_f4_plan_int8(wino_f4_plan_t* out, const int8_t* w_oihw_dev, int32_t w_scale_exp, int32_t cin,
+                              int32_t cout, const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                              int32_t out_shift, int32_t relu, hipStream_t stream);
+wino_status wino_f2_plan_int8(wino_f4_plan_t* out, const int8_t* w_oihw_dev, int32_t w_scale_exp, int32_t cin,
+                              int32_t cout, const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                              int32_t out_shift, int32_t relu, hipStream_t stream);
+
 /* Releases a plan and its device memory.  NULL is ignored.  The caller must
  * ensure no convolution using the plan is still running. */
 void wino_f4_plan_destroy(wino_f4_plan_t plan);

@@ -20,6 +20,7 @@ _LIB = None
 EXPORTS = [
     "wino_f4_plan", "wino_f4_plan_tables", "wino_f4_plan_destroy", "wino_f4_plan_info",
     "wino_f2_plan", "wino_f2_plan_tables", "wino_f2_calibrate_input",
+    "wino_f4_plan_device", "wino_f2_plan_device", "wino_f4_plan_int8", "wino_f2_plan_int8",
     "wino_f4_plan_set_tap_kernel", "wino_f4_tap_kernel_choice", "wino_select_algorithm",
     "wino_f4_workspace_bytes",
     "wino_f4_conv_int8", "wino_f4_input_transform", "wino_f4_tap_gemm", "wino_f4_calibrate_input", "wino_f4_calibrate_output",
@@ -58,6 +59,10 @@ def load_library():
         "wino_f2_plan": (I32, [P, P, I32, I32, P, P, P, I32, I32, P]),
         "wino_f2_plan_tables": (I32, [P, I32, I32, P, P, P, I32, P, P, P, P, P]),
         "wino_f2_calibrate_input": (I32, [P, I32, I32, I32, I32, I32, P, P, P]),
+        "wino_f4_plan_device": (I32, [P, P, I32, I32, P, P, P, I32, I32, P]),
+        "wino_f2_plan_device": (I32, [P, P, I32, I32, P, P, P, I32, I32, P]),
+        "wino_f4_plan_int8": (I32, [P, P, I32, I32, I32, P, P, P, I32, I32, P]),
+        "wino_f2_plan_int8": (I32, [P, P, I32, I32, I32, P, P, P, I32, I32, P]),
         "wino_f4_plan_destroy": (None, [P]),
         "wino_f4_plan_info": (I32, [P, P, P, P, P, P, P, P]),
         "wino_f4_plan_set_tap_kernel": (I32, [P, I32]),
@@ -170,6 +175,54 @@ def wino_f4_plan(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0, relu=False,
 def wino_f2_plan(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0, relu=False, stream=None):
     """F(2x2, 3x3) plan: 16-entry in_exp / w_exp."""
     return _make_plan("wino_f2_plan", 2, w_oihw, in_exp, w_exp, bias, out_shift, relu, stream)
+
+
+def _device_weights(w, dtype):
+    """Shape and pointer of a contiguous device weight tensor [cout][cin][3][3]."""
+    import torch
+    if not (isinstance(w, torch.Tensor) and w.is_cuda and w.dtype == dtype and w.dim() == 4
+            and tuple(w.shape[2:]) == (3, 3) and w.is_contiguous()):
+        raise ValueError(f"expected a contiguous {dtype} device tensor [cout][cin][3][3]")
+    return int(w.shape[0]), int(w.shape[1]), _ptr(w)
+
+
+def _make_plan_device(fn, m, w_dev, e_f, in_exp, w_exp, bias, out_shift, relu, stream):
+    import torch
+    ntap = (m + 2) * (m + 2)
+    int8 = e_f is not None
+    cout, cin, wp = _device_weights(w_dev, torch.int8 if int8 else torch.float32)
+    eb = _host(in_exp, np.int8, ntap)
+    eg = None if w_exp is None else _host(w_exp, np.int8, ntap)
+    b = None if bias is None else _host(bias, np.int32, cout)
+    h = ctypes.c_void_p()
+    args = [ctypes.byref(h), wp] + ([int(e_f)] if int8 else []) + [
+        cin, cout, eb.ctypes.data, None if eg is None else eg.ctypes.data,
+        None if b is None else b.ctypes.data, int(out_shift), int(bool(relu)), _stream(stream)]
+    _check(getattr(load_library(), fn)(*args), fn)
+    return WinoF4Plan(h, cin, cout, m)
+
+
+def wino_f4_plan_device(w_dev, in_exp, w_exp=None, bias=None, out_shift=0, relu=False, stream=None):
+    """Plan whose weight transform and tap calibration run on the GPU; w_dev:
+    contiguous fp32 device tensor [cout][cin][3][3].  Same tables as
+    wino_f4_plan on the same weights."""
+    return _make_plan_device("wino_f4_plan_device", 4, w_dev, None, in_exp, w_exp, bias, out_shift, relu, stream)
+
+
+def wino_f2_plan_device(w_dev, in_exp, w_exp=None, bias=None, out_shift=0, relu=False, stream=None):
+    return _make_plan_device("wino_f2_plan_device", 2, w_dev, None, in_exp, w_exp, bias, out_shift, relu, stream)
+
+
+def wino_f4_plan_int8(w_dev, w_scale_exp, in_exp, w_exp=None, bias=None, out_shift=0, relu=False, stream=None):
+    """Plan from int8 spatial weights w * 2^w_scale_exp (w_dev: contiguous
+    int8 device tensor [cout][cin][3][3]), transformed in integers on the GPU."""
+    return _make_plan_device("wino_f4_plan_int8", 4, w_dev, w_scale_exp, in_exp, w_exp, bias, out_shift, relu,
+                             stream)
+
+
+def wino_f2_plan_int8(w_dev, w_scale_exp, in_exp, w_exp=None, bias=None, out_shift=0, relu=False, stream=None):
+    return _make_plan_device("wino_f2_plan_int8", 2, w_dev, w_scale_exp, in_exp, w_exp, bias, out_shift, relu,
+                             stream)
 
 
 def _plan_tables(fn, m, w_oihw, in_exp, w_exp, bias, out_shift):

@@ -23,20 +23,6 @@ using namespace winof4;
 
 namespace {
 
-// One transform F(m x m, 3 x 3): n = m + 2 input rows, n^2 taps, Gint = d G,
-// den2 = d^2, A^T (m x n).
-struct Xform {
-    int m, n, ntap, den2;
-    int gint[6][3];
-    int at[4][6];
-};
-const Xform kF4 = {4, 6, 36, 576,
-                   {{6, 0, 0}, {-4, -4, -4}, {-4, 4, -4}, {1, 2, 4}, {1, -2, 4}, {0, 0, 24}},
-                   {{1, 1, 1, 1, 1, 0}, {0, 1, -1, 2, -2, 0}, {0, 1, 1, 4, 4, 0}, {0, 1, -1, 8, -8, 1}}};
-const Xform kF2 = {2, 4, 16, 4,
-                   {{2, 0, 0}, {1, 1, 1}, {1, -1, 1}, {0, 0, 2}},
-                   {{1, 1, 1, 0}, {0, 1, -1, -1}}};
-
 // Knuth's TwoSum: s + e == a + b exactly, s = fl(a + b).
 inline void two_sum(double a, double b, double& s, double& e) {
     s = a + b;
@@ -152,23 +138,23 @@ int8_t exact_quantize(const Xform& X, const double* t9, double approx, int e) {
 
 }  // namespace
 
-// Host part of the plan: validates the arguments and fills every table of
-// `p` (cin, cout, paddings, e_b, e_g, sh, e_o, epi_bits, uq_host, bias_host).
-static wino_status compute_tables(const Xform& X, wino_f4_plan_s* p, const float* w_oihw, int32_t cin,
-                                  int32_t cout, const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
-                                  int32_t out_shift, int32_t relu) {
-    const int kTaps = X.ntap, n = X.n;
-    if (!w_oihw || !in_exp) return WINO_EINVAL;
+namespace winof4 {
+
+wino_status plan_check_args(const Xform& X, int32_t cin, int32_t cout, const int8_t* in_exp,
+                            const int8_t* w_exp, int32_t out_shift, int32_t relu) {
+    if (!in_exp) return WINO_EINVAL;
     if (cin < 1 || cout < 1) return WINO_EINVAL;
     if (cin > 65536 || cout > 65536) return WINO_EUNSUPPORTED;
     if (out_shift < 0 || out_shift > 62 || (relu != 0 && relu != 1)) return WINO_EINVAL;
-    for (int t = 0; t < kTaps; ++t) {
+    for (int t = 0; t < X.ntap; ++t) {
         if (in_exp[t] < 0 || in_exp[t] > 15) return WINO_EINVAL;
         if (w_exp && (w_exp[t] < -126 || w_exp[t] > 126)) return WINO_EINVAL;
     }
-    for (int64_t i = 0; i < (int64_t)cout * cin * 9; ++i)
-        if (!std::isfinite(w_oihw[i])) return WINO_EINVAL;
+    return WINO_OK;
+}
 
+void plan_set_shape(const Xform& X, wino_f4_plan_s* p, int32_t cin, int32_t cout, int32_t out_shift,
+                    int32_t relu) {
     p->m = X.m;
     p->ntap = X.ntap;
     p->cin = cin;
@@ -177,14 +163,96 @@ static wino_status compute_tables(const Xform& X, wino_f4_plan_s* p, const float
     p->cout_pad = (int32_t)round_up(cout, kCoutPad);
     p->out_shift = out_shift;
     p->relu = relu;
+}
+
+wino_status plan_finish(const Xform& X, wino_f4_plan_s* p, const int8_t* in_exp, const int32_t* bias,
+                        const int32_t* colsum) {
+    const int kTaps = X.ntap, n = X.n, cout = p->cout;
+    for (int t = 0; t < kTaps; ++t)
+        if (p->e_g[t] < -126 || p->e_g[t] > 126) return WINO_ERANGE;
+    // exponents and alignment
+    int e_o = 1 << 20;
+    for (int t = 0; t < kTaps; ++t) {
+        p->e_b[t] = in_exp[t];
+        e_o = std::min(e_o, (int)in_exp[t] + (int)p->e_g[t]);
+    }
+    p->e_o = e_o;
+    for (int t = 0; t < kTaps; ++t) {
+        int s = (int)in_exp[t] + (int)p->e_g[t] - e_o;
+        if (s > 62) return WINO_ERANGE;
+        p->sh[t] = (int8_t)s;
+    }
+    // Epilogue bound: max over (co, i, j) of
+    //   sum_t |A^T[i][a] A^T[j][b]| 2^sh[t] 128 sum_ci |Uq[t][ci][co]|
+    // plus max|bias| plus the rounding constant.  Every partial sum of the
+    // separable output transform is a sub-sum of such a term set, so this
+    // bounds all of them.
+    int64_t maxbias = 0;
+    try {
+        p->bias_host.assign(cout, 0);
+    } catch (...) {
+        return WINO_ENOMEM;
+    }
+    for (int co = 0; co < cout; ++co) {
+        p->bias_host[co] = bias ? bias[co] : 0;
+        maxbias = std::max<int64_t>(maxbias, std::llabs((int64_t)p->bias_host[co]));
+    }
+    unsigned __int128 worst = 0;
+    for (int co = 0; co < cout; ++co)
+        for (int i = 0; i < X.m; ++i)
+            for (int j = 0; j < X.m; ++j) {
+                unsigned __int128 tot = 0;
+                for (int t = 0; t < kTaps; ++t) {
+                    int c = std::abs(X.at[i][t / n] * X.at[j][t % n]);
+                    tot += (unsigned __int128)c * (uint32_t)colsum[(size_t)t * cout + co] * 128u *
+                           ((unsigned __int128)1 << p->sh[t]);
+                }
+                worst = std::max(worst, tot);
+            }
+    worst += (unsigned __int128)maxbias;
+    if (p->out_shift > 0) worst += (unsigned __int128)1 << (p->out_shift - 1);
+    if (worst < ((unsigned __int128)1 << 31) && p->out_shift <= 31) p->epi_bits = 32;
+    else if (worst < ((unsigned __int128)1 << 62)) p->epi_bits = 64;
+    else return WINO_ERANGE;
+    return WINO_OK;
+}
+
+wino_status plan_upload_bias(wino_f4_plan_s* p, hipStream_t stream) {
+    std::vector<int32_t> bias_pad(p->cout_pad, 0);
+    for (int co = 0; co < p->cout; ++co) bias_pad[co] = p->bias_host[co];
+    if (hipMalloc(&p->bias_dev, bias_pad.size() * sizeof(int32_t)) != hipSuccess) {
+        p->bias_dev = nullptr;
+        return WINO_ENOMEM;
+    }
+    bool ok = hipMemcpyAsync(p->bias_dev, bias_pad.data(), bias_pad.size() * sizeof(int32_t),
+                             hipMemcpyHostToDevice, stream) == hipSuccess &&
+              hipStreamSynchronize(stream) == hipSuccess;
+    return ok ? WINO_OK : WINO_EHIP;
+}
+
+}  // namespace winof4
+
+// Host part of the plan: validates the arguments and fills every table of
+// `p` (cin, cout, paddings, e_b, e_g, sh, e_o, epi_bits, uq_host, bias_host).
+static wino_status compute_tables(const Xform& X, wino_f4_plan_s* p, const float* w_oihw, int32_t cin,
+                                  int32_t cout, const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                                  int32_t out_shift, int32_t relu) {
+    const int kTaps = X.ntap, n = X.n;
+    if (!w_oihw) return WINO_EINVAL;
+    wino_status st = plan_check_args(X, cin, cout, in_exp, w_exp, out_shift, relu);
+    if (st != WINO_OK) return st;
+    for (int64_t i = 0; i < (int64_t)cout * cin * 9; ++i)
+        if (!std::isfinite(w_oihw[i])) return WINO_EINVAL;
+    plan_set_shape(X, p, cin, cout, out_shift, relu);
 
     const int64_t nblk = (int64_t)cout * cin;
     // double approximations of d^2 U for every (block, tap)
     std::vector<double> approx;
+    std::vector<int32_t> colsum;
     try {
         approx.resize(nblk * kTaps);
         p->uq_host.assign((size_t)kTaps * cin * cout, 0);
-        p->bias_host.assign(cout, 0);
+        colsum.assign((size_t)kTaps * cout, 0);
     } catch (...) {
         return WINO_ENOMEM;
     }
@@ -213,61 +281,17 @@ static wino_status compute_tables(const Xform& X, wino_f4_plan_s* p, const float
         if (e < -126 || e > 126) return WINO_ERANGE;
         p->e_g[t] = (int8_t)e;
     }
-    // Uq[t][ci][co]
+    // Uq[t][ci][co] and its column sums
     for (int64_t k = 0; k < nblk; ++k) {
         int co = (int)(k / cin), ci = (int)(k % cin);
         for (int t = 0; t < kTaps; ++t) {
             tap_terms(X, w_oihw + k * 9, t / n, t % n, t9);
-            p->uq_host[((size_t)t * cin + ci) * cout + co] =
-                exact_quantize(X, t9, approx[k * kTaps + t], p->e_g[t]);
+            int8_t q = exact_quantize(X, t9, approx[k * kTaps + t], p->e_g[t]);
+            p->uq_host[((size_t)t * cin + ci) * cout + co] = q;
+            colsum[(size_t)t * cout + co] += std::abs((int)q);
         }
     }
-    // exponents and alignment
-    int e_o = 1 << 20;
-    for (int t = 0; t < kTaps; ++t) {
-        p->e_b[t] = in_exp[t];
-        e_o = std::min(e_o, (int)in_exp[t] + (int)p->e_g[t]);
-    }
-    p->e_o = e_o;
-    for (int t = 0; t < kTaps; ++t) {
-        int s = (int)in_exp[t] + (int)p->e_g[t] - e_o;
-        if (s > 62) return WINO_ERANGE;
-        p->sh[t] = (int8_t)s;
-    }
-    // Epilogue bound: max over (co, i, j) of
-    //   sum_t |A^T[i][a] A^T[j][b]| 2^sh[t] 128 sum_ci |Uq[t][ci][co]|
-    // plus max|bias| plus the rounding constant.  Every partial sum of the
-    // separable output transform is a sub-sum of such a term set, so this
-    // bounds all of them.
-    int64_t maxbias = 0;
-    for (int co = 0; co < cout; ++co) {
-        p->bias_host[co] = bias ? bias[co] : 0;
-        maxbias = std::max<int64_t>(maxbias, std::llabs((int64_t)p->bias_host[co]));
-    }
-    unsigned __int128 worst = 0;
-    std::vector<int64_t> colsum(kTaps);
-    for (int co = 0; co < cout; ++co) {
-        for (int t = 0; t < kTaps; ++t) {
-            int64_t s = 0;
-            for (int ci = 0; ci < cin; ++ci) s += std::abs((int)p->uq_host[((size_t)t * cin + ci) * cout + co]);
-            colsum[t] = s;
-        }
-        for (int i = 0; i < X.m; ++i)
-            for (int j = 0; j < X.m; ++j) {
-                unsigned __int128 tot = 0;
-                for (int t = 0; t < kTaps; ++t) {
-                    int c = std::abs(X.at[i][t / n] * X.at[j][t % n]);
-                    tot += (unsigned __int128)c * colsum[t] * 128u * ((unsigned __int128)1 << p->sh[t]);
-                }
-                worst = std::max(worst, tot);
-            }
-    }
-    worst += (unsigned __int128)maxbias;
-    if (out_shift > 0) worst += (unsigned __int128)1 << (out_shift - 1);
-    if (worst < ((unsigned __int128)1 << 31) && out_shift <= 31) p->epi_bits = 32;
-    else if (worst < ((unsigned __int128)1 << 62)) p->epi_bits = 64;
-    else return WINO_ERANGE;
-    return WINO_OK;
+    return plan_finish(X, p, in_exp, bias, colsum.data());
 }
 
 static wino_status plan_tables(const Xform& X, const float* w_oihw, int32_t cin, int32_t cout,
@@ -283,15 +307,21 @@ static wino_status plan_tables(const Xform& X, const float* w_oihw, int32_t cin,
     return st;
 }
 
+static wino_f4_plan_s* new_plan() {
+    wino_f4_plan_s* p = new (std::nothrow) wino_f4_plan_s();
+    if (!p) return nullptr;
+    p->uq_dev = nullptr;
+    p->bias_dev = nullptr;
+    return p;
+}
+
 static wino_status make_plan(const Xform& X, wino_f4_plan_t* out, const float* w_oihw, int32_t cin, int32_t cout,
                              const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias, int32_t out_shift,
                              int32_t relu, hipStream_t stream) {
     if (!out) return WINO_EINVAL;
     *out = nullptr;
-    wino_f4_plan_s* p = new (std::nothrow) wino_f4_plan_s();
+    wino_f4_plan_s* p = new_plan();
     if (!p) return WINO_ENOMEM;
-    p->uq_dev = nullptr;
-    p->bias_dev = nullptr;
     wino_status st = compute_tables(X, p, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, relu);
     if (st != WINO_OK) {
         delete p;
@@ -307,22 +337,46 @@ static wino_status make_plan(const Xform& X, wino_f4_plan_t* out, const float* w
             for (int co = 0; co < cout; ++co)
                 dev_layout[(((size_t)t * nkb + ci / kKStep) * p->cout_pad + co) * kKStep + ci % kKStep] =
                     p->uq_host[((size_t)t * cin + ci) * cout + co];
-    std::vector<int32_t> bias_pad(p->cout_pad, 0);
-    for (int co = 0; co < cout; ++co) bias_pad[co] = p->bias_host[co];
     if (hipGetDevice(&p->device) != hipSuccess) { delete p; return WINO_EHIP; }
     if (hipMalloc(&p->uq_dev, dev_layout.size()) != hipSuccess) { delete p; return WINO_ENOMEM; }
-    if (hipMalloc(&p->bias_dev, bias_pad.size() * sizeof(int32_t)) != hipSuccess) {
-        wino_f4_plan_destroy(p);
-        return WINO_ENOMEM;
-    }
-    bool ok = hipMemcpyAsync(p->uq_dev, dev_layout.data(), dev_layout.size(), hipMemcpyHostToDevice,
-                             stream) == hipSuccess &&
-              hipMemcpyAsync(p->bias_dev, bias_pad.data(), bias_pad.size() * sizeof(int32_t),
-                             hipMemcpyHostToDevice, stream) == hipSuccess &&
-              hipStreamSynchronize(stream) == hipSuccess;
-    if (!ok) {
+    if (hipMemcpyAsync(p->uq_dev, dev_layout.data(), dev_layout.size(), hipMemcpyHostToDevice, stream) !=
+        hipSuccess) {
         wino_f4_plan_destroy(p);
         return WINO_EHIP;
+    }
+    st = plan_upload_bias(p, stream);    // synchronizes the stream, so dev_layout may go
+    if (st != WINO_OK) {
+        wino_f4_plan_destroy(p);
+        return st;
+    }
+    *out = p;
+    return WINO_OK;
+}
+
+// Plans whose weight transform runs on the GPU (fp32 weights on the device,
+// or int8 spatial weights with one power-of-two scale).
+static wino_status make_plan_device(const Xform& X, wino_f4_plan_t* out, const float* w_f32,
+                                    const int8_t* w_i8, int32_t w_scale_exp, int32_t cin, int32_t cout,
+                                    const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                                    int32_t out_shift, int32_t relu, hipStream_t stream) {
+    if (!out) return WINO_EINVAL;
+    *out = nullptr;
+    if (!w_f32 && !w_i8) return WINO_EINVAL;
+    wino_status st = plan_check_args(X, cin, cout, in_exp, w_exp, out_shift, relu);
+    if (st != WINO_OK) return st;
+    if (w_i8 && (w_scale_exp < -126 || w_scale_exp > 120)) return WINO_EINVAL;
+    wino_f4_plan_s* p = new_plan();
+    if (!p) return WINO_ENOMEM;
+    plan_set_shape(X, p, cin, cout, out_shift, relu);
+    if (hipGetDevice(&p->device) != hipSuccess) { delete p; return WINO_EHIP; }
+    std::vector<int32_t> colsum;
+    st = w_f32 ? device_weight_tables(X, p, w_f32, w_exp, stream, colsum)
+               : device_weight_tables_int8(X, p, w_i8, w_scale_exp, w_exp, stream, colsum);
+    if (st == WINO_OK) st = plan_finish(X, p, in_exp, bias, colsum.data());
+    if (st == WINO_OK) st = plan_upload_bias(p, stream);
+    if (st != WINO_OK) {
+        wino_f4_plan_destroy(p);
+        return st;
     }
     *out = p;
     return WINO_OK;
@@ -356,6 +410,42 @@ extern "C" wino_status wino_f2_plan(wino_f4_plan_t* out, const float* w_oihw, in
     return make_plan(kF2, out, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, relu, stream);
 }
 
+extern "C" wino_status wino_f4_plan_device(wino_f4_plan_t* out, const float* w_oihw_dev, int32_t cin,
+                                           int32_t cout, const int8_t* in_exp, const int8_t* w_exp,
+                                           const int32_t* bias, int32_t out_shift, int32_t relu,
+                                           hipStream_t stream) {
+    if (!w_oihw_dev) return WINO_EINVAL;
+    return make_plan_device(kF4, out, w_oihw_dev, nullptr, 0, cin, cout, in_exp, w_exp, bias, out_shift, relu,
+                            stream);
+}
+
+extern "C" wino_status wino_f2_plan_device(wino_f4_plan_t* out, const float* w_oihw_dev, int32_t cin,
+                                           int32_t cout, const int8_t* in_exp, const int8_t* w_exp,
+                                           const int32_t* bias, int32_t out_shift, int32_t relu,
+                                           hipStream_t stream) {
+    if (!w_oihw_dev) return WINO_EINVAL;
+    return make_plan_device(kF2, out, w_oihw_dev, nullptr, 0, cin, cout, in_exp, w_exp, bias, out_shift, relu,
+                            stream);
+}
+
+extern "C" wino_status wino_f4_plan_int8(wino_f4_plan_t* out, const int8_t* w_oihw_dev, int32_t w_scale_exp,
+                                         int32_t cin, int32_t cout, const int8_t* in_exp, const int8_t* w_exp,
+                                         const int32_t* bias, int32_t out_shift, int32_t relu,
+                                         hipStream_t stream) {
+    if (!w_oihw_dev) return WINO_EINVAL;
+    return make_plan_device(kF4, out, nullptr, w_oihw_dev, w_scale_exp, cin, cout, in_exp, w_exp, bias,
+                            out_shift, relu, stream);
+}
+
+extern "C" wino_status wino_f2_plan_int8(wino_f4_plan_t* out, const int8_t* w_oihw_dev, int32_t w_scale_exp,
+                                         int32_t cin, int32_t cout, const int8_t* in_exp, const int8_t* w_exp,
+                                         const int32_t* bias, int32_t out_shift, int32_t relu,
+                                         hipStream_t stream) {
+    if (!w_oihw_dev) return WINO_EINVAL;
+    return make_plan_device(kF2, out, nullptr, w_oihw_dev, w_scale_exp, cin, cout, in_exp, w_exp, bias,
+                            out_shift, relu, stream);
+}
+
 extern "C" void wino_f4_plan_destroy(wino_f4_plan_t p) {
     if (!p) return;
     if (p->uq_dev) hipFree(p->uq_dev);
@@ -377,7 +467,25 @@ extern "C" wino_status wino_f4_plan_info(wino_f4_plan_t p, int8_t* e_g, int8_t* 
     if (sh) std::memcpy(sh, p->sh, p->ntap);
     if (e_o) *e_o = p->e_o;
     if (epilogue_bits) *epilogue_bits = p->epi_bits;
-    if (uq) std::memcpy(uq, p->uq_host.data(), p->uq_host.size());
+    if (uq) {
+        if (!p->uq_host.empty()) {
+            std::memcpy(uq, p->uq_host.data(), p->uq_host.size());
+        } else {
+            // device-built plan: read the k-blocked device copy back
+            const int nkb = p->cin_pad / kKStep;
+            std::vector<int8_t> dev((size_t)p->ntap * p->cout_pad * p->cin_pad);
+            int cur = 0;
+            if (hipGetDevice(&cur) != hipSuccess || hipSetDevice(p->device) != hipSuccess) return WINO_EHIP;
+            hipError_t e = hipMemcpy(dev.data(), p->uq_dev, dev.size(), hipMemcpyDeviceToHost);
+            hipSetDevice(cur);
+            if (e != hipSuccess) return WINO_EHIP;
+            for (int t = 0; t < p->ntap; ++t)
+                for (int ci = 0; ci < p->cin; ++ci)
+                    for (int co = 0; co < p->cout; ++co)
+                        uq[((size_t)t * p->cin + ci) * p->cout + co] =
+                            dev[(((size_t)t * nkb + ci / kKStep) * p->cout_pad + co) * kKStep + ci % kKStep];
+        }
+    }
     if (cin) *cin = p->cin;
     if (cout) *cout = p->cout;
     return WINO_OK;

@@ -26,6 +26,44 @@ struct TapTables {
     int32_t sh[kTaps];   // alignment shifts e_B + e_G - e_o
 };
 
+// One transform F(m x m, 3 x 3): n = m + 2 input rows, n^2 taps, Gint = d G
+// with integer entries (Sec. II matrices: d = 24 for F4, 2 for F2),
+// den2 = d^2, A^T (m x n).
+struct Xform {
+    int m, n, ntap, den2;
+    int gint[6][3];
+    int at[4][6];
+};
+inline constexpr Xform kF4 = {4, 6, 36, 576,
+                              {{6, 0, 0}, {-4, -4, -4}, {-4, 4, -4}, {1, 2, 4}, {1, -2, 4}, {0, 0, 24}},
+                              {{1, 1, 1, 1, 1, 0}, {0, 1, -1, 2, -2, 0}, {0, 1, 1, 4, 4, 0}, {0, 1, -1, 8, -8, 1}}};
+inline constexpr Xform kF2 = {2, 4, 16, 4,
+                              {{2, 0, 0}, {1, 1, 1}, {1, -1, 1}, {0, 0, 2}},
+                              {{1, 1, 1, 0}, {0, 1, -1, -1}}};
+
+}  // namespace winof4
+
+struct wino_f4_plan_s;
+
+namespace winof4 {
+// Plan assembly shared by the host plan (plan.cpp) and the on-device weight
+// transform (plan_device.hip).
+wino_status plan_check_args(const Xform& X, int32_t cin, int32_t cout, const int8_t* in_exp,
+                            const int8_t* w_exp, int32_t out_shift, int32_t relu);
+void plan_set_shape(const Xform& X, wino_f4_plan_s* p, int32_t cin, int32_t cout, int32_t out_shift,
+                    int32_t relu);
+// Fills e_b, e_o, sh, bias_host and epi_bits from p->e_g and the column sums
+// colsum[t * cout + co] = sum_ci |Uq[t][ci][co]|.
+wino_status plan_finish(const Xform& X, wino_f4_plan_s* p, const int8_t* in_exp, const int32_t* bias,
+                        const int32_t* colsum);
+// Uploads the zero-padded bias; synchronizes `stream`.
+wino_status plan_upload_bias(wino_f4_plan_s* p, hipStream_t stream);
+// Device parts of the plan (plan_device.hip): fill p->e_g, write p->uq_dev
+// (allocated here) and return the column sums.
+wino_status device_weight_tables(const Xform& X, wino_f4_plan_s* p, const float* w_dev, const int8_t* w_exp,
+                                 hipStream_t stream, std::vector<int32_t>& colsum);
+wino_status device_weight_tables_int8(const Xform& X, wino_f4_plan_s* p, const int8_t* w_dev, int32_t w_scale_exp,
+                                      const int8_t* w_exp, hipStream_t stream, std::vector<int32_t>& colsum);
 }  // namespace winof4
 
 struct wino_f4_plan_s {
@@ -40,6 +78,6 @@ struct wino_f4_plan_s {
     int32_t device;
     int8_t* uq_dev;                   // [ntap][cin_pad/64][cout_pad][64], zero padded
     int32_t* bias_dev;                // [cout_pad], zero padded
-    std::vector<int8_t> uq_host;      // [ntap][cin][cout]
+    std::vector<int8_t> uq_host;      // [ntap][cin][cout]; empty for device-built plans
     std::vector<int32_t> bias_host;   // [cout]
 };
