@@ -43,6 +43,7 @@ def parse():
                     help="Winograd F(4x4,3x3) (the default) or F(2x2,3x3)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-direct", action="store_true")
+    ap.add_argument("--no-plan-timing", action="store_true", help="skip timing the on-device plan builds")
     ap.add_argument("--cpu-images", type=int, default=0, help="oracle sample size (images); 0 = auto")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 256 MiB device-to-device copy (scale reference for HBM counters)")
@@ -177,8 +178,34 @@ def main():
     out_shift = spec.out_shift
     if out_shift is None:
         out_shift, _ = W.wino_f4_calibrate_output(plan0, xd, n, h, w, layout, ws)
+    t0 = time.perf_counter()
     plan = make_plan(f, eb, bias=bias, out_shift=out_shift, relu=spec.relu)
+    plan_host_ms = (time.perf_counter() - t0) * 1e3
     info = W.wino_f4_plan_info(plan)
+    plan_ms = {"host_exact": plan_host_ms}
+    if not args.no_plan_timing:
+        # the same plan with the weight transform on the device: fp32 weights,
+        # and int8 spatial weights (one power-of-two scale); wall time of the
+        # whole call (allocation, kernels, read-back, synchronization), median
+        make_dev = W.wino_f4_plan_device if mt == 4 else W.wino_f2_plan_device
+        make_i8 = W.wino_f4_plan_int8 if mt == 4 else W.wino_f2_plan_int8
+        fd = torch.from_numpy(np.ascontiguousarray(f, dtype=np.float32)).cuda()
+        wq8, e_f = W.direct_conv_quantize_weights(f)
+        wi8 = torch.from_numpy(np.ascontiguousarray(wq8.transpose(0, 3, 1, 2))).cuda()
+        torch.cuda.synchronize()
+        for key, mk in (("device_fp32", lambda: make_dev(fd, eb, bias=bias, out_shift=out_shift, relu=spec.relu)),
+                        ("device_int8", lambda: make_i8(wi8, e_f, eb, bias=bias, out_shift=out_shift,
+                                                        relu=spec.relu))):
+            ts = []
+            for _ in range(5):
+                t0 = time.perf_counter()
+                pd = mk()
+                ts.append((time.perf_counter() - t0) * 1e3)
+                if key == "device_fp32":
+                    di = W.wino_f4_plan_info(pd)
+                    assert di["e_g"] == info["e_g"] and di["sh"] == info["sh"], "device plan differs"
+                pd.close()
+            plan_ms[key] = float(np.median(ts))
 
     def step():
         W.wino_f4_conv_int8(plan, xd, y, n, h, w, layout, variant, ws if variant == W.SPLIT else None)
@@ -283,6 +310,7 @@ def main():
         "tap_gemm_mfma_frac_of_step": tap_ops / (ms * 1e-3) / 1e12 / PEAK_INT8_TOPS,
         "direct_conv": direct,
         "cpu_baseline": cpu,
+        "plan_ms": plan_ms,
     }
     print(json.dumps(line), flush=True)
 
