@@ -11,6 +11,9 @@ Readings of points the paper leaves open:
   * the power-of-two scale is 2^ceil(log2 s); with s = a/128 this is the
     smallest integer e with a <= 128 * 2^e (``cexp``), computed exactly.
     A zero maximum gets e = 0.
+  * n-bit quantization (Eq. quant with n = bits) uses s = a / 2^(n-1) and
+    [-2^(n-1), 2^(n-1)-1]; the Winograd domain of the int8/10 variant
+    (Sec. V) has n = 10, everything else n = 8.
 """
 from fractions import Fraction
 
@@ -30,21 +33,27 @@ def clamp(q, lo=QMIN, hi=QMAX):
     return max(lo, min(hi, q))
 
 
-def quantize_exact(x, e):
+def qrange(bits=8):
+    """Integer range [-2^(bits-1), 2^(bits-1) - 1] of a bits-wide quantizer."""
+    return -(1 << (bits - 1)), (1 << (bits - 1)) - 1
+
+
+def quantize_exact(x, e, bits=8):
     """Eq. quant with the power-of-two scale 2^e: clamp(R(x / 2^e)) for an
     exact rational x and an integer e (any sign)."""
-    return clamp(round_half_up(Fraction(x) / Fraction(2) ** e))
+    return clamp(round_half_up(Fraction(x) / Fraction(2) ** e), *qrange(bits))
 
 
-def cexp(a):
-    """Smallest integer e with a <= 128 * 2^e, i.e. ceil(log2(a / 128)),
-    for an exact non-negative rational a.  cexp(0) = 0."""
+def cexp(a, bits=8):
+    """Smallest integer e with a <= 2^(bits-1) * 2^e (128 * 2^e for int8),
+    i.e. ceil(log2(a / 2^(bits-1))), for an exact non-negative rational a.
+    cexp(0) = 0."""
     a = Fraction(a)
     if a < 0:
         raise ValueError("cexp of a negative value")
     if a == 0:
         return 0
-    q = a / 128
+    q = a / (1 << (bits - 1))
     # first guess from bit lengths, then correct exactly
     e = q.numerator.bit_length() - q.denominator.bit_length()
     while Fraction(2) ** e < q:
@@ -67,3 +76,8 @@ def shift_round_int(v, e):
 
 def clamp_int8(v):
     return np.clip(np.asarray(v, dtype=np.int64), QMIN, QMAX)
+
+
+def clamp_bits(v, bits=8):
+    lo, hi = qrange(bits)
+    return np.clip(np.asarray(v, dtype=np.int64), lo, hi)

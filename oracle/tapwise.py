@@ -28,6 +28,11 @@ pixel on each side; ceil(H/4) x ceil(W/4) tiles are computed and outputs
 outside the image are discarded (zero padding to a multiple of 4, Sec. V).
 For F(2x2, 3x3) the same holds with 4x4 windows at stride 2, 16 taps, and
 G = G2int / 2 (so U = unum * 2^p / 4).
+
+int8/10 (Sec. V): with bits = 10 the Winograd-domain integers Vq and Uq are
+quantized to 10 bits ([-512, 511], scale exponents from 2^9 instead of 2^7)
+while the spatial input and output stay int8; a plan
+records its ``bits`` and every function that takes a plan follows it.
 """
 from fractions import Fraction
 
@@ -105,7 +110,7 @@ def _u_abs_max_per_tap(unum, p, spec=F4):
     return out
 
 
-def _quantize_unum(unum, p, e_g, spec=F4):
+def _quantize_unum(unum, p, e_g, spec=F4, bits=8):
     """Uq = clamp(R(U / 2^e_G)) with U = unum * 2^p / den^2, per tap:
     R(v) = floor(v + 1/2) = floor((2 unum 2^(p - e_G) + den^2) / (2 den^2))."""
     cout, cin = unum.shape[:2]
@@ -124,13 +129,15 @@ def _quantize_unum(unum, p, e_g, spec=F4):
         q = num // den                                 # floor division
         uq[:, :, t] = np.clip(q.astype(np.int64) if q.dtype != object
                               else np.array([[int(v) for v in row] for row in q], dtype=np.int64),
-                              quant.QMIN, quant.QMAX)
+                              *quant.qrange(bits))
     return uq
 
 
-def make_plan(f, e_b, e_g=None, bias=None, out_shift=0, relu=False, m=4):
-    """The offline step: returns a dict with m, e_B, e_G, e, e_o, sh, Uq
-    [ntap, cin, cout] (tap-major GEMM operand), bias [cout], out_shift, relu."""
+def make_plan(f, e_b, e_g=None, bias=None, out_shift=0, relu=False, m=4, bits=8):
+    """The offline step: returns a dict with m, bits, e_B, e_G, e, e_o, sh, Uq
+    [ntap, cin, cout] (tap-major GEMM operand), bias [cout], out_shift, relu.
+    ``bits`` is the width of the Winograd-domain integers (Vq and Uq): 8, or
+    10 for the int8/10 variant of Sec. V (spatial input and output stay int8)."""
     spec = SPECS[m]
     f = np.asarray(f, dtype=np.float32)
     cout, cin = f.shape[:2]
@@ -138,17 +145,17 @@ def make_plan(f, e_b, e_g=None, bias=None, out_shift=0, relu=False, m=4):
     assert len(e_b) == spec.ntap
     unum, p = weight_transform_exact(f, spec)
     if e_g is None:
-        e_g = [quant.cexp(a) for a in _u_abs_max_per_tap(unum, p, spec)]
+        e_g = [quant.cexp(a, bits) for a in _u_abs_max_per_tap(unum, p, spec)]
     else:
         e_g = [int(v) for v in e_g]
         assert len(e_g) == spec.ntap
-    uq = _quantize_unum(unum, p, e_g, spec)           # [cout, cin, ntap]
+    uq = _quantize_unum(unum, p, e_g, spec, bits)     # [cout, cin, ntap]
     e = [e_b[t] + e_g[t] for t in range(spec.ntap)]
     e_o = min(e)
     sh = [e[t] - e_o for t in range(spec.ntap)]
     if bias is None:
         bias = np.zeros(cout, dtype=np.int64)
-    return dict(m=m, cin=cin, cout=cout, e_b=e_b, e_g=e_g, e=e, e_o=e_o, sh=sh,
+    return dict(m=m, bits=bits, cin=cin, cout=cout, e_b=e_b, e_g=e_g, e=e, e_o=e_o, sh=sh,
                 uq=np.ascontiguousarray(uq.transpose(2, 1, 0)),   # [ntap, cin, cout]
                 bias=np.asarray(bias, dtype=np.int64).copy(),
                 out_shift=int(out_shift), relu=bool(relu))
@@ -182,12 +189,12 @@ def input_transform(d, spec=F4):
     return np.einsum("ar,...rc,bc->...ab", spec.BT, d, spec.BT)
 
 
-def quantize_input_taps(v, e_b, spec=F4):
-    """Vq[..., a, b] = clamp(R(V[..., a, b] / 2^e_B[n a + b]))."""
+def quantize_input_taps(v, e_b, spec=F4, bits=8):
+    """Vq[..., a, b] = clamp(R(V[..., a, b] / 2^e_B[n a + b])) to bits-wide integers."""
     vq = np.empty_like(v)
     for t in range(spec.ntap):
         a, b = divmod(t, spec.n)
-        vq[..., a, b] = quant.clamp_int8(quant.shift_round_int(v[..., a, b], e_b[t]))
+        vq[..., a, b] = quant.clamp_bits(quant.shift_round_int(v[..., a, b], e_b[t]), bits)
     return vq
 
 
@@ -201,7 +208,7 @@ def tap_major(vq, spec=F4):
 def tap_gemm(vq_tm, uq):
     """M[t] = Vq[t] @ Uq[t]: [ntap, T, cin] x [ntap, cin, cout] -> int64 [ntap, T, cout].
     Evaluated with float64 BLAS, exact because every partial sum is an
-    integer of magnitude <= 2^14 * cin < 2^53."""
+    integer of magnitude <= 2^18 * cin < 2^53 (operands of at most 10 bits)."""
     cin = vq_tm.shape[2]
     assert cin < (1 << 38)
     m = np.matmul(vq_tm.astype(np.float64), uq.astype(np.float64))
@@ -238,7 +245,7 @@ def prequant_output(x, plan):
     n, cin, h, w = x.shape
     assert cin == plan["cin"]
     v = input_transform(input_tiles(x, spec), spec)
-    vq = quantize_input_taps(v, plan["e_b"], spec)
+    vq = quantize_input_taps(v, plan["e_b"], spec, plan.get("bits", 8))
     m = tap_gemm(tap_major(vq, spec), plan["uq"])
     y = assemble(output_transform(m, plan["sh"], spec), n, h, w, spec)
     return y + plan["bias"][None, :, None, None]
@@ -256,10 +263,10 @@ def conv_int8(x, plan):
     return requant(prequant_output(x, plan), plan["out_shift"], plan["relu"])
 
 
-def input_taps_quantized(x, e_b, m=4):
+def input_taps_quantized(x, e_b, m=4, bits=8):
     """Vq in tap-major layout [ntap, T, cin] (what the input-transform stage emits)."""
     spec = SPECS[m]
-    return tap_major(quantize_input_taps(input_transform(input_tiles(x, spec), spec), e_b, spec), spec)
+    return tap_major(quantize_input_taps(input_transform(input_tiles(x, spec), spec), e_b, spec, bits), spec)
 
 
 # ---------------------------------------------------------------------------
@@ -294,7 +301,8 @@ def conv_int8_naive(x, plan):
                         a, bb = divmod(t, k)
                         v = sum(bt[a][r] * d[r][c] * bt[bb][c]
                                 for r in range(k) for c in range(k))
-                        q = quant.clamp(quant.round_half_up(Fraction(v, 2 ** plan["e_b"][t])))
+                        q = quant.clamp(quant.round_half_up(Fraction(v, 2 ** plan["e_b"][t])),
+                                        *quant.qrange(plan.get("bits", 8)))
                         row.append(q)
                     vq.append(row)
                 for co in range(cout):
@@ -329,9 +337,10 @@ def input_tap_absmax(x, m=4):
     return [int(np.abs(v[..., t // spec.n, t % spec.n]).max(initial=0)) for t in range(spec.ntap)]
 
 
-def calibrate_input_exps(x, m=4):
-    """e_B[t] = max(0, cexp(max over tiles and channels of |V_t|)), <= 15."""
-    return [min(EB_MAX, max(0, quant.cexp(a))) for a in input_tap_absmax(x, m)]
+def calibrate_input_exps(x, m=4, bits=8):
+    """e_B[t] = max(0, cexp(max over tiles and channels of |V_t|)), <= 15, for
+    bits-wide input taps."""
+    return [min(EB_MAX, max(0, quant.cexp(a, bits))) for a in input_tap_absmax(x, m)]
 
 
 def calibrate_out_shift(x, plan):
@@ -346,9 +355,11 @@ def calibrate_out_shift(x, plan):
 def epilogue_bound(plan):
     """Upper bound on |every partial sum of the output transform| plus bias
     and rounding constant:
-      max_co max_ij sum_t |A^T[i,a] A^T[j,b]| 2^sh[t] 128 sum_ci |Uq[t,ci,co]|
-      + max|bias| + (2^(out_shift-1) if out_shift > 0)."""
+      max_co max_ij sum_t |A^T[i,a] A^T[j,b]| 2^sh[t] vmax sum_ci |Uq[t,ci,co]|
+      + max|bias| + (2^(out_shift-1) if out_shift > 0), with vmax = 2^(bits-1)
+      the largest |Vq| (128 for int8)."""
     spec = spec_of(plan)
+    vmax = 1 << (plan.get("bits", 8) - 1)
     uq = plan["uq"]
     s = np.abs(uq).sum(axis=1)                                 # [ntap, cout]
     best = 0
@@ -358,7 +369,7 @@ def epilogue_bound(plan):
                 tot = 0
                 for t in range(spec.ntap):
                     a, b = divmod(t, spec.n)
-                    tot += (abs(int(spec.AT[i, a]) * int(spec.AT[j, b])) * (1 << plan["sh"][t]) * 128
+                    tot += (abs(int(spec.AT[i, a]) * int(spec.AT[j, b])) * (1 << plan["sh"][t]) * vmax
                             * int(s[t, co]))
                 best = max(best, tot)
     rnd = (1 << (plan["out_shift"] - 1)) if plan["out_shift"] > 0 else 0
