@@ -25,6 +25,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "Winograd F4 int8 conv: effective TOPS (direct-equiv) + % of int8 MFMA peak"
 PEAK_INT8_TOPS = 5000.0      # MI355X dense int8 MFMA, TOP/s
+PEAK_FP16_TFLOPS = 2500.0    # MI355X dense fp16 MFMA, TFLOP/s (the int8/10 tap GEMM)
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, GB/s
 
 
@@ -42,6 +43,10 @@ def parse():
     ap.add_argument("--transform", default="f4", choices=["f4", "f2"],
                     help="Winograd F(4x4,3x3) (the default) or F(2x2,3x3)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--bits", type=int, default=8, choices=[8, 10],
+                    help="Winograd-domain integer width: 8, or 10 for the int8/10 variant")
+    ap.add_argument("--tap-kernel", default="auto", choices=["auto", "resident", "rows", "64x32", "32x32", "16x16"],
+                    help="force the tap-GEMM kernel (wino_f4_plan_set_tap_kernel)")
     ap.add_argument("--no-direct", action="store_true")
     ap.add_argument("--no-plan-timing", action="store_true", help="skip timing the on-device plan builds")
     ap.add_argument("--cpu-images", type=int, default=0, help="oracle sample size (images); 0 = auto")
@@ -170,8 +175,12 @@ def main():
 
     # offline: calibration and plan (not timed)
     mt = 4 if args.transform == "f4" else 2
-    calibrate = W.wino_f4_calibrate_input if mt == 4 else W.wino_f2_calibrate_input
-    make_plan = W.wino_f4_plan if mt == 4 else W.wino_f2_plan
+    if args.bits == 10:
+        calibrate = W.wino_f4_calibrate_input_i10 if mt == 4 else W.wino_f2_calibrate_input_i10
+        make_plan = W.wino_f4_plan_i10 if mt == 4 else W.wino_f2_plan_i10
+    else:
+        calibrate = W.wino_f4_calibrate_input if mt == 4 else W.wino_f2_calibrate_input
+        make_plan = W.wino_f4_plan if mt == 4 else W.wino_f2_plan
     eb, _ = calibrate(xd, n, cin, h, w, layout)
     plan0 = make_plan(f, eb, bias=bias, out_shift=0, relu=spec.relu)
     ws = torch.empty(max(1, W.wino_f4_workspace_bytes(plan0, n, h, w, W.SPLIT)), dtype=torch.int8, device="cuda")
@@ -182,8 +191,11 @@ def main():
     plan = make_plan(f, eb, bias=bias, out_shift=out_shift, relu=spec.relu)
     plan_host_ms = (time.perf_counter() - t0) * 1e3
     info = W.wino_f4_plan_info(plan)
+    W.wino_f4_plan_set_tap_kernel(plan, {"auto": W.TAP_AUTO, "resident": W.TAP_RESIDENT, "rows": W.TAP_ROWS,
+                                         "64x32": W.TAP_RESIDENT_64X32, "32x32": W.TAP_RESIDENT_32X32,
+                                         "16x16": W.TAP_RESIDENT_16X16}[args.tap_kernel])
     plan_ms = {"host_exact": plan_host_ms}
-    if not args.no_plan_timing:
+    if not args.no_plan_timing and args.bits == 8:
         # the same plan with the weight transform on the device: fp32 weights,
         # and int8 spatial weights (one power-of-two scale); wall time of the
         # whole call (allocation, kernels, read-back, synchronization), median
@@ -224,9 +236,10 @@ def main():
     rows = W.wino_f4_tap_kernel_choice(plan, n, h, w) == W.TAP_ROWS
     # kernel names as the profiler shows them (template arguments included;
     # the tap-resident kernel's block configuration is a class argument)
-    k1_name, k1_inst = "wino_input_xform", f"wino_input_xform<{mt},{lay},0>"
+    k1_name, k1_inst = "wino_input_xform", f"wino_input_xform<{mt},{lay},0,{args.bits}>"
     k2_name = "wino_tap_gemm_rows" if rows else "wino_tap_gemm"
-    k2_inst = f"wino_tap_gemm_rows<{lay}>" if rows else f"wino_tap_gemm<{mt},{lay},{info['epilogue_bits']},0>"
+    k2_inst = (f"wino_tap_gemm_rows<{lay}>" if rows
+               else f"wino_tap_gemm<{mt},{lay},{info['epilogue_bits']},0,{args.bits}>")
     k1_ms = k2_ms = None
     if variant == W.SPLIT:
         k1 = lambda: W.wino_f4_input_transform(plan, xd, n, h, w, layout, ws)
@@ -236,11 +249,14 @@ def main():
 
     direct_ops = 2.0 * 9 * n * h * w * cin * cout
     tap_ops = 2.0 * ntap * T * cin * cout
+    # the int8/10 tap GEMM multiplies exact 10-bit integers on fp16 matrix cores
+    k2_peak, k2_unit = (PEAK_FP16_TFLOPS, "TFLOP/s") if args.bits == 10 else (PEAK_INT8_TOPS, "TOP/s")
     value = direct_ops / (ms * 1e-3) / 1e12
-    k1_bytes = n * h * w * cin + ntap * T * cin                 # read x, write Vq
-    k2_bytes = ntap * T * cin + ntap * cin * cout + n * h * w * cout + 4 * cout
+    eb_bytes = 2 if args.bits == 10 else 1                       # Vq / Uq element: int8 or fp16
+    k1_bytes = n * h * w * cin + eb_bytes * ntap * T * cin      # read x, write Vq
+    k2_bytes = eb_bytes * (ntap * T * cin + ntap * cin * cout) + n * h * w * cout + 4 * cout
     kernels = {}
-    cfg_tag = args.config + (f"L{args.layer}" if args.layer else "")
+    cfg_tag = args.config + (f"L{args.layer}" if args.layer else "") + ("_i10" if args.bits == 10 else "")
     if k1_ms is not None:
         kernels[k1_name] = {"ms": k1_ms, "p10_ms": k1_p10, "p90_ms": k1_p90, "bound": "hbm", "bytes": k1_bytes,
                             "GB/s": k1_bytes / (k1_ms * 1e-3) / 1e9,
@@ -248,12 +264,12 @@ def main():
                             "traffic_bytes": counter_traffic(cfg_tag, args.layout, k1_inst, args.transform)}
         kernels[k2_name] = {"ms": k2_ms, "p10_ms": k2_p10, "p90_ms": k2_p90, "bound": "mfma", "ops": tap_ops,
                             "TOP/s": tap_ops / (k2_ms * 1e-3) / 1e12,
-                            "frac": tap_ops / (k2_ms * 1e-3) / 1e12 / PEAK_INT8_TOPS,
+                            "frac": tap_ops / (k2_ms * 1e-3) / 1e12 / k2_peak,
                             "GB/s_algorithmic": k2_bytes / (k2_ms * 1e-3) / 1e9,
                             "traffic_bytes": counter_traffic(cfg_tag, args.layout, k2_inst, args.transform)}
         if k2_ms >= k1_ms:
             roofline = {"kernel": k2_name, "bound": "mfma", "achieved": kernels[k2_name]["TOP/s"],
-                        "peak": PEAK_INT8_TOPS, "unit": "TOP/s", "frac": kernels[k2_name]["frac"],
+                        "peak": k2_peak, "unit": k2_unit, "frac": kernels[k2_name]["frac"],
                         "traffic": kernels[k2_name]["traffic_bytes"]}
         else:
             roofline = {"kernel": k1_name, "bound": "hbm", "achieved": kernels[k1_name]["GB/s"],
@@ -299,15 +315,16 @@ def main():
     line = {
         "metric": METRIC, "value": value, "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "int8", "data": "synthetic",
+        "vs_baseline": None, "dtype": "int8" if args.bits == 8 else "int8/int10", "data": "synthetic",
         "config": {"workload": f"{args.config}: {wl.desc}" + (f" (layer {args.layer})" if args.layer else ""),
                    "n": n, "cin": cin, "cout": cout, "h": h, "w": w,
-                   "layout": args.layout, "variant": args.variant, "transform": args.transform, "tiles": T,
+                   "layout": args.layout, "variant": args.variant, "transform": args.transform,
+                   "winograd_bits": args.bits, "tiles": T,
                    "e_b": eb, "e_g": info["e_g"], "out_shift": out_shift,
                    "epilogue_bits": info["epilogue_bits"]},
         "roofline": roofline,
         "kernels": kernels,
-        "tap_gemm_mfma_frac_of_step": tap_ops / (ms * 1e-3) / 1e12 / PEAK_INT8_TOPS,
+        "tap_gemm_mfma_frac_of_step": tap_ops / (ms * 1e-3) / 1e12 / k2_peak,
         "direct_conv": direct,
         "cpu_baseline": cpu,
         "plan_ms": plan_ms,

@@ -227,6 +227,40 @@ wino_status wino_f2_plan_int8(wino_f4_plan_t* out, const int8_t* w_oihw_dev, int
                               int32_t cout, const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
                               int32_t out_shift, int32_t relu, hipStream_t stream);
 
+/*
+ * wino_f4_plan_i10, wino_f2_plan_i10, wino_f4_plan_tables_i10,
+ * wino_f2_plan_tables_i10 -- the int8/10 variant (Sec. V): int8 input and
+ * output in the spatial domain, 10-bit integers in the Winograd domain.  Vq
+ * and Uq are quantized to [-512, 511] with power-of-two tap scales chosen
+ * from 2^9 (Eq. quant with n = 10: e_G[t] is the smallest e with
+ * max |U_t| <= 512 2^e); everything else is the 8-bit scheme.  Arguments,
+ * errors and exactness as for wino_f4_plan / wino_f4_plan_tables, except
+ * that in_exp should come from wino_f4_calibrate_input_i10 and the tables'
+ * uq output is int16 [ntap][cin][cout].  The resulting plan runs through
+ * wino_f4_conv_int8 (SPLIT only; FUSED returns WINO_EUNSUPPORTED),
+ * wino_f4_workspace_bytes (twice the 8-bit workspace: Vq is fp16),
+ * wino_f4_input_transform, wino_f4_tap_gemm, wino_f4_calibrate_output and
+ * the debug exports (wino_f4_debug_input_transform then writes fp16 values
+ * [ntap][ntiles][cin], each an exact 10-bit integer).  wino_f4_plan_info
+ * returns its exponents and epilogue width; its uq argument must be NULL
+ * (WINO_EINVAL otherwise).  The tap GEMM runs on fp16 matrix cores: the
+ * 10-bit integers are exact in fp16 and each 32-channel partial sum is an
+ * integer below 2^24, exact in the fp32 accumulator, before it is added to
+ * the int32 (or int64) accumulation -- the result is bit-exact.
+ */
+wino_status wino_f4_plan_i10(wino_f4_plan_t* out, const float* w_oihw, int32_t cin, int32_t cout,
+                             const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias, int32_t out_shift,
+                             int32_t relu, hipStream_t stream);
+wino_status wino_f2_plan_i10(wino_f4_plan_t* out, const float* w_oihw, int32_t cin, int32_t cout,
+                             const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias, int32_t out_shift,
+                             int32_t relu, hipStream_t stream);
+wino_status wino_f4_plan_tables_i10(const float* w_oihw, int32_t cin, int32_t cout, const int8_t* in_exp,
+                                    const int8_t* w_exp, const int32_t* bias, int32_t out_shift, int8_t* e_g,
+                                    int8_t* sh, int32_t* e_o, int32_t* epilogue_bits, int16_t* uq);
+wino_status wino_f2_plan_tables_i10(const float* w_oihw, int32_t cin, int32_t cout, const int8_t* in_exp,
+                                    const int8_t* w_exp, const int32_t* bias, int32_t out_shift, int8_t* e_g,
+                                    int8_t* sh, int32_t* e_o, int32_t* epilogue_bits, int16_t* uq);
+
 /* Releases a plan and its device memory.  NULL is ignored.  The caller must
  * ensure no convolution using the plan is still running. */
 void wino_f4_plan_destroy(wino_f4_plan_t plan);
@@ -309,6 +343,16 @@ wino_status wino_f4_calibrate_input(const int8_t* x, int32_t n, int32_t cin, int
 wino_status wino_f2_calibrate_input(const int8_t* x, int32_t n, int32_t cin, int32_t h,
                                     int32_t w, wino_layout layout, int32_t* absmax,
                                     int8_t* e_b, hipStream_t stream);
+
+/* wino_f4_calibrate_input_i10, wino_f2_calibrate_input_i10 -- the input
+ * calibration of the int8/10 variant (Sec. V): the same maxima, with
+ * e_B[t] = min(15, max(0, smallest e with absmax[t] <= 512 * 2^e)) for
+ * 10-bit input taps.  Arguments and errors as for wino_f4_calibrate_input
+ * (36 or 16 entries). */
+wino_status wino_f4_calibrate_input_i10(const int8_t* x, int32_t n, int32_t cin, int32_t h, int32_t w,
+                                        wino_layout layout, int32_t* absmax, int8_t* e_b, hipStream_t stream);
+wino_status wino_f2_calibrate_input_i10(const int8_t* x, int32_t n, int32_t cin, int32_t h, int32_t w,
+                                        wino_layout layout, int32_t* absmax, int8_t* e_b, hipStream_t stream);
 
 /*
  * wino_f4_calibrate_output -- max-abs calibration of the output shift: runs

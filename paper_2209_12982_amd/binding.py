@@ -21,6 +21,8 @@ EXPORTS = [
     "wino_f4_plan", "wino_f4_plan_tables", "wino_f4_plan_destroy", "wino_f4_plan_info",
     "wino_f2_plan", "wino_f2_plan_tables", "wino_f2_calibrate_input",
     "wino_f4_plan_device", "wino_f2_plan_device", "wino_f4_plan_int8", "wino_f2_plan_int8",
+    "wino_f4_plan_i10", "wino_f2_plan_i10", "wino_f4_plan_tables_i10", "wino_f2_plan_tables_i10",
+    "wino_f4_calibrate_input_i10", "wino_f2_calibrate_input_i10",
     "wino_f4_plan_set_tap_kernel", "wino_f4_tap_kernel_choice", "wino_select_algorithm",
     "wino_f4_workspace_bytes",
     "wino_f4_conv_int8", "wino_f4_input_transform", "wino_f4_tap_gemm", "wino_f4_calibrate_input", "wino_f4_calibrate_output",
@@ -51,6 +53,15 @@ def load_library():
     if not os.path.exists(path):
         raise LibraryNotBuilt(f"{path} is missing; run __graft_entry__.build() or "
                               "python paper_2209_12982_amd/build.py")
+    # PyTorch ships its own HIP runtime and loads it under a name that does
+    # not match the runtime's soname.  Loaded first, it satisfies this
+    # library's dependency as well and the process has one HIP runtime;
+    # loaded after this library, it would start a second one next to the
+    # system runtime this library bound to, and the library's HIP calls fail.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     sig = {
@@ -59,6 +70,12 @@ def load_library():
         "wino_f2_plan": (I32, [P, P, I32, I32, P, P, P, I32, I32, P]),
         "wino_f2_plan_tables": (I32, [P, I32, I32, P, P, P, I32, P, P, P, P, P]),
         "wino_f2_calibrate_input": (I32, [P, I32, I32, I32, I32, I32, P, P, P]),
+        "wino_f4_plan_i10": (I32, [P, P, I32, I32, P, P, P, I32, I32, P]),
+        "wino_f2_plan_i10": (I32, [P, P, I32, I32, P, P, P, I32, I32, P]),
+        "wino_f4_plan_tables_i10": (I32, [P, I32, I32, P, P, P, I32, P, P, P, P, P]),
+        "wino_f2_plan_tables_i10": (I32, [P, I32, I32, P, P, P, I32, P, P, P, P, P]),
+        "wino_f4_calibrate_input_i10": (I32, [P, I32, I32, I32, I32, I32, P, P, P]),
+        "wino_f2_calibrate_input_i10": (I32, [P, I32, I32, I32, I32, I32, P, P, P]),
         "wino_f4_plan_device": (I32, [P, P, I32, I32, P, P, P, I32, I32, P]),
         "wino_f2_plan_device": (I32, [P, P, I32, I32, P, P, P, I32, I32, P]),
         "wino_f4_plan_int8": (I32, [P, P, I32, I32, I32, P, P, P, I32, I32, P]),
@@ -131,13 +148,15 @@ def _host(a, dtype, n=None):
 
 class WinoF4Plan:
     """Owns a wino_f4_plan_t (from wino_f4_plan, m = 4, or wino_f2_plan,
-    m = 2); destroyed with the object or by close()."""
+    m = 2; bits = 10 for the int8/10 plans); destroyed with the object or by
+    close()."""
 
-    def __init__(self, handle, cin, cout, m=4):
+    def __init__(self, handle, cin, cout, m=4, bits=8):
         self.handle = handle
         self.cin = cin
         self.cout = cout
         self.m = m
+        self.bits = bits
         self.ntap = (m + 2) * (m + 2)
 
     def close(self):
@@ -152,7 +171,7 @@ class WinoF4Plan:
             pass
 
 
-def _make_plan(fn, m, w_oihw, in_exp, w_exp, bias, out_shift, relu, stream):
+def _make_plan(fn, m, w_oihw, in_exp, w_exp, bias, out_shift, relu, stream, bits=8):
     ntap = (m + 2) * (m + 2)
     w = _host(w_oihw, np.float32)
     cout, cin = w.shape[:2]
@@ -165,7 +184,7 @@ def _make_plan(fn, m, w_oihw, in_exp, w_exp, bias, out_shift, relu, stream):
                                      None if b is None else b.ctypes.data, int(out_shift), int(bool(relu)),
                                      _stream(stream))
     _check(st, fn)
-    return WinoF4Plan(h, cin, cout, m)
+    return WinoF4Plan(h, cin, cout, m, bits)
 
 
 def wino_f4_plan(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0, relu=False, stream=None):
@@ -175,6 +194,15 @@ def wino_f4_plan(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0, relu=False,
 def wino_f2_plan(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0, relu=False, stream=None):
     """F(2x2, 3x3) plan: 16-entry in_exp / w_exp."""
     return _make_plan("wino_f2_plan", 2, w_oihw, in_exp, w_exp, bias, out_shift, relu, stream)
+
+
+def wino_f4_plan_i10(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0, relu=False, stream=None):
+    """int8/10 plan: 10-bit Winograd-domain integers (Vq, Uq in [-512, 511])."""
+    return _make_plan("wino_f4_plan_i10", 4, w_oihw, in_exp, w_exp, bias, out_shift, relu, stream, bits=10)
+
+
+def wino_f2_plan_i10(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0, relu=False, stream=None):
+    return _make_plan("wino_f2_plan_i10", 2, w_oihw, in_exp, w_exp, bias, out_shift, relu, stream, bits=10)
 
 
 def _device_weights(w, dtype):
@@ -225,7 +253,7 @@ def wino_f2_plan_int8(w_dev, w_scale_exp, in_exp, w_exp=None, bias=None, out_shi
                              stream)
 
 
-def _plan_tables(fn, m, w_oihw, in_exp, w_exp, bias, out_shift):
+def _plan_tables(fn, m, w_oihw, in_exp, w_exp, bias, out_shift, qbits=8):
     ntap = (m + 2) * (m + 2)
     w = _host(w_oihw, np.float32)
     cout, cin = w.shape[:2]
@@ -236,7 +264,7 @@ def _plan_tables(fn, m, w_oihw, in_exp, w_exp, bias, out_shift):
     sh = np.zeros(ntap, np.int8)
     eo = ctypes.c_int32()
     bits = ctypes.c_int32()
-    uq = np.zeros((ntap, cin, cout), np.int8)
+    uq = np.zeros((ntap, cin, cout), np.int16 if qbits == 10 else np.int8)
     st = getattr(load_library(), fn)(w.ctypes.data, cin, cout, eb.ctypes.data,
                                      None if eg_in is None else eg_in.ctypes.data,
                                      None if b is None else b.ctypes.data, int(out_shift),
@@ -256,6 +284,15 @@ def wino_f4_plan_tables(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0):
 def wino_f2_plan_tables(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0):
     """The same for F(2x2, 3x3): 16 taps."""
     return _plan_tables("wino_f2_plan_tables", 2, w_oihw, in_exp, w_exp, bias, out_shift)
+
+
+def wino_f4_plan_tables_i10(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0):
+    """Host-only int8/10 plan arithmetic; uq is int16 [36][cin][cout]."""
+    return _plan_tables("wino_f4_plan_tables_i10", 4, w_oihw, in_exp, w_exp, bias, out_shift, qbits=10)
+
+
+def wino_f2_plan_tables_i10(w_oihw, in_exp, w_exp=None, bias=None, out_shift=0):
+    return _plan_tables("wino_f2_plan_tables_i10", 2, w_oihw, in_exp, w_exp, bias, out_shift, qbits=10)
 
 
 def wino_f4_plan_info(plan, with_uq=False):
@@ -335,6 +372,14 @@ def wino_f4_calibrate_input(x, n, cin, h, w, layout=NCHW, stream=None):
 
 def wino_f2_calibrate_input(x, n, cin, h, w, layout=NCHW, stream=None):
     return _calibrate_input("wino_f2_calibrate_input", 2, x, n, cin, h, w, layout, stream)
+
+
+def wino_f4_calibrate_input_i10(x, n, cin, h, w, layout=NCHW, stream=None):
+    return _calibrate_input("wino_f4_calibrate_input_i10", 4, x, n, cin, h, w, layout, stream)
+
+
+def wino_f2_calibrate_input_i10(x, n, cin, h, w, layout=NCHW, stream=None):
+    return _calibrate_input("wino_f2_calibrate_input_i10", 2, x, n, cin, h, w, layout, stream)
 
 
 def wino_f4_calibrate_output(plan, x, n, h, w, layout=NCHW, workspace=None, stream=None):

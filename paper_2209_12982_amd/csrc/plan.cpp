@@ -70,12 +70,12 @@ void tap_terms(const Xform& X, const float* f9, int a, int b, double* terms) {
             terms[k++] = (double)(X.gint[a][i] * X.gint[b][j]) * (double)f9[i * 3 + j];
 }
 
-// Smallest integer e with |S| <= 128 d^2 2^e over a set of sums S = d^2 U,
-// decided exactly.  `approx` holds the double approximation of each sum;
-// `terms_of(k, t9)` regenerates the exact terms of sum k.
+// Smallest integer e with |S| <= 2^(bits-1) d^2 2^e over a set of sums
+// S = d^2 U, decided exactly.  `approx` holds the double approximation of each
+// sum; `terms_of(k, t9)` regenerates the exact terms of sum k.
 template <class TermsOf>
-int exact_cexp_of_max(const Xform& X, const std::vector<double>& approx, TermsOf terms_of) {
-    const double unit = 128.0 * X.den2;
+int exact_cexp_of_max(const Xform& X, const std::vector<double>& approx, TermsOf terms_of, int bits) {
+    const double unit = (double)(1 << (bits - 1)) * X.den2;
     double amax = 0.0;
     for (double v : approx) amax = std::max(amax, std::fabs(v));
     if (amax == 0.0) {
@@ -118,12 +118,14 @@ int exact_cexp_of_max(const Xform& X, const std::vector<double>& approx, TermsOf
     return e;
 }
 
-// clamp(R(S / (d^2 2^e)), -128, 127) for the exact sum S of `t9`.
-int8_t exact_quantize(const Xform& X, const double* t9, double approx, int e) {
+// clamp(R(S / (d^2 2^e)), -2^(bits-1), 2^(bits-1) - 1) for the exact sum S
+// of `t9`.
+int16_t exact_quantize(const Xform& X, const double* t9, double approx, int e, int bits) {
+    const double qmax = (double)((1 << (bits - 1)) - 1), qmin = -(double)(1 << (bits - 1));
     double scale = std::ldexp((double)X.den2, e);
     double u = approx / scale;
-    if (!(u < 200.0)) return 127;       // also catches +inf
-    if (!(u > -200.0)) return -128;
+    if (!(u < 2.0 * qmax)) return (int16_t)qmax;   // also catches +inf
+    if (!(u > 2.0 * qmin)) return (int16_t)qmin;
     double q = std::floor(u + 0.5);
     for (int guard = 0; guard < 4; ++guard) {
         // need (q - 1/2) * scale <= S < (q + 1/2) * scale
@@ -131,9 +133,9 @@ int8_t exact_quantize(const Xform& X, const double* t9, double approx, int e) {
         if (exact_sign_minus(t9, (q + 0.5) * scale) >= 0) { q += 1; continue; }
         break;
     }
-    if (q > 127) q = 127;
-    if (q < -128) q = -128;
-    return (int8_t)q;
+    if (q > qmax) q = qmax;
+    if (q < qmin) q = qmin;
+    return (int16_t)q;
 }
 
 }  // namespace
@@ -183,7 +185,8 @@ wino_status plan_finish(const Xform& X, wino_f4_plan_s* p, const int8_t* in_exp,
         p->sh[t] = (int8_t)s;
     }
     // Epilogue bound: max over (co, i, j) of
-    //   sum_t |A^T[i][a] A^T[j][b]| 2^sh[t] 128 sum_ci |Uq[t][ci][co]|
+    //   sum_t |A^T[i][a] A^T[j][b]| 2^sh[t] vmax sum_ci |Uq[t][ci][co]|
+    // with vmax = 2^(bits-1) the largest |Vq|
     // plus max|bias| plus the rounding constant.  Every partial sum of the
     // separable output transform is a sub-sum of such a term set, so this
     // bounds all of them.
@@ -204,7 +207,8 @@ wino_status plan_finish(const Xform& X, wino_f4_plan_s* p, const int8_t* in_exp,
                 unsigned __int128 tot = 0;
                 for (int t = 0; t < kTaps; ++t) {
                     int c = std::abs(X.at[i][t / n] * X.at[j][t % n]);
-                    tot += (unsigned __int128)c * (uint32_t)colsum[(size_t)t * cout + co] * 128u *
+                    tot += (unsigned __int128)c * (uint32_t)colsum[(size_t)t * cout + co] *
+                           (unsigned)(1 << (p->bits - 1)) *
                            ((unsigned __int128)1 << p->sh[t]);
                 }
                 worst = std::max(worst, tot);
@@ -236,7 +240,7 @@ wino_status plan_upload_bias(wino_f4_plan_s* p, hipStream_t stream) {
 // `p` (cin, cout, paddings, e_b, e_g, sh, e_o, epi_bits, uq_host, bias_host).
 static wino_status compute_tables(const Xform& X, wino_f4_plan_s* p, const float* w_oihw, int32_t cin,
                                   int32_t cout, const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
-                                  int32_t out_shift, int32_t relu) {
+                                  int32_t out_shift, int32_t relu, int bits) {
     const int kTaps = X.ntap, n = X.n;
     if (!w_oihw) return WINO_EINVAL;
     wino_status st = plan_check_args(X, cin, cout, in_exp, w_exp, out_shift, relu);
@@ -244,6 +248,7 @@ static wino_status compute_tables(const Xform& X, wino_f4_plan_s* p, const float
     for (int64_t i = 0; i < (int64_t)cout * cin * 9; ++i)
         if (!std::isfinite(w_oihw[i])) return WINO_EINVAL;
     plan_set_shape(X, p, cin, cout, out_shift, relu);
+    p->bits = bits;
 
     const int64_t nblk = (int64_t)cout * cin;
     // double approximations of d^2 U for every (block, tap)
@@ -277,7 +282,7 @@ static wino_status compute_tables(const Xform& X, wino_f4_plan_s* p, const float
         for (int64_t k = 0; k < nblk; ++k) col[k] = approx[k * kTaps + t];
         int e = exact_cexp_of_max(X, col, [&](size_t kk, double* tt) {
             tap_terms(X, w_oihw + kk * 9, t / n, t % n, tt);
-        });
+        }, bits);
         if (e < -126 || e > 126) return WINO_ERANGE;
         p->e_g[t] = (int8_t)e;
     }
@@ -286,7 +291,7 @@ static wino_status compute_tables(const Xform& X, wino_f4_plan_s* p, const float
         int co = (int)(k / cin), ci = (int)(k % cin);
         for (int t = 0; t < kTaps; ++t) {
             tap_terms(X, w_oihw + k * 9, t / n, t % n, t9);
-            int8_t q = exact_quantize(X, t9, approx[k * kTaps + t], p->e_g[t]);
+            int16_t q = exact_quantize(X, t9, approx[k * kTaps + t], p->e_g[t], bits);
             p->uq_host[((size_t)t * cin + ci) * cout + co] = q;
             colsum[(size_t)t * cout + co] += std::abs((int)q);
         }
@@ -296,13 +301,19 @@ static wino_status compute_tables(const Xform& X, wino_f4_plan_s* p, const float
 
 static wino_status plan_tables(const Xform& X, const float* w_oihw, int32_t cin, int32_t cout,
                                const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias, int32_t out_shift,
-                               int8_t* e_g, int8_t* sh, int32_t* e_o, int32_t* epilogue_bits, int8_t* uq) {
+                               int8_t* e_g, int8_t* sh, int32_t* e_o, int32_t* epilogue_bits, void* uq, int bits) {
     wino_f4_plan_s* p = new (std::nothrow) wino_f4_plan_s();
     if (!p) return WINO_ENOMEM;
     p->uq_dev = nullptr;
     p->bias_dev = nullptr;
-    wino_status st = compute_tables(X, p, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, 0);
-    if (st == WINO_OK) st = wino_f4_plan_info(p, e_g, sh, e_o, epilogue_bits, uq, nullptr, nullptr);
+    wino_status st = compute_tables(X, p, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, 0, bits);
+    if (st == WINO_OK) st = wino_f4_plan_info(p, e_g, sh, e_o, epilogue_bits, nullptr, nullptr, nullptr);
+    if (st == WINO_OK && uq) {
+        for (size_t i = 0; i < p->uq_host.size(); ++i) {
+            if (bits == 10) ((int16_t*)uq)[i] = p->uq_host[i];
+            else ((int8_t*)uq)[i] = (int8_t)p->uq_host[i];
+        }
+    }
     delete p;
     return st;
 }
@@ -317,26 +328,37 @@ static wino_f4_plan_s* new_plan() {
 
 static wino_status make_plan(const Xform& X, wino_f4_plan_t* out, const float* w_oihw, int32_t cin, int32_t cout,
                              const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias, int32_t out_shift,
-                             int32_t relu, hipStream_t stream) {
+                             int32_t relu, hipStream_t stream, int bits = 8) {
     if (!out) return WINO_EINVAL;
     *out = nullptr;
     wino_f4_plan_s* p = new_plan();
     if (!p) return WINO_ENOMEM;
-    wino_status st = compute_tables(X, p, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, relu);
+    wino_status st = compute_tables(X, p, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, relu, bits);
     if (st != WINO_OK) {
         delete p;
         return st;
     }
-    // device upload: Uq k-blocked as [ntap][cin_pad/64][cout_pad][64] (GEMM A
-    // operand: rows = output channels, 64 input channels contiguous per row,
-    // so one k step of one tap is a single contiguous block), bias [cout_pad]
-    std::vector<int8_t> dev_layout((size_t)X.ntap * p->cout_pad * p->cin_pad, 0);
-    const int nkb = p->cin_pad / kKStep;
+    // device upload: Uq k-blocked (GEMM A operand: rows = output channels,
+    // one 64-byte k row per row, so one k step of one tap is a single
+    // contiguous block), bias [cout_pad]:
+    //   bits 8:  int8 [ntap][cin_pad/64][cout_pad][64]
+    //   bits 10: fp16 [ntap][cin_pad/32][cout_pad][32] (the 10-bit integers
+    //            are exact in fp16; the tap GEMM runs on fp16 matrix cores)
+    const int kpr = bits == 10 ? kKStep / 2 : kKStep;        // channels per 64-byte k row
+    const int nkb = p->cin_pad / kpr;
+    std::vector<int8_t> dev_layout((size_t)X.ntap * p->cout_pad * p->cin_pad * kbytes_per_channel(bits), 0);
     for (int t = 0; t < X.ntap; ++t)
         for (int ci = 0; ci < cin; ++ci)
-            for (int co = 0; co < cout; ++co)
-                dev_layout[(((size_t)t * nkb + ci / kKStep) * p->cout_pad + co) * kKStep + ci % kKStep] =
-                    p->uq_host[((size_t)t * cin + ci) * cout + co];
+            for (int co = 0; co < cout; ++co) {
+                const size_t idx = (((size_t)t * nkb + ci / kpr) * p->cout_pad + co) * kpr + ci % kpr;
+                const int16_t v = p->uq_host[((size_t)t * cin + ci) * cout + co];
+                if (bits == 10) {
+                    const _Float16 h = (_Float16)v;
+                    std::memcpy(dev_layout.data() + 2 * idx, &h, 2);
+                } else {
+                    dev_layout[idx] = (int8_t)v;
+                }
+            }
     if (hipGetDevice(&p->device) != hipSuccess) { delete p; return WINO_EHIP; }
     if (hipMalloc(&p->uq_dev, dev_layout.size()) != hipSuccess) { delete p; return WINO_ENOMEM; }
     if (hipMemcpyAsync(p->uq_dev, dev_layout.data(), dev_layout.size(), hipMemcpyHostToDevice, stream) !=
@@ -386,14 +408,40 @@ extern "C" wino_status wino_f4_plan_tables(const float* w_oihw, int32_t cin, int
                                            const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
                                            int32_t out_shift, int8_t* e_g, int8_t* sh, int32_t* e_o,
                                            int32_t* epilogue_bits, int8_t* uq) {
-    return plan_tables(kF4, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, e_g, sh, e_o, epilogue_bits, uq);
+    return plan_tables(kF4, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, e_g, sh, e_o, epilogue_bits, uq, 8);
 }
 
 extern "C" wino_status wino_f2_plan_tables(const float* w_oihw, int32_t cin, int32_t cout,
                                            const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
                                            int32_t out_shift, int8_t* e_g, int8_t* sh, int32_t* e_o,
                                            int32_t* epilogue_bits, int8_t* uq) {
-    return plan_tables(kF2, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, e_g, sh, e_o, epilogue_bits, uq);
+    return plan_tables(kF2, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, e_g, sh, e_o, epilogue_bits, uq, 8);
+}
+
+extern "C" wino_status wino_f4_plan_tables_i10(const float* w_oihw, int32_t cin, int32_t cout,
+                                               const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                                               int32_t out_shift, int8_t* e_g, int8_t* sh, int32_t* e_o,
+                                               int32_t* epilogue_bits, int16_t* uq) {
+    return plan_tables(kF4, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, e_g, sh, e_o, epilogue_bits, uq, 10);
+}
+
+extern "C" wino_status wino_f2_plan_tables_i10(const float* w_oihw, int32_t cin, int32_t cout,
+                                               const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                                               int32_t out_shift, int8_t* e_g, int8_t* sh, int32_t* e_o,
+                                               int32_t* epilogue_bits, int16_t* uq) {
+    return plan_tables(kF2, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, e_g, sh, e_o, epilogue_bits, uq, 10);
+}
+
+extern "C" wino_status wino_f4_plan_i10(wino_f4_plan_t* out, const float* w_oihw, int32_t cin, int32_t cout,
+                                        const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                                        int32_t out_shift, int32_t relu, hipStream_t stream) {
+    return make_plan(kF4, out, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, relu, stream, 10);
+}
+
+extern "C" wino_status wino_f2_plan_i10(wino_f4_plan_t* out, const float* w_oihw, int32_t cin, int32_t cout,
+                                        const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,
+                                        int32_t out_shift, int32_t relu, hipStream_t stream) {
+    return make_plan(kF2, out, w_oihw, cin, cout, in_exp, w_exp, bias, out_shift, relu, stream, 10);
 }
 
 extern "C" wino_status wino_f4_plan(wino_f4_plan_t* out, const float* w_oihw, int32_t cin,
@@ -463,13 +511,14 @@ extern "C" wino_status wino_f4_plan_info(wino_f4_plan_t p, int8_t* e_g, int8_t* 
                                          int32_t* epilogue_bits, int8_t* uq, int32_t* cin,
                                          int32_t* cout) {
     if (!p) return WINO_EINVAL;
+    if (uq && p->bits != 8) return WINO_EINVAL;         // 10-bit tables: wino_f4_plan_tables_i10
     if (e_g) std::memcpy(e_g, p->e_g, p->ntap);
     if (sh) std::memcpy(sh, p->sh, p->ntap);
     if (e_o) *e_o = p->e_o;
     if (epilogue_bits) *epilogue_bits = p->epi_bits;
     if (uq) {
         if (!p->uq_host.empty()) {
-            std::memcpy(uq, p->uq_host.data(), p->uq_host.size());
+            for (size_t i = 0; i < p->uq_host.size(); ++i) uq[i] = (int8_t)p->uq_host[i];
         } else {
             // device-built plan: read the k-blocked device copy back
             const int nkb = p->cin_pad / kKStep;

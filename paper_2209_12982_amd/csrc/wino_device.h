@@ -10,6 +10,10 @@ namespace winof4 {
 
 typedef short v2s __attribute__((ext_vector_type(2)));
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef _Float16 v2h __attribute__((ext_vector_type(2)));
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ v2s splat(int v) { return (v2s){(short)v, (short)v}; }
 
@@ -52,6 +56,22 @@ __device__ __forceinline__ uint32_t requant_pack(v2s ev, v2s od, int e) {
     b = __builtin_elementwise_min(__builtin_elementwise_max(b, splat(-128)), splat(127));
     // bytes: ch0 = a.lo, ch1 = b.lo, ch2 = a.hi, ch3 = b.hi
     return __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, b), __builtin_bit_cast(uint32_t, a), 0x06020400u);
+}
+
+// The int8/10 variant: requantize four channels to 10 bits ([-512, 511])
+// and store them as fp16, which holds every such integer exactly.
+// Halves: ch0 = a.x, ch1 = b.x, ch2 = a.y, ch3 = b.y (the channel order of
+// requant_pack).
+__device__ __forceinline__ uint2 requant10_pack(v2s ev, v2s od, int e) {
+    const v2s rnd = splat(e ? (1 << (e - 1)) : 0);
+    const v2s sh = splat(e);
+    v2s a = (ev + rnd) >> sh;
+    v2s b = (od + rnd) >> sh;
+    a = __builtin_elementwise_min(__builtin_elementwise_max(a, splat(-512)), splat(511));
+    b = __builtin_elementwise_min(__builtin_elementwise_max(b, splat(-512)), splat(511));
+    const v2h lo = {(_Float16)a.x, (_Float16)b.x};
+    const v2h hi = {(_Float16)a.y, (_Float16)b.y};
+    return make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
 }
 
 // median of three (clamp a to [lo, hi]) in one instruction

@@ -95,7 +95,9 @@ __device__ __forceinline__ void k1_stage_band(uint32_t* lds, const int8_t* __res
 }
 
 // MODE 0: write Vq.  MODE 1: per-tap max |V| into tapmax[NTAP] (calibration).
-template <int M, int LAYOUT, int MODE>
+// Q: Winograd-domain width, 8 (int8 Vq) or 10 (int8/10: fp16 Vq holding
+// 10-bit integers, [ntap][cin_pad/32][t_pad][32]).
+template <int M, int LAYOUT, int MODE, int Q = 8>
 __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __restrict__ x,
                                                                int8_t* __restrict__ vq,
                                                                int* __restrict__ tapmax, K1Args g) {
@@ -136,11 +138,22 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
     if (MODE == 0) {
         if (!valid) return;
         const long long tile = (long long)row * g.tw + tx;
-        // Vq[t][cgi][tile][64]: this block's 64 channels are k block cgi
-        uint32_t* dst = (uint32_t*)(vq + ((long long)cgi * g.t_pad + tile) * K1_CG) + q;
-        const long long plane = g.t_pad * g.cin_pad / 4;   // words per tap plane
+        if constexpr (Q == 10) {
+            // Vq[t][2 cgi + q / 8][tile][32] fp16: this block's 64 channels are
+            // the 32-channel k rows 2 cgi and 2 cgi + 1; 4 halves per thread
+            uint2* dst = (uint2*)((uint16_t*)vq + ((long long)(2 * cgi + (q >> 3)) * g.t_pad + tile) * 32) + (q & 7);
+            const long long plane = g.t_pad * g.cin_pad / 4;   // 4-half groups per tap plane
 #pragma unroll
-        for (int t = 0; t < NT; ++t) dst[t * plane] = requant_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t]);
+            for (int t = 0; t < NT; ++t)
+                dst[t * plane] = requant10_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t]);
+        } else {
+            // Vq[t][cgi][tile][64]: this block's 64 channels are k block cgi
+            uint32_t* dst = (uint32_t*)(vq + ((long long)cgi * g.t_pad + tile) * K1_CG) + q;
+            const long long plane = g.t_pad * g.cin_pad / 4;   // words per tap plane
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+                dst[t * plane] = requant_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t]);
+        }
     } else {
         if (valid) {
 #pragma unroll
@@ -177,7 +190,7 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
 // Three block shapes: 64x32 (8 waves, double buffer), the default; 32x32
 // (4 waves) and 16x16 (one wave) with 6-tap stages and rings small enough for
 // two and four workgroups per CU, selectable for small layers.
-template <int CW_, int TW_, int G_, int NBUF_>
+template <int CW_, int TW_, int G_, int NBUF_, int PF_ = G_ / 2>
 struct K2Cfg {
     static constexpr int CW = CW_, TW = TW_, G = G_, NBUF = NBUF_;   // G: taps per stage
     static constexpr int CO = 16 * CW, TL = 16 * TW;
@@ -186,7 +199,7 @@ struct K2Cfg {
     static constexpr int STAGE = A_BYTES + B_BYTES;
     static constexpr int KB = STAGE / 1024;              // 1-KB load instructions per stage
     static constexpr int LPW = (KB + WAVES - 1) / WAVES; // load instructions per wave per stage
-    static constexpr int PF = G / 2;                     // taps whose LDS fragments are in flight ahead
+    static constexpr int PF = PF_;                       // taps whose LDS fragments are in flight ahead
     static_assert(NBUF * STAGE <= 160 * 1024, "LDS");
     static_assert((NBUF - 2) * LPW <= 63, "vmcnt range");
     static_assert(G > PF, "stage shape");
@@ -198,6 +211,14 @@ using K2Mid = K2Cfg<2, 2, 6, 3>;
 using K2Small = K2Cfg<1, 1, 6, 3>;
 // F(2x2,3x3): 16 taps in two 8-tap stages per k step, 64 x 32 blocks
 using K2F2 = K2Cfg<4, 2, 8, 3>;
+// int8/10 (fp16 operands): shallower fragment prefetch, as each fp16 MFMA
+// result also needs registers until it is
+// folded into the int32 accumulator (64x32 keeps a one-tap prefetch; with
+// the 64-bit epilogue only the 32x32 shape stays clear of spills)
+using K2Big10 = K2Cfg<4, 2, 12, 2, 1>;
+using K2Mid10 = K2Cfg<2, 2, 12, 2, 2>;
+using K2Small10 = K2Cfg<2, 2, 6, 2, 2>;   // 48 KB of LDS: two workgroups per CU
+using K2F2_10 = K2Cfg<4, 2, 8, 3, 2>;
 
 struct K2Args {
     int cin_pad, cout, cout_pad;
@@ -211,7 +232,13 @@ struct K2Args {
 
 // MODE 0: store y.  MODE 1: max |Y + bias| into *zmax (calibration).
 // MODE 2: store raw M (debug export).
-template <class C, int M, int LAYOUT, int EPI, int MODE>
+// Q = 8: int8 operands, 16x16x64 int8 MFMA.  Q = 10 (int8/10): fp16 operands
+// holding 10-bit integers, 32 channels per 64-byte k row (g.cin_pad counts
+// k-row bytes, i.e. twice the channels), 16x16x32 fp16 MFMA.  Each fp16 MFMA
+// starts from zero: its 32 products and their partial sums are integers of
+// magnitude <= 32 * 2^18 = 2^23, so the fp32 result is exact, and it is
+// converted and added to the int32 accumulator right away.
+template <class C, int M, int LAYOUT, int EPI, int MODE, int Q = 8>
 __global__ __launch_bounds__(C::THREADS) void wino_tap_gemm(const int8_t* __restrict__ uq,
                                                             const int8_t* __restrict__ vq,
                                                             const int32_t* __restrict__ bias,
@@ -324,8 +351,20 @@ __global__ __launch_bounds__(C::THREADS) void wino_tap_gemm(const int8_t* __rest
 #pragma unroll
             for (int u = 0; u < C::G; ++u) {
                 const int slot = u % C::PF;
-                acc[C::G * grp + u] =
-                    __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[slot], fb[slot], acc[C::G * grp + u], 0, 0, 0);
+                if constexpr (Q == 10) {
+                    const v4f r = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                        __builtin_bit_cast(v8h, fa[slot]), __builtin_bit_cast(v8h, fb[slot]), (v4f){0.f, 0.f, 0.f, 0.f},
+                        0, 0, 0);
+                    // unsigned (wrapping) add: with a signed add the compiler
+                    // may carry the accumulators in 64 bits for the int64
+                    // epilogue (overflow being undefined), doubling them
+                    acc[C::G * grp + u] = __builtin_bit_cast(
+                        v4i, __builtin_bit_cast(v4u, acc[C::G * grp + u]) +
+                                 __builtin_bit_cast(v4u, __builtin_convertvector(r, v4i)));
+                } else {
+                    acc[C::G * grp + u] =
+                        __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[slot], fb[slot], acc[C::G * grp + u], 0, 0, 0);
+                }
                 if (u + C::PF < C::G) {
                     fa[slot] = *(const v4i*)(base + frag_a + (u + C::PF) * C::CO * 64);
                     fb[slot] = *(const v4i*)(base + frag_b + (u + C::PF) * C::TL * 64);
@@ -333,14 +372,21 @@ __global__ __launch_bounds__(C::THREADS) void wino_tap_gemm(const int8_t* __rest
             }
             // keep that order: the scheduler would otherwise pull the reads
             // next to their MFMAs to save registers (masks: 0x100 LDS read,
-            // 0x008 MFMA)
+            // 0x008 MFMA, 0x002 VALU).  With fp16 operands each MFMA is
+            // followed by the eight VALU ops that fold an earlier result into
+            // the int32 accumulators, so at most a few results are live.
             __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::PF, 0);
 #pragma unroll
             for (int u = 0; u < C::G - C::PF; ++u) {
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
                 __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+                if constexpr (Q == 10) __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
             }
-            __builtin_amdgcn_sched_group_barrier(0x008, C::PF, 0);
+#pragma unroll
+            for (int u = 0; u < C::PF; ++u) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                if constexpr (Q == 10) __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+            }
         }
     }
 
@@ -688,7 +734,7 @@ wino_status geometry(int32_t n, int32_t h, int32_t w, int m, Geometry& g) {
 }
 
 size_t vq_bytes(const wino_f4_plan_s* p, const Geometry& g) {
-    return (size_t)p->ntap * (size_t)g.t_pad * (size_t)p->cin_pad;
+    return (size_t)p->ntap * (size_t)g.t_pad * (size_t)p->cin_pad * kbytes_per_channel(p->bits);
 }
 
 TapTables tables_of(const wino_f4_plan_s* p) {
@@ -717,7 +763,7 @@ K1Args k1_args(const Geometry& g, int cin, int cin_pad, const TapTables& tab) {
     return a;
 }
 
-template <int M, int MODE>
+template <int M, int MODE, int Q = 8>
 wino_status launch_k1(const K1Args& a, wino_layout layout, const int8_t* x, int8_t* vq, int* tapmax,
                       hipStream_t stream) {
     long long blocks = (long long)a.ntxb * a.ncg * a.n * a.th;
@@ -726,10 +772,10 @@ wino_status launch_k1(const K1Args& a, wino_layout layout, const int8_t* x, int8
     K1Args args = a;
     args.x_vec = (a.cin % 16 == 0) && (((uintptr_t)x & 15) == 0);
     if (layout == WINO_NHWC)
-        hipLaunchKernelGGL((wino_input_xform<M, WINO_NHWC, MODE>), dim3((unsigned)blocks), dim3(K1_THREADS), 0,
+        hipLaunchKernelGGL((wino_input_xform<M, WINO_NHWC, MODE, Q>), dim3((unsigned)blocks), dim3(K1_THREADS), 0,
                            stream, x, vq, tapmax, args);
     else
-        hipLaunchKernelGGL((wino_input_xform<M, WINO_NCHW, MODE>), dim3((unsigned)blocks), dim3(K1_THREADS), 0,
+        hipLaunchKernelGGL((wino_input_xform<M, WINO_NCHW, MODE, Q>), dim3((unsigned)blocks), dim3(K1_THREADS), 0,
                            stream, x, vq, tapmax, args);
     return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
 }
@@ -749,7 +795,17 @@ long long resident_blocks(const wino_f4_plan_s* p, const Geometry& g) {
 // Calibration and debug exports (MODE 1, 2) always use the 64x32 shape.
 int tap_kernel_for(const wino_f4_plan_s* p, const Geometry& g, int mode) {
     const int k = p->tap_kernel;
-    if (mode != 0 || p->m != 4) return WINO_TAP_RESIDENT_64X32;   // F2: its own 64x32 configuration
+    // int8/10 (fp16 operands): a forced resident shape (16X16 stands for the
+    // 32x32 shape with 6-tap stages), else 64x32, or 32x32 with the 64-bit
+    // epilogue
+    if (p->bits == 10 && p->m == 4) {
+        if (mode == 0 && (k == WINO_TAP_RESIDENT_64X32 || k == WINO_TAP_RESIDENT_32X32 ||
+                          k == WINO_TAP_RESIDENT_16X16))
+            return k;
+        return p->epi_bits == 64 ? WINO_TAP_RESIDENT_32X32 : WINO_TAP_RESIDENT_64X32;
+    }
+    // F2: its own 64x32 configuration
+    if (mode != 0 || p->m != 4 || p->bits != 8) return WINO_TAP_RESIDENT_64X32;
     if (k == WINO_TAP_RESIDENT_64X32 || k == WINO_TAP_RESIDENT_32X32 || k == WINO_TAP_RESIDENT_16X16) return k;
     if (p->epi_bits == 32 && k != WINO_TAP_RESIDENT &&
         (k == WINO_TAP_ROWS || (long long)(p->cout_pad / KR_CO) * (g.t_pad / KR_TL) >= num_cus()))
@@ -757,7 +813,7 @@ int tap_kernel_for(const wino_f4_plan_s* p, const Geometry& g, int mode) {
     return WINO_TAP_RESIDENT_64X32;
 }
 
-template <class C, int M, int MODE>
+template <class C, int M, int MODE, int Q = 8>
 wino_status launch_resident(const wino_f4_plan_s* p, const Geometry& g, wino_layout layout, const int8_t* vq,
                             int8_t* y, void* aux, K2Args a, hipStream_t stream) {
     const long long blocks = resident_blocks<C>(p, g);
@@ -765,9 +821,10 @@ wino_status launch_resident(const wino_f4_plan_s* p, const Geometry& g, wino_lay
     if (blocks > 0x7fffffffll) return WINO_EUNSUPPORTED;
     a.nbco = p->cout_pad / C::CO;
     a.nblocks = (int)blocks;
+    a.cin_pad = p->cin_pad * kbytes_per_channel(Q);      // bytes of one operand row
     dim3 grid((unsigned)blocks), block(C::THREADS);
 #define K2_LAUNCH(L, E)                                                                              \
-    hipLaunchKernelGGL((wino_tap_gemm<C, M, L, E, MODE>), grid, block, 0, stream, p->uq_dev, vq, p->bias_dev, \
+    hipLaunchKernelGGL((wino_tap_gemm<C, M, L, E, MODE, Q>), grid, block, 0, stream, p->uq_dev, vq, p->bias_dev, \
                        y, aux, a)
     if (layout == WINO_NHWC) {
         if (p->epi_bits == 32) K2_LAUNCH(WINO_NHWC, 32); else K2_LAUNCH(WINO_NHWC, 64);
@@ -797,6 +854,20 @@ wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout la
     a.relu = p->relu;
     a.y_staged = layout == WINO_NHWC && p->cout % KR_CO == 0 && ((uintptr_t)y & 15) == 0;
     a.tab = tables_of(p);
+    if (p->bits == 10) {
+        if (p->m == 2) return launch_resident<K2F2_10, 2, MODE, 10>(p, g, layout, vq, y, aux, a, stream);
+        switch (tap_kernel_for(p, g, MODE)) {
+            case WINO_TAP_RESIDENT_64X32:
+                return launch_resident<K2Big10, 4, MODE, 10>(p, g, layout, vq, y, aux, a, stream);
+            case WINO_TAP_RESIDENT_16X16:
+                if constexpr (MODE == 0)
+                    return launch_resident<K2Small10, 4, MODE, 10>(p, g, layout, vq, y, aux, a, stream);
+                break;
+            default:
+                break;
+        }
+        return launch_resident<K2Mid10, 4, MODE, 10>(p, g, layout, vq, y, aux, a, stream);
+    }
     if (p->m == 2) return launch_resident<K2F2, 2, MODE>(p, g, layout, vq, y, aux, a, stream);
     switch (tap_kernel_for(p, g, MODE)) {
         case WINO_TAP_ROWS: {
@@ -831,18 +902,23 @@ wino_status check_common(const wino_f4_plan_s* p, const void* x, int32_t n, int3
     return geometry(n, h, w, p->m, g);
 }
 
-// K1 for the plan's transform
+// K1 for the plan's transform and Winograd-domain width
 template <int MODE>
-wino_status run_k1(int m, const K1Args& a, wino_layout layout, const int8_t* x, int8_t* vq, int* tapmax,
-                   hipStream_t stream) {
+wino_status run_k1(int m, int bits, const K1Args& a, wino_layout layout, const int8_t* x, int8_t* vq,
+                   int* tapmax, hipStream_t stream) {
+    if constexpr (MODE == 0) {
+        if (bits == 10)
+            return m == 2 ? launch_k1<2, MODE, 10>(a, layout, x, vq, tapmax, stream)
+                          : launch_k1<4, MODE, 10>(a, layout, x, vq, tapmax, stream);
+    }
     return m == 2 ? launch_k1<2, MODE>(a, layout, x, vq, tapmax, stream)
                   : launch_k1<4, MODE>(a, layout, x, vq, tapmax, stream);
 }
 
-int cexp_int(unsigned long long a) {
-    // smallest e >= 0 with a <= 128 * 2^e (callers clamp at 0 anyway)
+int cexp_int(unsigned long long a, int bits = 8) {
+    // smallest e >= 0 with a <= 2^(bits-1) * 2^e (callers clamp at 0 anyway)
     int e = 0;
-    while ((unsigned long long)128 << e < a && e < 62) ++e;
+    while (((unsigned __int128)1 << (bits - 1 + e)) < a) ++e;
     return e;
 }
 
@@ -894,12 +970,12 @@ extern "C" wino_status wino_f4_conv_int8(wino_f4_plan_t p, const int8_t* x, int8
     if (variant != WINO_SPLIT && variant != WINO_FUSED) return WINO_EINVAL;
     if (g.ntiles == 0) return WINO_OK;
     if (variant == WINO_FUSED) {
-        if (p->m != 4) return WINO_EUNSUPPORTED;
+        if (p->m != 4 || p->bits != 8) return WINO_EUNSUPPORTED;
         return wino_f4_conv_fused(p, x, y, n, h, w, layout, stream);
     }
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
     int8_t* vq = (int8_t*)ws;
-    st = run_k1<0>(p->m, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, vq, nullptr, stream);
+    st = run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, vq, nullptr, stream);
     if (st != WINO_OK) return st;
     return launch_k2<0>(p, g, layout, vq, y, nullptr, stream);
 }
@@ -912,7 +988,7 @@ extern "C" wino_status wino_f4_input_transform(wino_f4_plan_t p, const int8_t* x
     if (st != WINO_OK) return st;
     if (g.ntiles == 0) return WINO_OK;
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
-    return run_k1<0>(p->m, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
+    return run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
 }
 
 extern "C" wino_status wino_f4_tap_gemm(wino_f4_plan_t p, const void* ws, size_t ws_bytes, int8_t* y, int32_t n,
@@ -926,9 +1002,11 @@ extern "C" wino_status wino_f4_tap_gemm(wino_f4_plan_t p, const void* ws, size_t
     return launch_k2<0>(p, g, layout, (const int8_t*)ws, y, nullptr, stream);
 }
 
-// per-tap max |V| over the input and the exponents e_B = max(0, cexp(.))
-static wino_status calibrate_input(int m, const int8_t* x, int32_t n, int32_t cin, int32_t h, int32_t w,
-                                   wino_layout layout, int32_t* absmax, int8_t* e_b, hipStream_t stream) {
+// per-tap max |V| over the input and the exponents e_B = max(0, cexp(.)) for
+// bits-wide input taps
+static wino_status calibrate_input(int m, int bits, const int8_t* x, int32_t n, int32_t cin, int32_t h,
+                                   int32_t w, wino_layout layout, int32_t* absmax, int8_t* e_b,
+                                   hipStream_t stream) {
     if (!x || cin < 1) return WINO_EINVAL;
     if (cin > 65536) return WINO_EUNSUPPORTED;
     if (layout != WINO_NCHW && layout != WINO_NHWC) return WINO_EINVAL;
@@ -942,7 +1020,7 @@ static wino_status calibrate_input(int m, const int8_t* x, int32_t n, int32_t ci
         if (hipMalloc(&dmax, sizeof(int) * kTaps) != hipSuccess) return WINO_ENOMEM;
         TapTables tab = {};
         bool ok = hipMemsetAsync(dmax, 0, sizeof(int) * kTaps, stream) == hipSuccess;
-        if (ok) ok = run_k1<1>(m, k1_args(g, cin, (int)round_up(cin, kKStep), tab), layout, x, nullptr, dmax,
+        if (ok) ok = run_k1<1>(m, 8, k1_args(g, cin, (int)round_up(cin, kKStep), tab), layout, x, nullptr, dmax,
                                stream) == WINO_OK;
         if (ok) ok = hipMemcpyAsync(host, dmax, sizeof(int) * kTaps, hipMemcpyDeviceToHost, stream) == hipSuccess;
         if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
@@ -952,7 +1030,7 @@ static wino_status calibrate_input(int m, const int8_t* x, int32_t n, int32_t ci
     for (int t = 0; t < ntap; ++t) {
         if (absmax) absmax[t] = host[t];
         if (e_b) {
-            int e = cexp_int((unsigned long long)host[t]);
+            int e = cexp_int((unsigned long long)host[t], bits);
             e_b[t] = (int8_t)(e > 15 ? 15 : e);
         }
     }
@@ -962,13 +1040,25 @@ static wino_status calibrate_input(int m, const int8_t* x, int32_t n, int32_t ci
 extern "C" wino_status wino_f4_calibrate_input(const int8_t* x, int32_t n, int32_t cin, int32_t h, int32_t w,
                                                wino_layout layout, int32_t* absmax, int8_t* e_b,
                                                hipStream_t stream) {
-    return calibrate_input(4, x, n, cin, h, w, layout, absmax, e_b, stream);
+    return calibrate_input(4, 8, x, n, cin, h, w, layout, absmax, e_b, stream);
+}
+
+extern "C" wino_status wino_f4_calibrate_input_i10(const int8_t* x, int32_t n, int32_t cin, int32_t h, int32_t w,
+                                                   wino_layout layout, int32_t* absmax, int8_t* e_b,
+                                                   hipStream_t stream) {
+    return calibrate_input(4, 10, x, n, cin, h, w, layout, absmax, e_b, stream);
+}
+
+extern "C" wino_status wino_f2_calibrate_input_i10(const int8_t* x, int32_t n, int32_t cin, int32_t h, int32_t w,
+                                                   wino_layout layout, int32_t* absmax, int8_t* e_b,
+                                                   hipStream_t stream) {
+    return calibrate_input(2, 10, x, n, cin, h, w, layout, absmax, e_b, stream);
 }
 
 extern "C" wino_status wino_f2_calibrate_input(const int8_t* x, int32_t n, int32_t cin, int32_t h, int32_t w,
                                                wino_layout layout, int32_t* absmax, int8_t* e_b,
                                                hipStream_t stream) {
-    return calibrate_input(2, x, n, cin, h, w, layout, absmax, e_b, stream);
+    return calibrate_input(2, 8, x, n, cin, h, w, layout, absmax, e_b, stream);
 }
 
 extern "C" wino_status wino_f4_calibrate_output(wino_f4_plan_t p, const int8_t* x, int32_t n, int32_t h,
@@ -983,7 +1073,7 @@ extern "C" wino_status wino_f4_calibrate_output(wino_f4_plan_t p, const int8_t* 
         unsigned long long* dmax = nullptr;
         if (hipMalloc(&dmax, sizeof(unsigned long long)) != hipSuccess) return WINO_ENOMEM;
         bool ok = hipMemsetAsync(dmax, 0, sizeof(unsigned long long), stream) == hipSuccess;
-        if (ok) ok = run_k1<0>(p->m, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws,
+        if (ok) ok = run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws,
                                nullptr, stream) == WINO_OK;
         if (ok) ok = launch_k2<1>(p, g, layout, (const int8_t*)ws, nullptr, dmax, stream) == WINO_OK;
         if (ok) ok = hipMemcpyAsync(&host, dmax, sizeof(host), hipMemcpyDeviceToHost, stream) == hipSuccess;
@@ -1005,18 +1095,20 @@ extern "C" wino_status wino_f4_debug_input_transform(wino_f4_plan_t p, const int
     if (!vq_out) return WINO_EINVAL;
     if (g.ntiles == 0) return WINO_OK;
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
-    st = run_k1<0>(p->m, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
+    st = run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
     if (st != WINO_OK) return st;
-    // compact [ntap][cin_pad/64][t_pad][64] -> [ntap][ntiles][cin], one 2-D
-    // copy per (tap, k block)
-    const int nkb = p->cin_pad / kKStep;
+    // compact [ntap][cin_pad/kpr][t_pad][kpr] -> [ntap][ntiles][cin] (elements
+    // of es bytes: int8, or fp16 for 10-bit plans), one 2-D copy per (tap, k row)
+    const size_t es = kbytes_per_channel(p->bits);
+    const int kpr = kKStep / (int)es;                      // channels per 64-byte k row
+    const int nkb = p->cin_pad / kpr;
     for (int t = 0; t < p->ntap; ++t)
         for (int b = 0; b < nkb; ++b) {
-            const int width = std::min(kKStep, p->cin - b * kKStep);
+            const int width = std::min(kpr, p->cin - b * kpr);
             if (width <= 0) break;
-            if (hipMemcpy2DAsync(vq_out + (size_t)t * g.ntiles * p->cin + (size_t)b * kKStep, (size_t)p->cin,
+            if (hipMemcpy2DAsync(vq_out + es * ((size_t)t * g.ntiles * p->cin + (size_t)b * kpr), es * p->cin,
                                  (const int8_t*)ws + ((size_t)t * nkb + b) * g.t_pad * kKStep, (size_t)kKStep,
-                                 (size_t)width, (size_t)g.ntiles, hipMemcpyDeviceToDevice, stream) != hipSuccess)
+                                 es * width, (size_t)g.ntiles, hipMemcpyDeviceToDevice, stream) != hipSuccess)
                 return WINO_EHIP;
         }
     return WINO_OK;
@@ -1031,7 +1123,7 @@ extern "C" wino_status wino_f4_debug_tap_gemm(wino_f4_plan_t p, const int8_t* x,
     if (!m_out) return WINO_EINVAL;
     if (g.ntiles == 0) return WINO_OK;
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
-    st = run_k1<0>(p->m, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
+    st = run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
     if (st != WINO_OK) return st;
     return launch_k2<2>(p, g, layout, (const int8_t*)ws, nullptr, m_out, stream);
 }

@@ -50,6 +50,8 @@ namespace winof4 {
 // transform (plan_device.hip).
 wino_status plan_check_args(const Xform& X, int32_t cin, int32_t cout, const int8_t* in_exp,
                             const int8_t* w_exp, int32_t out_shift, int32_t relu);
+// Bytes of one k-row of 64 channels in the GEMM operands: 64 int8 or 64 fp16.
+inline int kbytes_per_channel(int bits) { return bits == 10 ? 2 : 1; }
 void plan_set_shape(const Xform& X, wino_f4_plan_s* p, int32_t cin, int32_t cout, int32_t out_shift,
                     int32_t relu);
 // Fills e_b, e_o, sh, bias_host and epi_bits from p->e_g and the column sums
@@ -69,6 +71,7 @@ wino_status device_weight_tables_int8(const Xform& X, wino_f4_plan_s* p, const i
 struct wino_f4_plan_s {
     int32_t m = 4;                    // output tile: F(m x m, 3 x 3), m = 4 or 2
     int32_t ntap = 36;                // (m + 2)^2 taps
+    int32_t bits = 8;                 // Winograd-domain integer width: 8, or 10 (int8/10)
     int32_t cin, cout, cin_pad, cout_pad;
     int8_t e_b[winof4::kTaps], e_g[winof4::kTaps], sh[winof4::kTaps];
     int32_t e_o;
@@ -76,8 +79,9 @@ struct wino_f4_plan_s {
     int32_t epi_bits;                 // 32 or 64
     int32_t tap_kernel = WINO_TAP_AUTO;
     int32_t device;
-    int8_t* uq_dev;                   // [ntap][cin_pad/64][cout_pad][64], zero padded
+    int8_t* uq_dev;                   // bits 8: int8 [ntap][cin_pad/64][cout_pad][64];
+                                      // bits 10: fp16 [ntap][cin_pad/32][cout_pad][32]; zero padded
     int32_t* bias_dev;                // [cout_pad], zero padded
-    std::vector<int8_t> uq_host;      // [ntap][cin][cout]; empty for device-built plans
+    std::vector<int16_t> uq_host;     // [ntap][cin][cout]; empty for device-built plans
     std::vector<int32_t> bias_host;   // [cout]
 };

@@ -8,8 +8,11 @@ the image), C4 and C5: the calibrated input tap exponents
 e_B, weight tap exponents e_G, alignment shifts, output shift, the SHA-256 of
 the full int8 output in NCHW order, and 64 sampled output values.
 
+With ``--bits 10`` the same records for the int8/10 variant (10-bit
+Winograd-domain integers, Sec. V) go to tests/golden/configs_i10.json.
+
 Uses only the oracle and the seeded input generators.  Run from the
-repository root:  python tests/golden/make_golden.py
+repository root:  python tests/golden/make_golden.py [--bits 10]
 """
 import hashlib
 import json
@@ -26,16 +29,16 @@ import workloads  # noqa: E402
 from oracle import quant, tapwise  # noqa: E402
 
 
-def layer_record(x, f, b, spec):
-    eb = tapwise.calibrate_input_exps(x)
-    plan0 = tapwise.make_plan(f, eb, bias=b, out_shift=0, relu=spec.relu)
+def layer_record(x, f, b, spec, bits=8):
+    eb = tapwise.calibrate_input_exps(x, bits=bits)
+    plan0 = tapwise.make_plan(f, eb, bias=b, out_shift=0, relu=spec.relu, bits=bits)
     if spec.out_shift is None:
         z = tapwise.prequant_output(x, plan0)
         zmax = int(np.abs(z).max(initial=0))
         s = min(tapwise.OUT_SHIFT_MAX, max(0, quant.cexp(zmax)))
     else:
         s, zmax = spec.out_shift, None
-    plan = tapwise.make_plan(f, eb, bias=b, out_shift=s, relu=spec.relu)
+    plan = tapwise.make_plan(f, eb, bias=b, out_shift=s, relu=spec.relu, bits=bits)
     y = tapwise.conv_int8(x, plan)
     rng = np.random.default_rng(1234)
     idx = [tuple(int(rng.integers(0, d)) for d in y.shape) for _ in range(64)]
@@ -51,6 +54,7 @@ def layer_record(x, f, b, spec):
 
 
 def main():
+    bits = 10 if "--bits" in sys.argv and sys.argv[sys.argv.index("--bits") + 1] == "10" else 8
     out = {}
     for name in ("C3", "C4", "C5"):
         t0 = time.time()
@@ -60,12 +64,13 @@ def main():
         for k, (f, b, spec) in enumerate(layers):
             if k > 0:
                 cur = workloads.next_layer_input(cur, spec)
-            rec, y = layer_record(cur, f, b, spec)
+            rec, y = layer_record(cur, f, b, spec, bits)
             recs.append(rec)
             cur = y
         out[name] = {"layers": recs}
         print(f"{name}: {len(recs)} layer(s) in {time.time() - t0:.1f} s", flush=True)
-    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "configs.json")
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                        "configs.json" if bits == 8 else "configs_i10.json")
     with open(path, "w") as fh:
         json.dump(out, fh, indent=1)
     print("wrote", path)
