@@ -77,8 +77,14 @@ def counter_traffic(cfg, layout, kernel, transform="f4"):
             kern[tok[1]] = (float(tok[3]), float(tok[5]))
         elif len(tok) == 2:
             vals[tok[0]] = float(tok[1])
-    src = os.path.join(ROOT, "paper_2209_12982_amd", "csrc", vals.get("src_file", ""))
-    if not os.path.isfile(src) or hashlib.sha256(open(src, "rb").read()).hexdigest() != vals.get("src_hash"):
+    # the hash covers every listed source ("a.hip+b.h": the files' bytes in order)
+    h = hashlib.sha256()
+    for name in vals.get("src_file", "").split("+"):
+        src = os.path.join(ROOT, "paper_2209_12982_amd", "csrc", name)
+        if not name or not os.path.isfile(src):
+            return None
+        h.update(open(src, "rb").read())
+    if h.hexdigest() != vals.get("src_hash"):
         return None
     for name, (f, w) in kern.items():
         if name.startswith(kernel):

@@ -35,13 +35,19 @@ namespace {
 
 constexpr int kBlock = 256;
 
+// Per-tap slot of the device state, one 128-byte line per tap so that the
+// workgroups' atomics on different taps do not queue on one line.
+struct alignas(128) TapSlot {
+    unsigned long long amax;          // bit pattern of max |approx d^2 U| (non-negative doubles order as integers)
+    int hi;                           // some |d^2 U| > 128 d^2 2^e_c
+    int lo;                           // some |d^2 U| > 128 d^2 2^(e_c - 1)
+    int imax;                         // int8 input: max |d^2 U|
+    int e_g;                          // result
+};
+
 // Per-call device state, cleared before pass 1.
 struct CalState {
-    unsigned long long amax[kTaps];   // bit pattern of max |approx d^2 U| (non-negative doubles order as integers)
-    int hi[kTaps];                    // some |d^2 U| > 128 d^2 2^e_c
-    int lo[kTaps];                    // some |d^2 U| > 128 d^2 2^(e_c - 1)
-    int imax[kTaps];                  // int8 input: max |d^2 U|
-    int e_g[kTaps];                   // result
+    TapSlot tap[kTaps];
     int bad;                          // a non-finite weight was seen
 };
 
@@ -128,10 +134,10 @@ __host__ __device__ inline int cexp_of(double amax, double unit) {
 // e_c + 1, and the two flags tell which.
 __device__ inline int tap_exponent(const CalState* st, const TapExps& te, int t, double unit) {
     if (te.given) return te.e[t];
-    const double amax = __longlong_as_double((long long)st->amax[t]);
+    const double amax = __longlong_as_double((long long)st->tap[t].amax);
     if (amax == 0.0) return 0;        // an expansion sums to 0.0 only when it is exactly 0
     const int ec = cexp_of(amax, unit);
-    return st->hi[t] ? ec + 1 : (st->lo[t] ? ec : ec - 1);
+    return st->tap[t].hi ? ec + 1 : (st->tap[t].lo ? ec : ec - 1);
 }
 
 __device__ inline double wave_max(double v) {
@@ -152,6 +158,16 @@ __device__ inline int wave_max_i(int v) {
     return v;
 }
 
+// Maximum over the workgroup (kBlock / 64 waves), valid in thread 0.
+template <class T>
+__device__ inline T block_max(T v, T* red) {
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    if (threadIdx.x == 0)
+        for (int i = 1; i < kBlock / 64; ++i) v = red[i] > v ? red[i] : v;
+    return v;
+}
+
 // Pass 1 (fp32): per-tap maximum of |approx d^2 U|; non-finite weights.
 __global__ void __launch_bounds__(kBlock) wt_f32_max(Xform X, Geo g, const float* __restrict__ w,
                                                      CalState* st) {
@@ -167,9 +183,11 @@ __global__ void __launch_bounds__(kBlock) wt_f32_max(Xform X, Geo g, const float
         bad = !finite;
         if (bad) v = 0.0;
     }
-    v = wave_max(v);
-    if ((threadIdx.x & 63) == 0 && v > 0.0) atomicMax(&st->amax[t], (unsigned long long)__double_as_longlong(v));
-    if (__any(bad) && (threadIdx.x & 63) == 0) atomicOr(&st->bad, 1);
+    __shared__ double red[kBlock / 64];
+    const bool any_bad = __any(bad);
+    v = block_max(wave_max(v), red);
+    if (threadIdx.x == 0 && v > 0.0) atomicMax(&st->tap[t].amax, (unsigned long long)__double_as_longlong(v));
+    if (any_bad && (threadIdx.x & 63) == 0) atomicOr(&st->bad, 1);
 }
 
 // Pass 2 (fp32): exact tests against 128 d^2 2^e_c and 128 d^2 2^(e_c - 1).
@@ -177,7 +195,7 @@ __global__ void __launch_bounds__(kBlock) wt_f32_flags(Xform X, Geo g, const flo
                                                        CalState* st) {
     const int t = blockIdx.y, a = t / X.n, b = t % X.n;
     const double unit = 128.0 * X.den2;
-    const double amax = __longlong_as_double((long long)st->amax[t]);
+    const double amax = __longlong_as_double((long long)st->tap[t].amax);
     if (amax == 0.0) return;                        // uniform per block
     const int ec = cexp_of(amax, unit);
     const double hi = ldexp(unit, ec), lo = ldexp(unit, ec - 1);
@@ -195,10 +213,13 @@ __global__ void __launch_bounds__(kBlock) wt_f32_flags(Xform X, Geo g, const flo
             else if (v >= lo * (1 - rel)) over_lo = sign_minus(c, lo) > 0 || sign_minus(c, -lo) < 0;
         }
     }
-    const bool any_hi = __any(over_hi), any_lo = __any(over_lo);
-    if ((threadIdx.x & 63) == 0) {
-        if (any_hi) atomicOr(&st->hi[t], 1);
-        if (any_lo) atomicOr(&st->lo[t], 1);
+    // one atomic per workgroup and flag, skipped once the flag is seen set
+    const int any_hi = __syncthreads_or(over_hi), any_lo = __syncthreads_or(over_lo);
+    if (threadIdx.x == 0) {
+        if (any_hi && !__hip_atomic_load(&st->tap[t].hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+            atomicOr(&st->tap[t].hi, 1);
+        if (any_lo && !__hip_atomic_load(&st->tap[t].lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+            atomicOr(&st->tap[t].lo, 1);
     }
 }
 
@@ -225,7 +246,7 @@ __global__ void __launch_bounds__(kBlock) wt_f32_quant(Xform X, Geo g, TapExps t
                                                        int* __restrict__ colsum) {
     const int t = blockIdx.y, a = t / X.n, b = t % X.n;
     const int e = tap_exponent(st, te, t, 128.0 * X.den2);
-    if (blockIdx.x == 0 && threadIdx.x == 0) st->e_g[t] = e;
+    if (blockIdx.x == 0 && threadIdx.x == 0) st->tap[t].e_g = e;
     const bool ok = e >= -126 && e <= 126;
     const long long j = (long long)blockIdx.x * kBlock + threadIdx.x;
     if (j >= g.plane) return;                        // whole waves: plane is a multiple of 64
@@ -257,8 +278,9 @@ __global__ void __launch_bounds__(kBlock) wt_i8_max(Xform X, Geo g, const int8_t
     const long long j = (long long)blockIdx.x * kBlock + threadIdx.x;
     int co, ci, v = 0;
     if (j < g.plane && locate(g, j, co, ci)) v = abs(tap_int(X, w + ((long long)co * g.cin + ci) * 9, a, b));
-    v = wave_max_i(v);
-    if ((threadIdx.x & 63) == 0 && v > 0) atomicMax(&st->imax[t], v);
+    __shared__ int red[kBlock / 64];
+    v = block_max(wave_max_i(v), red);
+    if (threadIdx.x == 0 && v > 0) atomicMax(&st->tap[t].imax, v);
 }
 
 // m <= unit 2^d for 1 <= m < 2^20, unit < 2^20, -40 <= d <= 40.
@@ -302,8 +324,8 @@ __global__ void __launch_bounds__(kBlock) wt_i8_quant(Xform X, Geo g, TapExps te
                                                       const int8_t* __restrict__ w, CalState* st,
                                                       int8_t* __restrict__ uq, int* __restrict__ colsum) {
     const int t = blockIdx.y, a = t / X.n, b = t % X.n;
-    const int e = te.given ? te.e[t] : (st->imax[t] == 0 ? 0 : int8_tap_exponent(st->imax[t], X.den2, e_f));
-    if (blockIdx.x == 0 && threadIdx.x == 0) st->e_g[t] = e;
+    const int e = te.given ? te.e[t] : (st->tap[t].imax == 0 ? 0 : int8_tap_exponent(st->tap[t].imax, X.den2, e_f));
+    if (blockIdx.x == 0 && threadIdx.x == 0) st->tap[t].e_g = e;
     const long long j = (long long)blockIdx.x * kBlock + threadIdx.x;
     if (j >= g.plane) return;
     int co, ci, q = 0;
@@ -357,8 +379,8 @@ wino_status run_device_tables(const Xform& X, wino_f4_plan_s* p, const int8_t* w
     if (!ok) return WINO_EHIP;
     if (host.bad) return WINO_EINVAL;
     for (int t = 0; t < X.ntap; ++t) {
-        if (host.e_g[t] < -126 || host.e_g[t] > 126) return WINO_ERANGE;
-        p->e_g[t] = (int8_t)host.e_g[t];
+        if (host.tap[t].e_g < -126 || host.tap[t].e_g > 126) return WINO_ERANGE;
+        p->e_g[t] = (int8_t)host.tap[t].e_g;
     }
     return WINO_OK;
 }

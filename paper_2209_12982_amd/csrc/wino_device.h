@@ -270,13 +270,17 @@ __device__ __forceinline__ void tap_epilogue(const v4i (&acc)[Wino<M>::NTAP], co
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int co = co_base + 4 * lk + r;
-        acc_t mv[NT];
-#pragma unroll
-        for (int t = 0; t < NT; ++t) mv[t] = (acc_t)acc[t][r] << g.tab.sh[t];
-        mv[N + 1] += (acc_t)bias[co] + rnd;
+        // row pass one row of taps at a time, so only N widened values are
+        // live besides the row results
         acc_t rp[N][M];
 #pragma unroll
-        for (int a = 0; a < N; ++a) Wino<M>::at(&mv[N * a], rp[a]);
+        for (int a = 0; a < N; ++a) {
+            acc_t mv[N];
+#pragma unroll
+            for (int bb = 0; bb < N; ++bb) mv[bb] = (acc_t)acc[N * a + bb][r] << g.tab.sh[N * a + bb];
+            if (a == 1) mv[1] += (acc_t)bias[co] + rnd;   // tap (1, 1)
+            Wino<M>::at(mv, rp[a]);
+        }
         acc_t yv[M][M];
 #pragma unroll
         for (int jj = 0; jj < M; ++jj) {
