@@ -33,35 +33,42 @@ namespace {
 // ---------------------------------------------------------------------------
 // K1: input transform
 // ---------------------------------------------------------------------------
-constexpr int K1_TX = 16;               // tiles per block along x
+// tiles per block along x (TX below): 16, one thread per (tile, 4 channels).
+// Blocks of 20 tiles would leave no idle tiles in a row of 40 (C5: three
+// blocks of 16, the third half empty), but measured slower there (24.3 against
+// 23.3 us).
+constexpr int K1_TX = 16;
 constexpr int K1_CG = 64;               // channels per block
 constexpr int K1_CS = 20;               // LDS words per pixel (16 used, 4 pad)
-constexpr int K1_THREADS = 256;
-// halo band of a block: M + 2 rows x (M * K1_TX + 2) pixels
-template <int M>
+// halo band of a block: M + 2 rows x (M * TX + 2) pixels
+template <int M, int TX>
 struct K1Band {
-    static constexpr int ROWS = M + 2, COLS = M * K1_TX + 2;
+    static constexpr int ROWS = M + 2, COLS = M * TX + 2, THREADS = 16 * TX;
 };
+
 
 struct K1Args {
     int n, cin, h, w, th, tw, cin_pad;
     int ntxb, ncg;
     int x_vec;                          // 16-byte loads allowed (Cin % 16 == 0, x aligned)
+    int vq_buf;                         // tap planes below 4 GiB: buffer stores with a scalar base
     long long t_pad;                    // tile stride of a tap plane in Vq
+    long long plane_bytes;              // bytes of one tap plane of Vq
     TapTables tab;
+    uint32_t rnd2[kTaps];               // 2^(e_B - 1) (0 for e_B = 0) in both 16-bit halves
 };
 
 // Stage the halo band of one block into LDS as [row][col][channel] bytes
 // (channel fastest, K1_CS words per pixel).  Rows M ty - 1 .. M ty + M,
-// columns M tx0 - 1 .. M (tx0 + K1_TX), channels ci0 .. ci0+63; zero outside
+// columns M tx0 - 1 .. M (tx0 + TX), channels ci0 .. ci0+63; zero outside
 // the image and beyond Cin.
-template <int M, int LAYOUT>
+template <int M, int LAYOUT, int TX>
 __device__ __forceinline__ void k1_stage_band(uint32_t* lds, const int8_t* __restrict__ x,
                                               const K1Args& g, int img, int ty, int tx0, int ci0) {
-    constexpr int ROWS = K1Band<M>::ROWS, COLS = K1Band<M>::COLS;
+    constexpr int ROWS = K1Band<M, TX>::ROWS, COLS = K1Band<M, TX>::COLS, THREADS = K1Band<M, TX>::THREADS;
     const int h0 = M * ty - 1, w0 = M * tx0 - 1;
     if (LAYOUT == WINO_NHWC) {
-        for (int id = threadIdx.x; id < ROWS * COLS * 4; id += K1_THREADS) {
+        for (int id = threadIdx.x; id < ROWS * COLS * 4; id += THREADS) {
             int pix = id >> 2, part = id & 3;
             int r = pix / COLS, c = pix - r * COLS;
             int hh = h0 + r, ww = w0 + c, cb = ci0 + 16 * part;
@@ -81,7 +88,7 @@ __device__ __forceinline__ void k1_stage_band(uint32_t* lds, const int8_t* __res
         }
     } else {
         uint8_t* lb = (uint8_t*)lds;
-        for (int id = threadIdx.x; id < K1_CG * ROWS * COLS; id += K1_THREADS) {
+        for (int id = threadIdx.x; id < K1_CG * ROWS * COLS; id += THREADS) {
             int c = id % COLS;
             int rest = id / COLS;
             int r = rest % ROWS, ch = rest / ROWS;
@@ -97,13 +104,13 @@ __device__ __forceinline__ void k1_stage_band(uint32_t* lds, const int8_t* __res
 // MODE 0: write Vq.  MODE 1: per-tap max |V| into tapmax[NTAP] (calibration).
 // Q: Winograd-domain width, 8 (int8 Vq) or 10 (int8/10: fp16 Vq holding
 // 10-bit integers, [ntap][cin_pad/32][t_pad][32]).
-template <int M, int LAYOUT, int MODE, int Q = 8>
-__global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __restrict__ x,
+template <int M, int LAYOUT, int MODE, int Q = 8, int TX = K1_TX>
+__global__ __launch_bounds__(16 * TX) void wino_input_xform(const int8_t* __restrict__ x,
                                                                int8_t* __restrict__ vq,
                                                                int* __restrict__ tapmax, K1Args g) {
     constexpr int N = Wino<M>::N, NT = Wino<M>::NTAP;
-    constexpr int COLS = K1Band<M>::COLS;
-    __shared__ uint32_t band[K1Band<M>::ROWS * COLS * K1_CS];
+    constexpr int COLS = K1Band<M, TX>::COLS;
+    __shared__ uint32_t band[K1Band<M, TX>::ROWS * COLS * K1_CS];
     __shared__ int red[NT];
     // Logical block order: channel group fastest, then tile-column block,
     // then tile row; consecutive logical ids are kept on one XCD (its L2),
@@ -115,10 +122,10 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
     const int txb = bid % g.ntxb;
     const int row = bid / g.ntxb;         // img * th + ty
     const int img = row / g.th, ty = row - img * g.th;
-    const int tx0 = txb * K1_TX, ci0 = cgi * K1_CG;
+    const int tx0 = txb * TX, ci0 = cgi * K1_CG;
     if (MODE == 1 && threadIdx.x < NT) red[threadIdx.x] = 0;
 
-    k1_stage_band<M, LAYOUT>(band, x, g, img, ty, tx0, ci0);
+    k1_stage_band<M, LAYOUT, TX>(band, x, g, img, ty, tx0, ci0);
     __syncthreads();
 
     // thread -> (tile j, channel quad q): 16 quads x 16 tiles
@@ -138,21 +145,38 @@ __global__ __launch_bounds__(K1_THREADS) void wino_input_xform(const int8_t* __r
     if (MODE == 0) {
         if (!valid) return;
         const long long tile = (long long)row * g.tw + tx;
-        if constexpr (Q == 10) {
-            // Vq[t][2 cgi + q / 8][tile][32] fp16: this block's 64 channels are
-            // the 32-channel k rows 2 cgi and 2 cgi + 1; 4 halves per thread
-            uint2* dst = (uint2*)((uint16_t*)vq + ((long long)(2 * cgi + (q >> 3)) * g.t_pad + tile) * 32) + (q & 7);
-            const long long plane = g.t_pad * g.cin_pad / 4;   // 4-half groups per tap plane
+        // byte offset of this thread's values within a tap plane:
+        //   Q = 8:  Vq[t][cgi][tile][64], 4 bytes (channels 4q .. 4q + 3)
+        //   Q = 10: Vq[t][2 cgi + q / 8][tile][32] fp16 (this block's 64
+        //           channels are the 32-channel k rows 2 cgi and 2 cgi + 1),
+        //           8 bytes (4 halves)
+        const long long off = Q == 10 ? (((long long)(2 * cgi + (q >> 3)) * g.t_pad + tile) * 32 + 4 * (q & 7)) * 2
+                                      : ((long long)cgi * g.t_pad + tile) * K1_CG + 4 * q;
+        if (g.vq_buf) {
+            // per tap a buffer resource on the tap plane (scalar base and
+            // size) and one 32-bit lane offset for all taps
+            const int voff = (int)off;
 #pragma unroll
-            for (int t = 0; t < NT; ++t)
-                dst[t * plane] = requant10_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t]);
+            for (int t = 0; t < NT; ++t) {
+                const __amdgpu_buffer_rsrc_t rs =
+                    __builtin_amdgcn_make_buffer_rsrc(vq + t * g.plane_bytes, 0, (int)g.plane_bytes, 0x00020000);
+                if constexpr (Q == 10) {
+                    const uint2 v = requant10_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t], g.rnd2[t]);
+                    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u, v), rs, voff, 0, 0);
+                } else {
+                    __builtin_amdgcn_raw_buffer_store_b32(
+                        requant_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t], g.rnd2[t]), rs, voff, 0, 0);
+                }
+            }
         } else {
-            // Vq[t][cgi][tile][64]: this block's 64 channels are k block cgi
-            uint32_t* dst = (uint32_t*)(vq + ((long long)cgi * g.t_pad + tile) * K1_CG) + q;
-            const long long plane = g.t_pad * g.cin_pad / 4;   // words per tap plane
 #pragma unroll
-            for (int t = 0; t < NT; ++t)
-                dst[t * plane] = requant_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t]);
+            for (int t = 0; t < NT; ++t) {
+                int8_t* dst = vq + t * g.plane_bytes + off;
+                if constexpr (Q == 10)
+                    *(uint2*)dst = requant10_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t], g.rnd2[t]);
+                else
+                    *(uint32_t*)dst = requant_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t], g.rnd2[t]);
+            }
         }
     } else {
         if (valid) {
@@ -746,7 +770,7 @@ TapTables tables_of(const wino_f4_plan_s* p) {
     return t;
 }
 
-K1Args k1_args(const Geometry& g, int cin, int cin_pad, const TapTables& tab) {
+K1Args k1_args(const Geometry& g, int cin, int cin_pad, const TapTables& tab, int bits = 8) {
     K1Args a;
     a.n = g.n;
     a.cin = cin;
@@ -755,29 +779,43 @@ K1Args k1_args(const Geometry& g, int cin, int cin_pad, const TapTables& tab) {
     a.th = g.th;
     a.tw = g.tw;
     a.cin_pad = cin_pad;
-    a.ntxb = (g.tw + K1_TX - 1) / K1_TX;
+    a.ntxb = 0;                          // set at launch with the block width
     a.ncg = cin_pad / K1_CG;
     a.t_pad = g.t_pad;
     a.tab = tab;
+    for (int t = 0; t < kTaps; ++t) {
+        const int e = tab.eb[t];
+        const uint32_t r = e > 0 ? (1u << (e - 1)) : 0u;
+        a.rnd2[t] = r | (r << 16);
+    }
+    a.plane_bytes = g.t_pad * cin_pad * kbytes_per_channel(bits);
+    a.vq_buf = a.plane_bytes < 0x7fffffffLL;
     a.x_vec = 0;
     return a;
+}
+
+template <int M, int MODE, int Q, int TX>
+wino_status launch_k1_tx(const K1Args& a, wino_layout layout, const int8_t* x, int8_t* vq, int* tapmax,
+                         hipStream_t stream) {
+    K1Args args = a;
+    args.ntxb = (a.tw + TX - 1) / TX;
+    long long blocks = (long long)args.ntxb * a.ncg * a.n * a.th;
+    if (blocks == 0) return WINO_OK;
+    if (blocks > 0x7fffffffll) return WINO_EUNSUPPORTED;
+    args.x_vec = (a.cin % 16 == 0) && (((uintptr_t)x & 15) == 0);
+    if (layout == WINO_NHWC)
+        hipLaunchKernelGGL((wino_input_xform<M, WINO_NHWC, MODE, Q, TX>), dim3((unsigned)blocks), dim3(16 * TX), 0,
+                           stream, x, vq, tapmax, args);
+    else
+        hipLaunchKernelGGL((wino_input_xform<M, WINO_NCHW, MODE, Q, TX>), dim3((unsigned)blocks), dim3(16 * TX), 0,
+                           stream, x, vq, tapmax, args);
+    return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
 }
 
 template <int M, int MODE, int Q = 8>
 wino_status launch_k1(const K1Args& a, wino_layout layout, const int8_t* x, int8_t* vq, int* tapmax,
                       hipStream_t stream) {
-    long long blocks = (long long)a.ntxb * a.ncg * a.n * a.th;
-    if (blocks == 0) return WINO_OK;
-    if (blocks > 0x7fffffffll) return WINO_EUNSUPPORTED;
-    K1Args args = a;
-    args.x_vec = (a.cin % 16 == 0) && (((uintptr_t)x & 15) == 0);
-    if (layout == WINO_NHWC)
-        hipLaunchKernelGGL((wino_input_xform<M, WINO_NHWC, MODE, Q>), dim3((unsigned)blocks), dim3(K1_THREADS), 0,
-                           stream, x, vq, tapmax, args);
-    else
-        hipLaunchKernelGGL((wino_input_xform<M, WINO_NCHW, MODE, Q>), dim3((unsigned)blocks), dim3(K1_THREADS), 0,
-                           stream, x, vq, tapmax, args);
-    return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
+    return launch_k1_tx<M, MODE, Q, K1_TX>(a, layout, x, vq, tapmax, stream);
 }
 
 template <class C>
@@ -975,7 +1013,7 @@ extern "C" wino_status wino_f4_conv_int8(wino_f4_plan_t p, const int8_t* x, int8
     }
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
     int8_t* vq = (int8_t*)ws;
-    st = run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, vq, nullptr, stream);
+    st = run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p), p->bits), layout, x, vq, nullptr, stream);
     if (st != WINO_OK) return st;
     return launch_k2<0>(p, g, layout, vq, y, nullptr, stream);
 }
@@ -988,7 +1026,7 @@ extern "C" wino_status wino_f4_input_transform(wino_f4_plan_t p, const int8_t* x
     if (st != WINO_OK) return st;
     if (g.ntiles == 0) return WINO_OK;
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
-    return run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
+    return run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p), p->bits), layout, x, (int8_t*)ws, nullptr, stream);
 }
 
 extern "C" wino_status wino_f4_tap_gemm(wino_f4_plan_t p, const void* ws, size_t ws_bytes, int8_t* y, int32_t n,
@@ -1073,7 +1111,7 @@ extern "C" wino_status wino_f4_calibrate_output(wino_f4_plan_t p, const int8_t* 
         unsigned long long* dmax = nullptr;
         if (hipMalloc(&dmax, sizeof(unsigned long long)) != hipSuccess) return WINO_ENOMEM;
         bool ok = hipMemsetAsync(dmax, 0, sizeof(unsigned long long), stream) == hipSuccess;
-        if (ok) ok = run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws,
+        if (ok) ok = run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p), p->bits), layout, x, (int8_t*)ws,
                                nullptr, stream) == WINO_OK;
         if (ok) ok = launch_k2<1>(p, g, layout, (const int8_t*)ws, nullptr, dmax, stream) == WINO_OK;
         if (ok) ok = hipMemcpyAsync(&host, dmax, sizeof(host), hipMemcpyDeviceToHost, stream) == hipSuccess;
@@ -1095,7 +1133,7 @@ extern "C" wino_status wino_f4_debug_input_transform(wino_f4_plan_t p, const int
     if (!vq_out) return WINO_EINVAL;
     if (g.ntiles == 0) return WINO_OK;
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
-    st = run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
+    st = run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p), p->bits), layout, x, (int8_t*)ws, nullptr, stream);
     if (st != WINO_OK) return st;
     // compact [ntap][cin_pad/kpr][t_pad][kpr] -> [ntap][ntiles][cin] (elements
     // of es bytes: int8, or fp16 for 10-bit plans), one 2-D copy per (tap, k row)
@@ -1123,7 +1161,7 @@ extern "C" wino_status wino_f4_debug_tap_gemm(wino_f4_plan_t p, const int8_t* x,
     if (!m_out) return WINO_EINVAL;
     if (g.ntiles == 0) return WINO_OK;
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
-    st = run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p)), layout, x, (int8_t*)ws, nullptr, stream);
+    st = run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p), p->bits), layout, x, (int8_t*)ws, nullptr, stream);
     if (st != WINO_OK) return st;
     return launch_k2<2>(p, g, layout, (const int8_t*)ws, nullptr, m_out, stream);
 }
