@@ -242,7 +242,7 @@ def main():
     rows = W.wino_f4_tap_kernel_choice(plan, n, h, w) == W.TAP_ROWS
     # kernel names as the profiler shows them (template arguments included;
     # the tap-resident kernel's block configuration is a class argument)
-    k1_name, k1_inst = "wino_input_xform", f"wino_input_xform<{mt},{lay},0,{args.bits}>"
+    k1_name, k1_inst = "wino_input_xform", f"wino_input_xform<{mt},{lay},0,{args.bits},16>"
     k2_name = "wino_tap_gemm_rows" if rows else "wino_tap_gemm"
     k2_inst = (f"wino_tap_gemm_rows<{lay}>" if rows
                else f"wino_tap_gemm<{mt},{lay},{info['epilogue_bits']},0,{args.bits}>")
