@@ -139,6 +139,11 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def _nbytes(t):
+    """Size in bytes of a device tensor, 0 for None."""
+    return 0 if t is None else t.numel() * t.element_size()
+
+
 def _host(a, dtype, n=None):
     a = np.ascontiguousarray(np.asarray(a, dtype=dtype))
     if n is not None and a.size != n:
@@ -336,7 +341,7 @@ def wino_f4_workspace_bytes(plan, n, h, w, variant=SPLIT):
 
 def wino_f4_conv_int8(plan, x, y, n, h, w, layout=NCHW, variant=SPLIT, workspace=None, stream=None):
     lib = load_library()
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    ws_bytes = _nbytes(workspace)
     st = lib.wino_f4_conv_int8(plan.handle, _ptr(x), _ptr(y), n, h, w, layout, variant,
                                _ptr(workspace), ws_bytes, _stream(stream))
     _check(st, "wino_f4_conv_int8")
@@ -344,14 +349,14 @@ def wino_f4_conv_int8(plan, x, y, n, h, w, layout=NCHW, variant=SPLIT, workspace
 
 def wino_f4_input_transform(plan, x, n, h, w, layout, workspace, stream=None):
     lib = load_library()
-    ws_bytes = workspace.numel() * workspace.element_size()
+    ws_bytes = _nbytes(workspace)
     _check(lib.wino_f4_input_transform(plan.handle, _ptr(x), n, h, w, layout, _ptr(workspace), ws_bytes,
                                        _stream(stream)), "wino_f4_input_transform")
 
 
 def wino_f4_tap_gemm(plan, workspace, y, n, h, w, layout, stream=None):
     lib = load_library()
-    ws_bytes = workspace.numel() * workspace.element_size()
+    ws_bytes = _nbytes(workspace)
     _check(lib.wino_f4_tap_gemm(plan.handle, _ptr(workspace), ws_bytes, _ptr(y), n, h, w, layout,
                                 _stream(stream)), "wino_f4_tap_gemm")
 
@@ -384,7 +389,7 @@ def wino_f2_calibrate_input_i10(x, n, cin, h, w, layout=NCHW, stream=None):
 
 def wino_f4_calibrate_output(plan, x, n, h, w, layout=NCHW, workspace=None, stream=None):
     lib = load_library()
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    ws_bytes = _nbytes(workspace)
     zmax = ctypes.c_int64()
     shift = ctypes.c_int32()
     st = lib.wino_f4_calibrate_output(plan.handle, _ptr(x), n, h, w, layout, _ptr(workspace), ws_bytes,
@@ -395,7 +400,7 @@ def wino_f4_calibrate_output(plan, x, n, h, w, layout=NCHW, workspace=None, stre
 
 def wino_f4_debug_input_transform(plan, x, n, h, w, layout, vq, workspace, stream=None):
     lib = load_library()
-    ws_bytes = workspace.numel() * workspace.element_size()
+    ws_bytes = _nbytes(workspace)
     st = lib.wino_f4_debug_input_transform(plan.handle, _ptr(x), n, h, w, layout, _ptr(vq), _ptr(workspace),
                                            ws_bytes, _stream(stream))
     _check(st, "wino_f4_debug_input_transform")
@@ -403,7 +408,7 @@ def wino_f4_debug_input_transform(plan, x, n, h, w, layout, vq, workspace, strea
 
 def wino_f4_debug_tap_gemm(plan, x, n, h, w, layout, m, workspace, stream=None):
     lib = load_library()
-    ws_bytes = workspace.numel() * workspace.element_size()
+    ws_bytes = _nbytes(workspace)
     st = lib.wino_f4_debug_tap_gemm(plan.handle, _ptr(x), n, h, w, layout, _ptr(m), _ptr(workspace),
                                     ws_bytes, _stream(stream))
     _check(st, "wino_f4_debug_tap_gemm")
