@@ -554,9 +554,15 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
                                         : vq + (tl_blk + 16 * (grp - 4)) * kKStep) +
                               b0 * tap_stride;
     uint8_t* const dst = lds + 1024 * grp + b0 * KR_CHUNK;
-    int next_a = 0, next_kc = 0, next_buf = 0;
+    // The copy source advances by one k-chunk per stage and by a row of taps
+    // (minus the chunks walked) at the end of a row: one 64-bit add per stage
+    // instead of rebuilding the address from (row, chunk) products, which
+    // cost ~50 scalar instructions per stage and wave.
+    const int8_t* next_src = src;
+    const long long row_adv = 6 * tap_stride - (long long)(nkc - 1) * kc_stride;
+    const long long slice_step = step * tap_stride;
+    int next_kc = 0, next_buf = 0;
     auto issue_next = [&]() {
-        const int8_t* p = src + (long long)(6 * next_a) * tap_stride + next_kc * kc_stride;
         uint8_t* d = dst + next_buf * KR_STAGE;
         // plain (temporal) loads for Vq too: the four channel blocks of one
         // tile block run side by side on one XCD (consecutive logical ids)
@@ -564,12 +570,14 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
         // the later readers go back to memory and cost 8%
 #pragma unroll
         for (int i = 0; i < KR_LPW; ++i)
-            __builtin_amdgcn_global_load_lds((const void*)(p + step * i * tap_stride + lane_off),
+            __builtin_amdgcn_global_load_lds((const void*)(next_src + i * slice_step + lane_off),
                                              (__attribute__((address_space(3))) void*)(d + step * i * KR_CHUNK), 16,
                                              0, 0);
         if (++next_kc == nkc) {
             next_kc = 0;
-            ++next_a;
+            next_src += row_adv;
+        } else {
+            next_src += kc_stride;
         }
         next_buf = next_buf == KR_NBUF - 1 ? 0 : next_buf + 1;
     };
