@@ -222,6 +222,22 @@ __device__ __forceinline__ void input_tile_transform(const uint32_t (&wv)[N][N],
 // (workgroup i runs on XCD i % 8).  Remap so that each XCD works through one
 // contiguous range of logical block ids, i.e. blocks with neighbouring ids
 // share that XCD's L2.
+// floor(n / f.d) for 0 <= n < 2^31 (FastDiv).
+__device__ __forceinline__ uint32_t fast_div(uint32_t n, const winof4::FastDiv& f) {
+    return f.d == 1 ? n : __umulhi(n, f.mul) >> f.shr;
+}
+
+// Image, tile row and tile column of a tile index (tiles < 2^26); G provides
+// th, tw and the FastDivs dimg (th * tw) and dtw (tw).
+template <class G>
+__device__ __forceinline__ void tile_coords(long long tile, const G& g, int& img, int& ty, int& tx) {
+    const uint32_t t = (uint32_t)tile;
+    img = (int)fast_div(t, g.dimg);
+    const uint32_t trem = t - (uint32_t)img * (uint32_t)(g.th * g.tw);
+    ty = (int)fast_div(trem, g.dtw);
+    tx = (int)(trem - (uint32_t)ty * (uint32_t)g.tw);
+}
+
 __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
     const int nx = 8;
     const int full = nblocks / nx * nx;
@@ -289,9 +305,8 @@ __device__ __forceinline__ void tap_epilogue(const v4i (&acc)[Wino<M>::NTAP], co
     }
 
     const long long tt = tile_ok ? tile : 0;
-    const int img = (int)(tt / ((long long)g.th * g.tw));
-    const int trem = (int)(tt - (long long)img * g.th * g.tw);
-    const int ty = trem / g.tw, tx = trem - ty * g.tw;
+    int img, ty, tx;
+    tile_coords(tt, g, img, ty, tx);
     const int s = g.out_shift;
     const acc_t rnd = (MODE == 0 && s > 0) ? ((acc_t)1 << (s - 1)) : 0;
     const int lo = g.relu ? 0 : -128;

@@ -40,6 +40,7 @@ struct K4Args {
     int nbco, nblocks;
     int out_shift, relu;
     int x_vec;                      // NHWC 2-byte channel-pair loads allowed
+    FastDiv dimg, dtw;              // division by th * tw and by tw (tile coordinates)
     TapTables tab;
 };
 
@@ -211,6 +212,8 @@ wino_status wino_f4_conv_fused(const wino_f4_plan_s* p, const int8_t* x, int8_t*
     a.tw = (w + 3) / 4;
     a.ntiles = (long long)n * a.th * a.tw;
     if (a.ntiles == 0) return WINO_OK;
+    a.dimg = make_fastdiv((uint32_t)(a.th * a.tw));
+    a.dtw = make_fastdiv((uint32_t)a.tw);
     a.nbco = p->cout_pad / K4_CO;
     const long long blocks = (a.ntiles + K4_TL - 1) / K4_TL * a.nbco;
     if (blocks > 0x7fffffffll) return WINO_EUNSUPPORTED;

@@ -251,6 +251,7 @@ struct K2Args {
     int nbco, nblocks;
     int out_shift, relu;
     int y_staged;              // row-streamed kernel: stage NHWC output through LDS
+    FastDiv dimg, dtw;         // division by th * tw and by tw (tile coordinates)
     TapTables tab;
 };
 
@@ -466,9 +467,8 @@ template <int LAYOUT, class G>
 __device__ __forceinline__ void store_tile(const int (&q)[4][16], const G& g, int8_t* __restrict__ y, int co0,
                                            long long tile) {
     if (tile >= g.ntiles) return;
-    const int img = (int)(tile / ((long long)g.th * g.tw));
-    const int trem = (int)(tile - (long long)img * g.th * g.tw);
-    const int ty = trem / g.tw, tx = trem - ty * g.tw;
+    int img, ty, tx;
+    tile_coords(tile, g, img, ty, tx);
     const int s = g.out_shift;
     const int lo = g.relu ? 0 : -128;
     int v[4][16];
@@ -715,9 +715,8 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
         for (int tl = wave; tl < KR_TL; tl += KR_WAVES) {
             const long long tile = tl_blk + tl;   // wave-uniform
             if (tile >= g.ntiles) break;
-            const int img = (int)(tile / ((long long)g.th * g.tw));
-            const int trem = (int)(tile - (long long)img * g.th * g.tw);
-            const int ty = trem / g.tw, tx = trem - ty * g.tw;
+            int img, ty, tx;
+            tile_coords(tile, g, img, ty, tx);
             const int yy = 4 * ty + (p >> 2), xx = 4 * tx + (p & 3);
             if (yy < g.h && xx < g.w) {
                 const uint4 v = *(const uint4*)(lds + tl * PITCH + 64 * p + 16 * q);
@@ -899,6 +898,8 @@ wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout la
     a.out_shift = p->out_shift;
     a.relu = p->relu;
     a.y_staged = layout == WINO_NHWC && p->cout % KR_CO == 0 && ((uintptr_t)y & 15) == 0;
+    a.dimg = make_fastdiv((uint32_t)(g.th * g.tw));
+    a.dtw = make_fastdiv((uint32_t)g.tw);
     a.tab = tables_of(p);
     if (p->bits == 10) {
         if (p->m == 2) return launch_resident<K2F2_10, 2, MODE, 10>(p, g, layout, vq, y, aux, a, stream);

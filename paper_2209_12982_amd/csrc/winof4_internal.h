@@ -26,6 +26,27 @@ struct TapTables {
     int32_t sh[kTaps];   // alignment shifts e_B + e_G - e_o
 };
 
+// Division by a fixed divisor 1 <= d < 2^26 of dividends n < 2^31 without a
+// divide instruction (Granlund and Montgomery, "Division by Invariant
+// Integers using Multiplication", 1994): with l = ceil(log2 d) and
+// p = 31 + l, m = ceil(2^p / d) < 2^32 gives floor(n / d) =
+// floor(n m / 2^p), because n m / 2^p - n / d < n / 2^p <= n / (2^31 d) < 1/d.
+struct FastDiv {
+    uint32_t mul;     // m (unused for d = 1)
+    uint32_t shr;     // p - 32
+    uint32_t d;
+};
+inline FastDiv make_fastdiv(uint32_t d) {
+    FastDiv f = {0u, 0u, d};
+    if (d <= 1) return f;
+    int l = 0;
+    while ((1ull << l) < d) ++l;
+    const int p = 31 + l;
+    f.mul = (uint32_t)(((1ull << p) + d - 1) / d);
+    f.shr = (uint32_t)(p - 32);
+    return f;
+}
+
 // One transform F(m x m, 3 x 3): n = m + 2 input rows, n^2 taps, Gint = d G
 // with integer entries (Sec. II matrices: d = 24 for F4, 2 for F2),
 // den2 = d^2, A^T (m x n).
