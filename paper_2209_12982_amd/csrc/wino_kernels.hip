@@ -105,7 +105,7 @@ __device__ __forceinline__ void k1_stage_band(uint32_t* lds, const int8_t* __res
 // Q: Winograd-domain width, 8 (int8 Vq) or 10 (int8/10: fp16 Vq holding
 // 10-bit integers, [ntap][cin_pad/32][t_pad][32]).
 template <int M, int LAYOUT, int MODE, int Q = 8, int TX = K1_TX>
-__global__ __launch_bounds__(16 * TX) void wino_input_xform(const int8_t* __restrict__ x,
+__global__ __launch_bounds__(16 * TX, 5) void wino_input_xform(const int8_t* __restrict__ x,
                                                                int8_t* __restrict__ vq,
                                                                int* __restrict__ tapmax, K1Args g) {
     constexpr int N = Wino<M>::N, NT = Wino<M>::NTAP;
