@@ -162,7 +162,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
-              "(the layer shards by batch with no communication; see DESIGN.md)", file=sys.stderr)
+              "(the layer shards by batch with no communication between GPUs)", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
