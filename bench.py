@@ -161,7 +161,7 @@ def cpu_baseline(x, layers_plan, n_img, spec, target_s=10.0):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
               "(the layer shards by batch with no communication between GPUs)", file=sys.stderr)
         sys.exit(2)
     import numpy as np
