@@ -249,9 +249,13 @@ def main():
     # kernel names as the profiler shows them (template arguments included;
     # the tap-resident kernel's block configuration is a class argument)
     k1_name, k1_inst = "wino_input_xform", f"wino_input_xform<{mt},{lay},0,{args.bits},16>"
-    k2_name = "wino_tap_gemm_rows" if rows else "wino_tap_gemm"
-    k2_inst = (f"wino_tap_gemm_rows<{lay}>" if rows
-               else f"wino_tap_gemm<{mt},{lay},{info['epilogue_bits']},0,{args.bits}>")
+    if rows and args.bits == 10:
+        k2_name = "wino_tap_gemm_rows_wide"
+        k2_inst = f"wino_tap_gemm_rows_wide<{lay},10,{'int' if info['epilogue_bits'] == 32 else 'longlong'}>"
+    elif rows:
+        k2_name, k2_inst = "wino_tap_gemm_rows", f"wino_tap_gemm_rows<{lay}>"
+    else:
+        k2_name, k2_inst = "wino_tap_gemm", f"wino_tap_gemm<{mt},{lay},{info['epilogue_bits']},0,{args.bits}>"
     k1_ms = k2_ms = None
     if variant == W.SPLIT:
         k1 = lambda: W.wino_f4_input_transform(plan, xd, n, h, w, layout, ws)

@@ -463,8 +463,19 @@ static_assert(kTilePad % KR_TL == 0, "tile blocks tile the padded tiles");
 // Requantize and store the 4 channels x 16 pixels of one tile held by a lane:
 // q[r][4i+j] is Y + bias + rounding constant of channel co0 + r at pixel
 // (i, j) of the tile.
-template <int LAYOUT, class G>
-__device__ __forceinline__ void store_tile(const int (&q)[4][16], const G& g, int8_t* __restrict__ y, int co0,
+// Y (int32 or int64 T) -> clamp(Y >> out_shift, lo, 127) as int
+template <class T>
+__device__ __forceinline__ int requant_out(T yv, int s, int lo) {
+    if constexpr (sizeof(T) == 4) {
+        return med3_i32(yv >> s, lo, 127);
+    } else {
+        const T v = yv >> s;
+        return (int)(v < (T)lo ? (T)lo : (v > (T)127 ? (T)127 : v));
+    }
+}
+
+template <int LAYOUT, class G, class T>
+__device__ __forceinline__ void store_tile(const T (&q)[4][16], const G& g, int8_t* __restrict__ y, int co0,
                                            long long tile) {
     if (tile >= g.ntiles) return;
     int img, ty, tx;
@@ -475,7 +486,7 @@ __device__ __forceinline__ void store_tile(const int (&q)[4][16], const G& g, in
 #pragma unroll
     for (int r = 0; r < 4; ++r)
 #pragma unroll
-        for (int p = 0; p < 16; ++p) v[r][p] = med3_i32(q[r][p] >> s, lo, 127);
+        for (int p = 0; p < 16; ++p) v[r][p] = requant_out(q[r][p], s, lo);
     if (LAYOUT == WINO_NCHW) {
         const bool full_cols = (4 * tx + 3 < g.w) && ((g.w & 3) == 0);
 #pragma unroll
@@ -730,6 +741,184 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
 }
 
 // ---------------------------------------------------------------------------
+// K2W wino_tap_gemm_rows_wide: the row-streamed scheme of wino_tap_gemm_rows
+// for the int8/10 operands (Q = 10: fp16 holding 10-bit integers, 32
+// channels per 64-byte k row) and a 32- or 64-bit output accumulator YT.
+// With the 64-bit epilogue the tap-resident kernel needs 144 accumulators
+// plus the int64 fold per lane and only fits 32x32 blocks of four waves;
+// here a lane keeps the six accumulators of the current row of taps and
+// 4 x 16 YT values, so a 64 (channels) x 32 (tiles) block of eight waves fits
+// (two waves per SIMD, one workgroup per CU: the ring takes 144 KB of LDS).
+//
+// Ring stage = one row a of taps and one 64-byte k row: six slices of 64 Uq +
+// 32 Vq rows (6 KB each, 36 KB); four stages rotate through 144 KB of LDS,
+// three in flight.  A stage is 36 loads of 16 rows x 64 B; wave w issues
+// loads w, w + 8, ..., w + 32 (the last wraps onto an earlier load: the same
+// bytes to the same place).  Load j covers slice j / 6 and row group j % 6
+// (groups 0-3: Uq, 4-5: Vq).
+// ---------------------------------------------------------------------------
+constexpr int KW_CO = 64;
+constexpr int KW_TL = 32;
+constexpr int KW_WAVES = (KW_CO / 16) * (KW_TL / 16);
+constexpr int KW_THREADS = 64 * KW_WAVES;
+constexpr int KW_GROUPS = (KW_CO + KW_TL) / 16;            // 16-row groups per slice
+constexpr int KW_CHUNK = (KW_CO + KW_TL) * kKStep;         // one slice
+constexpr int KW_STAGE = 6 * KW_CHUNK;
+constexpr int KW_NBUF = 4;
+constexpr int KW_LOADS = 6 * KW_GROUPS;                     // 1-KB loads per stage
+constexpr int KW_LPW = (KW_LOADS + KW_WAVES - 1) / KW_WAVES;
+static_assert(KW_NBUF * KW_STAGE <= 160 * 1024, "LDS");
+static_assert((KW_NBUF - 2) * KW_LPW <= 63, "vmcnt range");
+static_assert(kTilePad % KW_TL == 0 && kCoutPad % KW_CO == 0, "blocks tile the padded sizes");
+
+template <int LAYOUT, int Q, class YT>
+__global__ __launch_bounds__(KW_THREADS) void wino_tap_gemm_rows_wide(const int8_t* __restrict__ uq,
+                                                                        const int8_t* __restrict__ vq,
+                                                                        const int32_t* __restrict__ bias,
+                                                                        int8_t* __restrict__ y, K2Args g) {
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[KW_NBUF * KW_STAGE];
+    const int lbid = xcd_remap(blockIdx.x, g.nblocks);
+    const int bco = lbid % g.nbco, btl = lbid / g.nbco;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int cw = wave & 3, tw = wave >> 2;
+    const int co_blk = bco * KW_CO;
+    const long long tl_blk = (long long)btl * KW_TL;
+    const int lr = lane & 15, lk = lane >> 4;
+    const int nkc = g.cin_pad / kKStep;          // 64-byte k rows
+    const int nstage = 6 * nkc;
+
+    // copy side: every load advances by one k row per stage and by a row of
+    // taps (minus the k rows walked) at the end of a row of taps
+    const long long su = (long long)g.cout_pad * g.cin_pad, sv = g.t_pad * g.cin_pad;   // tap strides
+    const long long ku = (long long)g.cout_pad * kKStep, kv = g.t_pad * kKStep;           // k-row strides
+    const int rr = lane >> 2;
+    const uint32_t lane_off = (uint32_t)(rr * 64 + 16 * lds_slot(rr, lane & 3));
+    const int8_t* src[KW_LPW];
+    long long kadv[KW_LPW], radv[KW_LPW];
+    int dsto[KW_LPW];
+#pragma unroll
+    for (int i = 0; i < KW_LPW; ++i) {
+        int j = wave + KW_WAVES * i;
+        if (j >= KW_LOADS) j -= KW_WAVES;
+        const int b = j / KW_GROUPS, q = j % KW_GROUPS;
+        const bool isu = q < KW_CO / 16;
+        src[i] = isu ? uq + b * su + (long long)(co_blk + 16 * q) * kKStep
+                     : vq + b * sv + (tl_blk + 16 * (q - KW_CO / 16)) * kKStep;
+        kadv[i] = isu ? ku : kv;
+        radv[i] = (isu ? 6 * su : 6 * sv) - (long long)(nkc - 1) * kadv[i];
+        dsto[i] = b * KW_CHUNK + q * 1024;
+    }
+    int next_kc = 0, next_buf = 0;
+    auto issue_next = [&]() {
+        uint8_t* d = lds + next_buf * KW_STAGE;
+        const bool row_end = ++next_kc == nkc;
+        if (row_end) next_kc = 0;
+#pragma unroll
+        for (int i = 0; i < KW_LPW; ++i) {
+            __builtin_amdgcn_global_load_lds((const void*)(src[i] + lane_off),
+                                             (__attribute__((address_space(3))) void*)(d + dsto[i]), 16, 0, 0);
+            src[i] += row_end ? radv[i] : kadv[i];
+        }
+        next_buf = next_buf == KW_NBUF - 1 ? 0 : next_buf + 1;
+    };
+
+    // compute side
+    const int row_a = 16 * cw + lr, row_b = KW_CO + 16 * tw + lr;
+    const int frag_a = row_a * 64 + 16 * lds_slot(row_a, lk);
+    const int frag_b = row_b * 64 + 16 * lds_slot(row_b, lk);
+    const int co0 = co_blk + 16 * cw + 4 * lk;
+    const YT rnd = g.out_shift > 0 ? (YT)1 << (g.out_shift - 1) : (YT)0;
+    // loaded ahead of the ring: a load issued behind the prefetched stages
+    // would make its first use wait for all of them
+    const v4i bias4 = *(const v4i*)(bias + co0);
+
+    YT yv[4][16];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int p = 0; p < 16; ++p) yv[r][p] = 0;
+
+#pragma unroll
+    for (int st = 0; st < KW_NBUF - 1; ++st)
+        if (st < nstage) issue_next();
+    int s = 0, buf = 0;
+#pragma unroll
+    for (int a = 0; a < 6; ++a) {
+        v4i m[6];
+        auto stage = [&](bool first) {
+            // stage s has landed once only the stages issued after it are
+            // pending: min(NBUF - 2, nstage - 1 - s) of them
+            const int ahead = min(KW_NBUF - 2, nstage - 1 - s);
+            if (ahead >= 2)
+                WINO_WAIT_VM_LDS(2 * KW_LPW);
+            else if (ahead == 1)
+                WINO_WAIT_VM_LDS(KW_LPW);
+            else
+                WINO_WAIT_VM_LDS(0);
+            ring_barrier();   // stage s visible; stage s-1 (the buffer refilled next) consumed
+            if (s + KW_NBUF - 1 < nstage) issue_next();
+            const uint8_t* base = lds + buf * KW_STAGE;
+            buf = buf == KW_NBUF - 1 ? 0 : buf + 1;
+            ++s;
+            v4i fa[2], fb[2];
+            auto frag = [&](int b) {
+                fa[b & 1] = *(const v4i*)(base + b * KW_CHUNK + frag_a);
+                fb[b & 1] = *(const v4i*)(base + b * KW_CHUNK + frag_b);
+            };
+            frag(0);
+            frag(1);
+            const v4i zero = (v4i){0, 0, 0, 0};
+#pragma unroll
+            for (int b = 0; b < 6; ++b) {
+                if constexpr (Q == 10) {
+                    // fp16 10-bit integers: 32 products and their sums are
+                    // integers below 2^24, exact in fp32
+                    const v4f r = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                        __builtin_bit_cast(v8h, fa[b & 1]), __builtin_bit_cast(v8h, fb[b & 1]),
+                        (v4f){0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                    const v4i ri = __builtin_convertvector(r, v4i);
+                    m[b] = first ? ri
+                                 : __builtin_bit_cast(v4i, __builtin_bit_cast(v4u, m[b]) + __builtin_bit_cast(v4u, ri));
+                } else {
+                    m[b] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[b & 1], fb[b & 1], first ? zero : m[b], 0, 0, 0);
+                }
+                if (b + 2 < 6) frag(b + 2);
+            }
+        };
+        stage(true);
+        for (int kc = 1; kc < nkc; ++kc) stage(false);
+
+        // fold row a: z = (M'[a, :]) A, then Y += A^T[:, a] z, in YT
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            YT mv[6], z[4];
+#pragma unroll
+            for (int b = 0; b < 6; ++b) mv[b] = (YT)m[b][r] << g.tab.sh[6 * a + b];
+            if (a == 1) mv[1] += (YT)bias4[r] + rnd;      // tap (1, 1): bias and rounding constant
+            at_1d(mv, z);
+            YT* yr = yv[r];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                // column a of A^T: 1 1 1 1 1 0 / 0 1 -1 2 -2 0 / 0 1 1 4 4 0 / 0 1 -1 8 -8 1
+                if (a < 5) yr[j] += z[j];
+                if (a == 1) { yr[4 + j] += z[j]; yr[8 + j] += z[j]; yr[12 + j] += z[j]; }
+                if (a == 2) { yr[4 + j] -= z[j]; yr[8 + j] += z[j]; yr[12 + j] -= z[j]; }
+                if (a == 3) { yr[4 + j] += z[j] << 1; yr[8 + j] += z[j] << 2; yr[12 + j] += z[j] << 3; }
+                if (a == 4) { yr[4 + j] -= z[j] << 1; yr[8 + j] += z[j] << 2; yr[12 + j] -= z[j] << 3; }
+                if (a == 5) yr[12 + j] += z[j];
+            }
+        }
+        // keep the folds here (the compiler would sink them past later rows)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int p = 0; p < 16; ++p) asm volatile("" : "+v"(yv[r][p]));
+    }
+    store_tile<LAYOUT>(yv, g, y, co0, tl_blk + 16 * tw + lr);
+}
+
+// ---------------------------------------------------------------------------
 // host-side helpers
 // ---------------------------------------------------------------------------
 // compute units of the current device (the launch heuristics use it),
@@ -840,13 +1029,15 @@ long long resident_blocks(const wino_f4_plan_s* p, const Geometry& g) {
 // Calibration and debug exports (MODE 1, 2) always use the 64x32 shape.
 int tap_kernel_for(const wino_f4_plan_s* p, const Geometry& g, int mode) {
     const int k = p->tap_kernel;
-    // int8/10 (fp16 operands): a forced resident shape (16X16 stands for the
-    // 32x32 shape with 6-tap stages), else 64x32, or 32x32 with the 64-bit
-    // epilogue
+    // int8/10 (fp16 operands): the row-streamed 64x32 kernel by default; a
+    // forced resident shape (16X16 stands for the 32x32 shape with 6-tap
+    // stages), or RESIDENT: 64x32, 32x32 with the 64-bit epilogue (its only
+    // resident shape without spills), as for calibration and exports
     if (p->bits == 10 && p->m == 4) {
         if (mode == 0 && (k == WINO_TAP_RESIDENT_64X32 || k == WINO_TAP_RESIDENT_32X32 ||
                           k == WINO_TAP_RESIDENT_16X16))
             return k;
+        if (mode == 0 && k != WINO_TAP_RESIDENT) return WINO_TAP_ROWS;
         return p->epi_bits == 64 ? WINO_TAP_RESIDENT_32X32 : WINO_TAP_RESIDENT_64X32;
     }
     // F2: its own 64x32 configuration
@@ -880,6 +1071,26 @@ wino_status launch_resident(const wino_f4_plan_s* p, const Geometry& g, wino_lay
     return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
 }
 
+// the row-streamed kernel for int8/10 operands, with the plan's epilogue width
+wino_status launch_rows_wide(const wino_f4_plan_s* p, const Geometry& g, wino_layout layout, const int8_t* vq,
+                             int8_t* y, K2Args a, hipStream_t stream) {
+    const long long blocks = (long long)(p->cout_pad / KW_CO) * (g.t_pad / KW_TL);
+    if (blocks > 0x7fffffffll) return WINO_EUNSUPPORTED;
+    a.nbco = p->cout_pad / KW_CO;
+    a.nblocks = (int)blocks;
+    a.cin_pad = p->cin_pad * kbytes_per_channel(10);
+    dim3 grid((unsigned)blocks), block(KW_THREADS);
+#define KW_LAUNCH(L, T) \
+    hipLaunchKernelGGL((wino_tap_gemm_rows_wide<L, 10, T>), grid, block, 0, stream, p->uq_dev, vq, p->bias_dev, y, a)
+    if (layout == WINO_NHWC) {
+        if (p->epi_bits == 32) KW_LAUNCH(WINO_NHWC, int); else KW_LAUNCH(WINO_NHWC, long long);
+    } else {
+        if (p->epi_bits == 32) KW_LAUNCH(WINO_NCHW, int); else KW_LAUNCH(WINO_NCHW, long long);
+    }
+#undef KW_LAUNCH
+    return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
+}
+
 template <int MODE>
 wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout layout, const int8_t* vq,
                       int8_t* y, void* aux, hipStream_t stream) {
@@ -904,6 +1115,9 @@ wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout la
     if (p->bits == 10) {
         if (p->m == 2) return launch_resident<K2F2_10, 2, MODE, 10>(p, g, layout, vq, y, aux, a, stream);
         switch (tap_kernel_for(p, g, MODE)) {
+            case WINO_TAP_ROWS:
+                if constexpr (MODE == 0) return launch_rows_wide(p, g, layout, vq, y, a, stream);
+                break;
             case WINO_TAP_RESIDENT_64X32:
                 return launch_resident<K2Big10, 4, MODE, 10>(p, g, layout, vq, y, aux, a, stream);
             case WINO_TAP_RESIDENT_16X16:

@@ -165,20 +165,21 @@ def test_i10_unsupported_and_rejected_calls():
 
 
 def test_i10_tap_kernel_choice_and_forced_shapes():
-    """int8/10 runs the tap-resident kernel with fp16 operands: 64x32 by
-    default, 32x32 with the 64-bit epilogue; a forced resident shape is
-    honoured (16X16 stands for 32x32 blocks with 6-tap stages), ROWS is not
-    (int8 only); every choice is exact."""
+    """int8/10 runs the row-streamed kernel with fp16 operands by default,
+    with either epilogue width; RESIDENT picks the tap-resident 64x32 shape,
+    or 32x32 with the 64-bit epilogue; a forced resident shape is honoured
+    (16X16 stands for 32x32 blocks with 6-tap stages); every choice is
+    exact.  Two k rows, 100 tiles in four blocks with a ragged last one."""
     n, cin, cout, h, w = 1, 64, 64, 40, 40
     x, f, b = workloads.random_case(59, n, cin, cout, h, w, signed=True)
-    for eb, default in (([0] * 36, W.TAP_RESIDENT_64X32),
-                        ([15 if t % 3 == 0 else 0 for t in range(36)], W.TAP_RESIDENT_32X32)):
-        f2 = f * (0.05 if default == W.TAP_RESIDENT_64X32 else 1.0)
+    for eb, resident in (([0] * 36, W.TAP_RESIDENT_64X32),
+                         ([15 if t % 3 == 0 else 0 for t in range(36)], W.TAP_RESIDENT_32X32)):
+        f2 = f * (0.05 if resident == W.TAP_RESIDENT_64X32 else 1.0)
         gp = W.wino_f4_plan_i10(f2, eb, bias=b, out_shift=14)
-        assert W.wino_f4_plan_info(gp)["epilogue_bits"] == (32 if default == W.TAP_RESIDENT_64X32 else 64)
+        assert W.wino_f4_plan_info(gp)["epilogue_bits"] == (32 if resident == W.TAP_RESIDENT_64X32 else 64)
         op = _oplan(4, f2, eb, bias=b, out_shift=14)
         ref = tapwise.conv_int8(x, op)
-        for forced, want in ((W.TAP_AUTO, default), (W.TAP_ROWS, default), (W.TAP_RESIDENT, default),
+        for forced, want in ((W.TAP_AUTO, W.TAP_ROWS), (W.TAP_ROWS, W.TAP_ROWS), (W.TAP_RESIDENT, resident),
                              (W.TAP_RESIDENT_64X32, W.TAP_RESIDENT_64X32),
                              (W.TAP_RESIDENT_32X32, W.TAP_RESIDENT_32X32),
                              (W.TAP_RESIDENT_16X16, W.TAP_RESIDENT_16X16)):
