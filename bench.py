@@ -248,7 +248,9 @@ def main():
     rows = W.wino_f4_tap_kernel_choice(plan, n, h, w) == W.TAP_ROWS
     # kernel names as the profiler shows them (template arguments included;
     # the tap-resident kernel's block configuration is a class argument)
-    k1_name, k1_inst = "wino_input_xform", f"wino_input_xform<{mt},{lay},0,{args.bits},16>"
+    # the one-instruction requantization serves plans whose e_B are all <= 16 - bits
+    k1_sat = "true" if all(0 <= e <= 16 - args.bits for e in eb) else "false"
+    k1_name, k1_inst = "wino_input_xform", f"wino_input_xform<{mt},{lay},0,{args.bits},16,{k1_sat}>"
     if rows and args.bits == 10:
         k2_name = "wino_tap_gemm_rows_wide"
         k2_inst = f"wino_tap_gemm_rows_wide<{lay},10,{'int' if info['epilogue_bits'] == 32 else 'longlong'}>"

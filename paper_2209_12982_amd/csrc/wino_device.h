@@ -107,6 +107,32 @@ __device__ __forceinline__ uint2 requant10_pack(v2s ev, v2s od, int e, uint32_t 
     return make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
 }
 
+// R(v / 2^e) clamped to Q bits with one instruction per pair of lanes, for
+// e <= 16 - Q: x = v * 2^(16-Q-e) + 2^(15-Q) (the rounding constant 2^(e-1)
+// scaled alike; 0 for e = 0) is formed at full width and saturated to int16
+// by v_pk_mad_i16's clamp, and x >> (16 - Q) = floor((v + 2^(e-1)) / 2^e)
+// clamped to [-2^(Q-1), 2^(Q-1) - 1] (for Q = 8: the high byte of each lane).
+// scale2 / add2: 2^(16-Q-e) and the scaled rounding constant in both halves.
+// (s: a wave-uniform multiplier, read from a scalar register)
+__device__ __forceinline__ uint32_t pk_mad_sat(uint32_t a, uint32_t s, uint32_t c) {
+    uint32_t r;
+    asm("v_pk_mad_i16 %0, %1, %2, %3 clamp" : "=v"(r) : "v"(a), "s"(s), "v"(c));
+    return r;
+}
+__device__ __forceinline__ uint32_t requant_pack_sat(v2s ev, v2s od, uint32_t scale2, uint32_t add2) {
+    const uint32_t a = pk_mad_sat(__builtin_bit_cast(uint32_t, ev), scale2, add2);
+    const uint32_t b = pk_mad_sat(__builtin_bit_cast(uint32_t, od), scale2, add2);
+    // high bytes: ch0 = a.lo, ch1 = b.lo, ch2 = a.hi, ch3 = b.hi
+    return __builtin_amdgcn_perm(b, a, 0x07030501u);
+}
+__device__ __forceinline__ uint2 requant10_pack_sat(v2s ev, v2s od, uint32_t scale2, uint32_t add2) {
+    const v2s a = __builtin_bit_cast(v2s, pk_mad_sat(__builtin_bit_cast(uint32_t, ev), scale2, add2)) >> splat(6);
+    const v2s b = __builtin_bit_cast(v2s, pk_mad_sat(__builtin_bit_cast(uint32_t, od), scale2, add2)) >> splat(6);
+    const v2h lo = {(_Float16)a.x, (_Float16)b.x};
+    const v2h hi = {(_Float16)a.y, (_Float16)b.y};
+    return make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+}
+
 // median of three (clamp a to [lo, hi]) in one instruction
 __device__ __forceinline__ int med3_i32(int a, int lo, int hi) {
     int r;

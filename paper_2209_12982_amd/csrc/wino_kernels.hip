@@ -56,7 +56,51 @@ struct K1Args {
     long long plane_bytes;              // bytes of one tap plane of Vq
     TapTables tab;
     uint32_t rnd2[kTaps];               // 2^(e_B - 1) (0 for e_B = 0) in both 16-bit halves
+    int q_sat;                          // every e_B <= 16 - Q: one-instruction requantization
 };
+
+// Requantize the tile's taps and store them to the tap planes of Vq at byte
+// offset off (see the kernel); SAT: the one-instruction saturating form.
+// The saturating form takes 2^(16-Q-e) (a scalar per tap) and 2^(15-Q) as
+// the addend for every tap: for e = 0 that adds half a unit below the kept
+// bits, which leaves the floor of an integer unchanged.
+template <int N, int Q, bool SAT>
+__device__ __forceinline__ void k1_store(const v2s (&ev)[N][N], const v2s (&od)[N][N], const K1Args& g,
+                                         int8_t* __restrict__ vq, long long off) {
+    constexpr int NT = N * N;
+    constexpr uint32_t kAdd2 = (1u << (15 - Q)) * 0x10001u;
+    auto scale2 = [&](int t) { return (1u << (16 - Q - g.tab.eb[t])) * 0x10001u; };
+    if (g.vq_buf) {
+        // per tap a buffer resource on the tap plane (scalar base and size)
+        // and one 32-bit lane offset for all taps
+        const int voff = (int)off;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const __amdgpu_buffer_rsrc_t rs =
+                __builtin_amdgcn_make_buffer_rsrc(vq + t * g.plane_bytes, 0, (int)g.plane_bytes, 0x00020000);
+            if constexpr (Q == 10) {
+                const uint2 v = SAT ? requant10_pack_sat(ev[t / N][t % N], od[t / N][t % N], scale2(t), kAdd2)
+                                    : requant10_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t], g.rnd2[t]);
+                __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u, v), rs, voff, 0, 0);
+            } else {
+                const uint32_t v = SAT ? requant_pack_sat(ev[t / N][t % N], od[t / N][t % N], scale2(t), kAdd2)
+                                       : requant_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t], g.rnd2[t]);
+                __builtin_amdgcn_raw_buffer_store_b32(v, rs, voff, 0, 0);
+            }
+        }
+    } else {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            int8_t* dst = vq + t * g.plane_bytes + off;
+            if constexpr (Q == 10)
+                *(uint2*)dst = SAT ? requant10_pack_sat(ev[t / N][t % N], od[t / N][t % N], scale2(t), kAdd2)
+                                   : requant10_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t], g.rnd2[t]);
+            else
+                *(uint32_t*)dst = SAT ? requant_pack_sat(ev[t / N][t % N], od[t / N][t % N], scale2(t), kAdd2)
+                                      : requant_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t], g.rnd2[t]);
+        }
+    }
+}
 
 // Stage the halo band of one block into LDS as [row][col][channel] bytes
 // (channel fastest, K1_CS words per pixel).  Rows M ty - 1 .. M ty + M,
@@ -104,7 +148,10 @@ __device__ __forceinline__ void k1_stage_band(uint32_t* lds, const int8_t* __res
 // MODE 0: write Vq.  MODE 1: per-tap max |V| into tapmax[NTAP] (calibration).
 // Q: Winograd-domain width, 8 (int8 Vq) or 10 (int8/10: fp16 Vq holding
 // 10-bit integers, [ntap][cin_pad/32][t_pad][32]).
-template <int M, int LAYOUT, int MODE, int Q = 8, int TX = K1_TX>
+// SAT: requantize with the one-instruction saturating form (every e_B <=
+// 16 - Q), a kernel of its own so the other form's per-tap constants are not
+// held in scalar registers too.
+template <int M, int LAYOUT, int MODE, int Q = 8, int TX = K1_TX, bool SAT = false>
 __global__ __launch_bounds__(16 * TX, 5) void wino_input_xform(const int8_t* __restrict__ x,
                                                                int8_t* __restrict__ vq,
                                                                int* __restrict__ tapmax, K1Args g) {
@@ -152,32 +199,7 @@ __global__ __launch_bounds__(16 * TX, 5) void wino_input_xform(const int8_t* __r
         //           8 bytes (4 halves)
         const long long off = Q == 10 ? (((long long)(2 * cgi + (q >> 3)) * g.t_pad + tile) * 32 + 4 * (q & 7)) * 2
                                       : ((long long)cgi * g.t_pad + tile) * K1_CG + 4 * q;
-        if (g.vq_buf) {
-            // per tap a buffer resource on the tap plane (scalar base and
-            // size) and one 32-bit lane offset for all taps
-            const int voff = (int)off;
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                const __amdgpu_buffer_rsrc_t rs =
-                    __builtin_amdgcn_make_buffer_rsrc(vq + t * g.plane_bytes, 0, (int)g.plane_bytes, 0x00020000);
-                if constexpr (Q == 10) {
-                    const uint2 v = requant10_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t], g.rnd2[t]);
-                    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u, v), rs, voff, 0, 0);
-                } else {
-                    __builtin_amdgcn_raw_buffer_store_b32(
-                        requant_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t], g.rnd2[t]), rs, voff, 0, 0);
-                }
-            }
-        } else {
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                int8_t* dst = vq + t * g.plane_bytes + off;
-                if constexpr (Q == 10)
-                    *(uint2*)dst = requant10_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t], g.rnd2[t]);
-                else
-                    *(uint32_t*)dst = requant_pack(ev[t / N][t % N], od[t / N][t % N], g.tab.eb[t], g.rnd2[t]);
-            }
-        }
+        k1_store<N, Q, SAT>(ev, od, g, vq, off);
     } else {
         if (valid) {
 #pragma unroll
@@ -984,6 +1006,10 @@ K1Args k1_args(const Geometry& g, int cin, int cin_pad, const TapTables& tab, in
         const uint32_t r = e > 0 ? (1u << (e - 1)) : 0u;
         a.rnd2[t] = r | (r << 16);
     }
+    // the saturating requantization needs 0 <= e_B <= 16 - bits for every tap
+    a.q_sat = 1;
+    for (int t = 0; t < kTaps; ++t)
+        if (tab.eb[t] < 0 || tab.eb[t] > 16 - bits) a.q_sat = 0;
     a.plane_bytes = g.t_pad * cin_pad * kbytes_per_channel(bits);
     a.vq_buf = a.plane_bytes < 0x7fffffffLL;
     a.x_vec = 0;
@@ -999,12 +1025,16 @@ wino_status launch_k1_tx(const K1Args& a, wino_layout layout, const int8_t* x, i
     if (blocks == 0) return WINO_OK;
     if (blocks > 0x7fffffffll) return WINO_EUNSUPPORTED;
     args.x_vec = (a.cin % 16 == 0) && (((uintptr_t)x & 15) == 0);
-    if (layout == WINO_NHWC)
-        hipLaunchKernelGGL((wino_input_xform<M, WINO_NHWC, MODE, Q, TX>), dim3((unsigned)blocks), dim3(16 * TX), 0,
-                           stream, x, vq, tapmax, args);
-    else
-        hipLaunchKernelGGL((wino_input_xform<M, WINO_NCHW, MODE, Q, TX>), dim3((unsigned)blocks), dim3(16 * TX), 0,
-                           stream, x, vq, tapmax, args);
+#define K1_LAUNCH(L, S)                                                                                      \
+    hipLaunchKernelGGL((wino_input_xform<M, L, MODE, Q, TX, S>), dim3((unsigned)blocks), dim3(16 * TX), 0, stream, \
+                       x, vq, tapmax, args)
+    const bool sat = MODE == 0 && a.q_sat;
+    if (layout == WINO_NHWC) {
+        if (sat) K1_LAUNCH(WINO_NHWC, MODE == 0); else K1_LAUNCH(WINO_NHWC, false);
+    } else {
+        if (sat) K1_LAUNCH(WINO_NCHW, MODE == 0); else K1_LAUNCH(WINO_NCHW, false);
+    }
+#undef K1_LAUNCH
     return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
 }
 
@@ -1285,7 +1315,7 @@ static wino_status calibrate_input(int m, int bits, const int8_t* x, int32_t n, 
                                stream) == WINO_OK;
         if (ok) ok = hipMemcpyAsync(host, dmax, sizeof(int) * kTaps, hipMemcpyDeviceToHost, stream) == hipSuccess;
         if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
-        hipFree(dmax);
+        (void)hipFree(dmax);
         if (!ok) return WINO_EHIP;
     }
     for (int t = 0; t < ntap; ++t) {
@@ -1339,7 +1369,7 @@ extern "C" wino_status wino_f4_calibrate_output(wino_f4_plan_t p, const int8_t* 
         if (ok) ok = launch_k2<1>(p, g, layout, (const int8_t*)ws, nullptr, dmax, stream) == WINO_OK;
         if (ok) ok = hipMemcpyAsync(&host, dmax, sizeof(host), hipMemcpyDeviceToHost, stream) == hipSuccess;
         if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
-        hipFree(dmax);
+        (void)hipFree(dmax);
         if (!ok) return WINO_EHIP;
     }
     if (zmax) *zmax = (int64_t)host;
