@@ -250,7 +250,11 @@ def main():
     # the tap-resident kernel's block configuration is a class argument)
     # the one-instruction requantization serves plans whose e_B are all <= 16 - bits
     k1_sat = "true" if all(0 <= e <= 16 - args.bits for e in eb) else "false"
-    k1_name, k1_inst = "wino_input_xform", f"wino_input_xform<{mt},{lay},0,{args.bits},16,{k1_sat}>"
+    if layout == W.NHWC and cin % 4 == 0:
+        # NHWC with whole 4-channel words: the transform reads global memory directly
+        k1_name, k1_inst = "wino_input_xform_nhwc", f"wino_input_xform_nhwc<{mt},{args.bits},16,{k1_sat}>"
+    else:
+        k1_name, k1_inst = "wino_input_xform", f"wino_input_xform<{mt},{lay},0,{args.bits},16,{k1_sat}>"
     if rows and args.bits == 10:
         k2_name = "wino_tap_gemm_rows_wide"
         k2_inst = f"wino_tap_gemm_rows_wide<{lay},10,{'int' if info['epilogue_bits'] == 32 else 'longlong'}>"

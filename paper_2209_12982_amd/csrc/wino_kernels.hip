@@ -216,6 +216,58 @@ __global__ __launch_bounds__(16 * TX, 5) void wino_input_xform(const int8_t* __r
     }
 }
 
+// K1 for NHWC input without the LDS band: each thread reads its tile's
+// (M+2) x (M+2) pixels x 4 channels straight from global memory (L1 and L2
+// serve the halo that neighbouring tiles share).  Row r of the patch goes
+// through a buffer resource on that image row (num_records: the row's bytes,
+// 0 above or below the image) and column c through a per-lane offset (past
+// the row's end left or right of the image, for idle tiles and for channels
+// >= Cin), so pixels outside the image read as zero with no arithmetic per
+// load.  No LDS and no barrier: one wave's loads overlap other waves'
+// arithmetic.  Needs Cin % 4 == 0 (whole 4-channel words), a 4-byte aligned
+// x and image rows below 2 GiB.
+template <int M, int Q, int TX, bool SAT>
+__global__ __launch_bounds__(16 * TX, 5) void wino_input_xform_nhwc(const int8_t* __restrict__ x,
+                                                                    int8_t* __restrict__ vq, K1Args g) {
+    constexpr int N = Wino<M>::N;
+    // the block order of wino_input_xform
+    int bid = xcd_remap((int)blockIdx.x, (int)gridDim.x);
+    const int cgi = bid % g.ncg;
+    bid /= g.ncg;
+    const int txb = bid % g.ntxb;
+    const int row = bid / g.ntxb;         // img * th + ty
+    const int img = row / g.th, ty = row - img * g.th;
+    const int q = threadIdx.x & 15, j = threadIdx.x >> 4;
+    const int tx = txb * TX + j;
+    const int ci = cgi * K1_CG + 4 * q;
+    const bool lane_ok = tx < g.tw && ci < g.cin;
+    const int row_bytes = g.w * g.cin;
+    constexpr int kOut = 0x7ffffff0;      // >= any row's num_records
+    int coff[N];
+#pragma unroll
+    for (int c = 0; c < N; ++c) {
+        const int xx = M * tx - 1 + c;
+        coff[c] = (lane_ok && xx >= 0 && xx < g.w) ? xx * g.cin + ci : kOut;
+    }
+    uint32_t wv[N][N];
+#pragma unroll
+    for (int r = 0; r < N; ++r) {
+        const int yy = M * ty - 1 + r;
+        const bool rok = yy >= 0 && yy < g.h;
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(x + (rok ? ((long long)img * g.h + yy) * row_bytes : 0)), 0, rok ? row_bytes : 0, 0x00020000);
+#pragma unroll
+        for (int c = 0; c < N; ++c) wv[r][c] = __builtin_amdgcn_raw_buffer_load_b32(rs, coff[c], 0, 0);
+    }
+    v2s ev[N][N], od[N][N];
+    input_tile_transform<M>(wv, ev, od);
+    if (tx >= g.tw) return;
+    const long long tile = (long long)row * g.tw + tx;
+    const long long off = Q == 10 ? (((long long)(2 * cgi + (q >> 3)) * g.t_pad + tile) * 32 + 4 * (q & 7)) * 2
+                                  : ((long long)cgi * g.t_pad + tile) * K1_CG + 4 * q;
+    k1_store<N, Q, SAT>(ev, od, g, vq, off);
+}
+
 // ---------------------------------------------------------------------------
 // K2: tap GEMM with fused output transform
 // ---------------------------------------------------------------------------
@@ -1029,6 +1081,17 @@ wino_status launch_k1_tx(const K1Args& a, wino_layout layout, const int8_t* x, i
     hipLaunchKernelGGL((wino_input_xform<M, L, MODE, Q, TX, S>), dim3((unsigned)blocks), dim3(16 * TX), 0, stream, \
                        x, vq, tapmax, args)
     const bool sat = MODE == 0 && a.q_sat;
+    if constexpr (MODE == 0) {
+        if (layout == WINO_NHWC && a.cin % 4 == 0 && ((uintptr_t)x & 3) == 0 && (long long)a.w * a.cin < 0x7ffffff0ll) {
+            if (sat)
+                hipLaunchKernelGGL((wino_input_xform_nhwc<M, Q, TX, true>), dim3((unsigned)blocks), dim3(16 * TX), 0,
+                                   stream, x, vq, args);
+            else
+                hipLaunchKernelGGL((wino_input_xform_nhwc<M, Q, TX, false>), dim3((unsigned)blocks), dim3(16 * TX), 0,
+                                   stream, x, vq, args);
+            return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
+        }
+    }
     if (layout == WINO_NHWC) {
         if (sat) K1_LAUNCH(WINO_NHWC, MODE == 0); else K1_LAUNCH(WINO_NHWC, false);
     } else {
