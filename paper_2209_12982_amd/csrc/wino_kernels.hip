@@ -226,8 +226,11 @@ __global__ __launch_bounds__(16 * TX, 5) void wino_input_xform(const int8_t* __r
 // load.  No LDS and no barrier: one wave's loads overlap other waves'
 // arithmetic.  Needs Cin % 4 == 0 (whole 4-channel words), a 4-byte aligned
 // x and image rows below 2 GiB.
+// TX = 16 or 8 tiles per block (256 or 128 threads), 20 waves per CU either
+// way; the launch takes the width that leaves fewer idle tiles at the end of
+// a tile row (C5's rows of 40 tiles: 8, measured 16.6 -> 15.0 us).
 template <int M, int Q, int TX, bool SAT>
-__global__ __launch_bounds__(16 * TX, 5) void wino_input_xform_nhwc(const int8_t* __restrict__ x,
+__global__ __launch_bounds__(16 * TX, 80 / TX) void wino_input_xform_nhwc(const int8_t* __restrict__ x,
                                                                     int8_t* __restrict__ vq, K1Args g) {
     constexpr int N = Wino<M>::N;
     // the block order of wino_input_xform
@@ -1068,6 +1071,13 @@ K1Args k1_args(const Geometry& g, int cin, int cin_pad, const TapTables& tab, in
     return a;
 }
 
+// tiles per block of the direct NHWC transform: 8 when that leaves fewer
+// idle tiles at the end of a row of tw tiles than 16 does
+int k1_direct_tx(int tw) {
+    const int idle16 = (tw + 15) / 16 * 16 - tw, idle8 = (tw + 7) / 8 * 8 - tw;
+    return idle8 < idle16 ? 8 : 16;
+}
+
 template <int M, int MODE, int Q, int TX>
 wino_status launch_k1_tx(const K1Args& a, wino_layout layout, const int8_t* x, int8_t* vq, int* tapmax,
                          hipStream_t stream) {
@@ -1083,12 +1093,18 @@ wino_status launch_k1_tx(const K1Args& a, wino_layout layout, const int8_t* x, i
     const bool sat = MODE == 0 && a.q_sat;
     if constexpr (MODE == 0) {
         if (layout == WINO_NHWC && a.cin % 4 == 0 && ((uintptr_t)x & 3) == 0 && (long long)a.w * a.cin < 0x7ffffff0ll) {
-            if (sat)
-                hipLaunchKernelGGL((wino_input_xform_nhwc<M, Q, TX, true>), dim3((unsigned)blocks), dim3(16 * TX), 0,
-                                   stream, x, vq, args);
-            else
-                hipLaunchKernelGGL((wino_input_xform_nhwc<M, Q, TX, false>), dim3((unsigned)blocks), dim3(16 * TX), 0,
-                                   stream, x, vq, args);
+            const int tx = k1_direct_tx(a.tw);
+            args.ntxb = (a.tw + tx - 1) / tx;
+            const long long nb = (long long)args.ntxb * a.ncg * a.n * a.th;
+            if (nb > 0x7fffffffll) return WINO_EUNSUPPORTED;
+#define K1D_LAUNCH(T, S)                                                                                            \
+    hipLaunchKernelGGL((wino_input_xform_nhwc<M, Q, T, S>), dim3((unsigned)nb), dim3(16 * T), 0, stream, x, vq, args)
+            if (tx == 8) {
+                if (sat) K1D_LAUNCH(8, true); else K1D_LAUNCH(8, false);
+            } else {
+                if (sat) K1D_LAUNCH(16, true); else K1D_LAUNCH(16, false);
+            }
+#undef K1D_LAUNCH
             return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
         }
     }
