@@ -49,6 +49,37 @@ def test_input_transform_bitexact(shape, layout):
     assert (vq.cpu().numpy() == ref).all()
 
 
+# NHWC input-transform kernels: the direct kernel with 16-tile blocks (rows of
+# 16 and 32 tiles, ragged image edges, several blocks per row) and 8-tile
+# blocks, Cin % 4 == 0 but not % 16, and Cin % 4 != 0 (the LDS-band kernel)
+K1_SHAPES = [
+    # n, cin, h, w
+    (1, 64, 9, 64),       # 16 tiles per row: one 16-tile block, ragged rows
+    (2, 72, 5, 125),      # 32 tiles per row, last column ragged: two 16-tile blocks
+    (1, 12, 7, 37),       # 10 tiles per row: 8-tile blocks, Cin % 16 != 0
+    (1, 130, 6, 70),      # 18 tiles per row, Cin % 4 != 0: the LDS-band kernel
+    (3, 4, 3, 3),         # one tile, four channels
+]
+
+
+@pytest.mark.parametrize("m", [4, 2])
+@pytest.mark.parametrize("shape", K1_SHAPES)
+def test_input_transform_nhwc_block_widths(shape, m):
+    torch = torch_dev()
+    n, cin, h, w = shape
+    x, f, b = workloads.random_case(11, n, cin, 8, h, w, signed=True)
+    ntap = (m + 2) ** 2
+    eb = [int(v) for v in np.random.default_rng(12).integers(0, 9, ntap)]
+    gp = (W.wino_f4_plan if m == 4 else W.wino_f2_plan)(f, eb, bias=b)
+    ws = workspace(gp, n, h, w)
+    th, tw = tapwise.tile_grid(h, w, m)
+    vq = torch.empty((ntap, n * th * tw, cin), dtype=torch.int8, device="cuda")
+    W.wino_f4_debug_input_transform(gp, to_device(x, W.NHWC), n, h, w, W.NHWC, vq, ws)
+    torch.cuda.synchronize()
+    ref = tapwise.input_taps_quantized(x, eb, m=m)
+    assert (vq.cpu().numpy() == ref).all()
+
+
 @pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("shape", SHAPES)
 def test_tap_gemm_bitexact(shape, layout):
