@@ -122,6 +122,25 @@ def time_calls(torch, fn, calls):
     return q(0.5), q(0.1), q(0.9)
 
 
+def time_cold(torch, fn, calls, flush):
+    """Per-call GPU duration with the device caches flushed before each call:
+    a 1 GiB buffer is read between calls (a sum over it), which evicts the
+    call's inputs from L2 and from the 256 MB Infinity Cache (MALL) and
+    leaves clean lines there, so the call reads its inputs from HBM and
+    pays no write-back of someone else's data.  Returns (median, p10, p90) ms."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(calls)]
+    torch.cuda.synchronize()
+    for s, e in ev:
+        flush.sum()
+        s.record()
+        fn()
+        e.record()
+    torch.cuda.synchronize()
+    t = sorted(s.elapsed_time(e) for s, e in ev)
+    q = lambda f: t[min(len(t) - 1, int(f * (len(t) - 1) + 0.5))]
+    return q(0.5), q(0.1), q(0.9)
+
+
 def kernel_ms(torch, fn, calls):
     """A single-kernel call's duration: the smaller of the back-to-back loop
     average (exact for long kernels, host-bound for short ones) and the
@@ -272,6 +291,15 @@ def main():
         k1_ms, k1_p10, k1_p90 = kernel_ms(torch, k1, args.steps)
         k2_ms, k2_p10, k2_p90 = kernel_ms(torch, k2, args.steps)
 
+    # cold: every call starts with its inputs in HBM only (caches flushed)
+    flush = torch.ones(1 << 27, dtype=torch.int64, device="cuda")
+    ncold = max(5, min(20, args.steps))
+    cold = {"step_ms": time_cold(torch, step, ncold, flush)[0]}
+    if variant == W.SPLIT:
+        cold["kernels_ms"] = {k1_name: time_cold(torch, k1, ncold, flush)[0],
+                              k2_name: time_cold(torch, k2, ncold, flush)[0]}
+    del flush
+
     direct_ops = 2.0 * 9 * n * h * w * cin * cout
     tap_ops = 2.0 * ntap * T * cin * cout
     # the int8/10 tap GEMM multiplies exact 10-bit integers on fp16 matrix cores
@@ -292,6 +320,9 @@ def main():
                             "frac": tap_ops / (k2_ms * 1e-3) / 1e12 / k2_peak,
                             "GB/s_algorithmic": k2_bytes / (k2_ms * 1e-3) / 1e9,
                             "traffic_bytes": counter_traffic(cfg_tag, args.layout, k2_inst, args.transform)}
+        kernels[k1_name]["cold_ms"] = cold["kernels_ms"][k1_name]
+        kernels[k1_name]["cold_GB/s"] = k1_bytes / (cold["kernels_ms"][k1_name] * 1e-3) / 1e9
+        kernels[k2_name]["cold_ms"] = cold["kernels_ms"][k2_name]
         if k2_ms >= k1_ms:
             roofline = {"kernel": k2_name, "bound": "mfma", "achieved": kernels[k2_name]["TOP/s"],
                         "peak": k2_peak, "unit": k2_unit, "frac": kernels[k2_name]["frac"],
@@ -348,6 +379,8 @@ def main():
         "roofline": roofline,
         "kernels": kernels,
         "tap_gemm_mfma_frac_of_step": tap_ops / (ms * 1e-3) / 1e12 / k2_peak,
+        "cold": {"step_ms": cold["step_ms"], "TOPS": direct_ops / (cold["step_ms"] * 1e-3) / 1e12,
+                 "calls": ncold, "flush": "1 GiB read before each call (L2 and MALL evicted, clean)"},
         "direct_conv": direct,
         "cpu_baseline": cpu,
         "plan_ms": plan_ms,
