@@ -410,6 +410,26 @@ wino_status direct_conv_int8(const int8_t* x, const int8_t* w_ohwi, const int32_
                              wino_layout layout, int32_t out_shift, int32_t relu,
                              hipStream_t stream);
 
+/*
+ * wino_f4_conv_float -- the unquantized Winograd F(4x4, 3x3) convolution of
+ * Eq. (winograd), Sec. II, evaluated in fp32: V = B^T d B, U = G f G^T,
+ * M = sum_ci V (.) U, Y = A^T M A, every intermediate an fp32 value, no
+ * tap-wise quantization, no bias, no requantization.  It is the real-valued
+ * convolution the integer pipeline approximates, kept as a reference stage
+ * whose floating-point intermediates a test can hold to a relative
+ * tolerance; it is not on the hot path.
+ *   x       device int8, NCHW [n][cin][h][w] or NHWC [n][h][w][cin]
+ *   w_oihw  device fp32 [cout][cin][3][3]
+ *   y       device fp32, same layout as x with cout channels (written)
+ * 3x3, stride 1, pad 1; 1 <= cin, cout <= 65536; h, w <= 65536.  Empty
+ * inputs launch nothing.  Asynchronous on `stream`; WINO_EINVAL for NULL
+ * pointers or bad sizes, WINO_EUNSUPPORTED beyond the limits, WINO_EHIP if
+ * the launch fails.
+ */
+wino_status wino_f4_conv_float(const int8_t* x, const float* w_oihw, float* y, int32_t n,
+                               int32_t cin, int32_t cout, int32_t h, int32_t w,
+                               wino_layout layout, hipStream_t stream);
+
 /* Static description of a status code; never NULL. */
 const char* wino_strerror(wino_status status);
 

@@ -27,7 +27,7 @@ EXPORTS = [
     "wino_f4_workspace_bytes",
     "wino_f4_conv_int8", "wino_f4_input_transform", "wino_f4_tap_gemm", "wino_f4_calibrate_input", "wino_f4_calibrate_output",
     "wino_f4_debug_input_transform", "wino_f4_debug_tap_gemm",
-    "direct_conv_quantize_weights", "direct_conv_int8", "wino_strerror",
+    "direct_conv_quantize_weights", "direct_conv_int8", "wino_f4_conv_float", "wino_strerror",
 ]
 
 
@@ -95,6 +95,7 @@ def load_library():
         "wino_f4_debug_tap_gemm": (I32, [P, P, I32, I32, I32, I32, P, P, SZ, P]),
         "direct_conv_quantize_weights": (I32, [P, I32, I32, P, P]),
         "direct_conv_int8": (I32, [P, P, P, P, I32, I32, I32, I32, I32, I32, I32, I32, P]),
+        "wino_f4_conv_float": (I32, [P, P, P, I32, I32, I32, I32, I32, I32, P]),
         "wino_strerror": (ctypes.c_char_p, [I32]),
     }
     for name, (res, args) in sig.items():
@@ -432,3 +433,11 @@ def direct_conv_int8(x, w_ohwi, bias, y, n, cin, cout, h, w, layout=NCHW, out_sh
     st = lib.direct_conv_int8(_ptr(x), _ptr(w_ohwi), _ptr(bias), _ptr(y), n, cin, cout, h, w, layout,
                               int(out_shift), int(bool(relu)), _stream(stream))
     _check(st, "direct_conv_int8")
+
+
+def wino_f4_conv_float(x, w_oihw, y, n, cin, cout, h, w, layout=NCHW, stream=None):
+    """Unquantized fp32 Winograd F(4x4,3x3) (reference stage): x int8, w_oihw
+    fp32 [cout][cin][3][3], y fp32 in x's layout, all torch device tensors."""
+    lib = load_library()
+    st = lib.wino_f4_conv_float(_ptr(x), _ptr(w_oihw), _ptr(y), n, cin, cout, h, w, layout, _stream(stream))
+    _check(st, "wino_f4_conv_float")
