@@ -51,6 +51,10 @@ def parse():
     ap.add_argument("--no-plan-timing", action="store_true", help="skip timing the on-device plan builds")
     ap.add_argument("--cpu-images", type=int, default=0,
                     help="oracle sample size in images; 0 = as many as fill ~10 s of CPU work")
+    ap.add_argument("--chain", action="store_true",
+                    help="C3 only: time the four layers as one chained step (each layer's input the previous "
+                         "layer's GPU output, 2x2 max-pooled where the stage halves the image), eager and as a "
+                         "replayed HIP graph, with the algorithm wino_select_algorithm picks per layer")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 256 MiB device-to-device copy (scale reference for HBM counters)")
     return ap.parse_args()
@@ -177,12 +181,120 @@ def cpu_baseline(x, layers_plan, n_img, spec, target_s=10.0):
             "affinity": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None}
 
 
+def run_chain(args):
+    """The C3 stack as one step: four layers chained on the device, NHWC.
+    Per layer, wino_select_algorithm picks direct, F2 or F4 (direct is not
+    chained here: a layer that picks it runs F2, and the line says so);
+    calibration and plans are set up untimed on the layer's real chained
+    input.  Between stages the 2x2 max-pooling is two elementwise maxima
+    (glue of the workload, not part of a layer; timed on its own)."""
+    import numpy as np
+    import torch
+
+    import paper_2209_12982_amd as W
+    import workloads
+
+    torch.cuda.set_device(0)
+    wl = workloads.WORKLOADS["C3"]
+    x, layers = workloads.generate("C3")
+    n = x.shape[0]
+    cur = torch.from_numpy(np.ascontiguousarray(x.transpose(0, 2, 3, 1))).cuda()
+    stages, ops, picked = [], 0.0, []
+    for k, (f, bias, spec) in enumerate(layers):
+        pool = None
+        if k > 0 and (spec.h, spec.w) != (layers[k - 1][2].h, layers[k - 1][2].w):
+            # rows first (two contiguous half-images), then column pairs
+            rows = cur.view(n, spec.h, 2, 2 * spec.w * spec.cin)
+            t = torch.empty((n, spec.h, 2 * spec.w * spec.cin), dtype=torch.int8, device="cuda")
+            cols = t.view(n, spec.h, spec.w, 2, spec.cin)
+            dst = torch.empty((n, spec.h, spec.w, spec.cin), dtype=torch.int8, device="cuda")
+
+            def pool(rows=rows, t=t, cols=cols, dst=dst):
+                torch.maximum(rows[:, :, 0], rows[:, :, 1], out=t)
+                torch.maximum(cols[:, :, :, 0], cols[:, :, :, 1], out=dst)
+            pool()
+            cur = dst
+        algo = W.wino_select_algorithm(n, spec.cin, spec.cout, spec.h, spec.w)
+        mt = 4 if algo == W.ALGO_F4 else 2
+        picked.append({W.ALGO_F4: "f4", W.ALGO_F2: "f2", W.ALGO_DIRECT: "direct (ran f2)"}[algo])
+        calibrate = W.wino_f4_calibrate_input if mt == 4 else W.wino_f2_calibrate_input
+        make_plan = W.wino_f4_plan if mt == 4 else W.wino_f2_plan
+        eb, _ = calibrate(cur, n, spec.cin, spec.h, spec.w, W.NHWC)
+        plan0 = make_plan(f, eb, bias=bias, out_shift=0, relu=spec.relu)
+        ws = torch.empty(max(1, W.wino_f4_workspace_bytes(plan0, n, spec.h, spec.w)), dtype=torch.int8,
+                         device="cuda")
+        s, _ = W.wino_f4_calibrate_output(plan0, cur, n, spec.h, spec.w, W.NHWC, ws)
+        plan = make_plan(f, eb, bias=bias, out_shift=s, relu=spec.relu)
+        y = torch.empty((n, spec.h, spec.w, spec.cout), dtype=torch.int8, device="cuda")
+        stages.append((pool, plan, cur, y, ws, spec))
+        W.wino_f4_conv_int8(plan, cur, y, n, spec.h, spec.w, W.NHWC, W.SPLIT, ws)
+        cur = y
+        ops += 2.0 * 9 * n * spec.h * spec.w * spec.cin * spec.cout
+    torch.cuda.synchronize()
+
+    def step():
+        for pool, plan, xin, y, ws, spec in stages:
+            if pool is not None:
+                pool()
+            W.wino_f4_conv_int8(plan, xin, y, n, spec.h, spec.w, W.NHWC, W.SPLIT, ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    eager_ref = stages[-1][3].clone()
+    ms = time_loop(torch, step, args.steps)
+    layer_ms = []
+    for pool, plan, xin, y, ws, spec in stages:
+        layer_ms.append(kernel_ms(torch, lambda plan=plan, xin=xin, y=y, ws=ws, spec=spec: W.wino_f4_conv_int8(
+            plan, xin, y, n, spec.h, spec.w, W.NHWC, W.SPLIT, ws), args.steps)[0])
+    pools = [st[0] for st in stages if st[0] is not None]
+    pool_ms = sum(kernel_ms(torch, p, args.steps)[0] for p in pools)
+
+    # the same step captured once as a HIP graph and replayed: the launches
+    # of the step's kernels are submitted as one graph launch
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        step()
+    replays_ok = True
+    for _ in range(3):
+        stages[-1][3].zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        replays_ok &= bool(torch.equal(stages[-1][3], eager_ref))
+    graph_ms = time_loop(torch, g.replay, args.steps)
+
+    line = {
+        "metric": METRIC, "value": ops / (ms * 1e-3) / 1e12, "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "int8", "data": "synthetic",
+        "config": {"workload": f"C3 chain: {wl.desc}, four layers chained on the device", "n": n,
+                   "layout": "nhwc", "algorithms": picked,
+                   "layers": [f"{sp.cin}->{sp.cout}@{sp.h}x{sp.w}" for _, _, _, _, _, sp in stages]},
+        "layer_ms": layer_ms, "pool_ms": pool_ms,
+        "graph": {"ms_per_step": graph_ms, "TOPS": ops / (graph_ms * 1e-3) / 1e12,
+                  "replays_match_eager": replays_ok},
+        "roofline": None, "cpu_baseline": None,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
               "(the layer shards by batch with no communication between GPUs)", file=sys.stderr)
         sys.exit(2)
+    if args.chain:
+        if args.config != "C3":
+            print("--chain times the C3 stack; use --config C3", file=sys.stderr)
+            sys.exit(2)
+        return run_chain(args)
     import numpy as np
     import torch
 
