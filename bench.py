@@ -131,7 +131,11 @@ def time_cold(torch, fn, calls, flush):
     a 1 GiB buffer is read between calls (a sum over it), which evicts the
     call's inputs from L2 and from the 256 MB Infinity Cache (MALL) and
     leaves clean lines there, so the call reads its inputs from HBM and
-    pays no write-back of someone else's data.  Returns (median, p10, p90) ms."""
+    pays no write-back of someone else's data.  As in kernel_ms, the smaller
+    of two estimates: the median of event pairs around single calls (which
+    also count the dispatch latency after the flush) and the difference
+    between a loop of flush + call and a loop of flushes alone, divided by
+    the calls.  Returns (ms, p10, p90) with p10/p90 of the event pairs."""
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(calls)]
     torch.cuda.synchronize()
     for s, e in ev:
@@ -142,7 +146,20 @@ def time_cold(torch, fn, calls, flush):
     torch.cuda.synchronize()
     t = sorted(s.elapsed_time(e) for s, e in ev)
     q = lambda f: t[min(len(t) - 1, int(f * (len(t) - 1) + 0.5))]
-    return q(0.5), q(0.1), q(0.9)
+
+    def loop(with_call):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        s.record()
+        for _ in range(calls):
+            flush.sum()
+            if with_call:
+                fn()
+        e.record()
+        torch.cuda.synchronize()
+        return s.elapsed_time(e)
+    diff = (loop(True) - loop(False)) / calls
+    return (min(q(0.5), diff) if diff > 0 else q(0.5)), q(0.1), q(0.9)
 
 
 def kernel_ms(torch, fn, calls):
