@@ -180,6 +180,13 @@ def test_invalid_arguments_return_status():
     eg = np.zeros(36, np.int8); eg[0] = 100; eg[1] = -100
     assert lib.wino_f4_plan_tables(f.ctypes.data, 1, 1, eb.ctypes.data, eg.ctypes.data, None, 0,
                                    None, None, None, None, None) == -3
+    # the fp32 reference stage validates before any launch too
+    fw = np.zeros(9, np.float32)
+    yf = np.zeros(16, np.float32)
+    assert lib.wino_f4_conv_float(None, fw.ctypes.data, yf.ctypes.data, 1, 1, 1, 4, 4, 0, None) == -1
+    assert lib.wino_f4_conv_float(x.ctypes.data, fw.ctypes.data, yf.ctypes.data, 1, 0, 1, 4, 4, 0, None) == -1
+    assert lib.wino_f4_conv_float(x.ctypes.data, fw.ctypes.data, yf.ctypes.data, 1, 1, 1, 4, 4, 7, None) == -1
+    assert lib.wino_f4_conv_float(x.ctypes.data, fw.ctypes.data, yf.ctypes.data, 1, 70000, 1, 4, 4, 0, None) == -2
     lib.wino_f4_plan_destroy(None)
     assert W.wino_strerror(-5).startswith("workspace")
 
