@@ -51,6 +51,7 @@ struct K1Args {
     int n, cin, h, w, th, tw, cin_pad;
     int ntxb, ncg;
     int x_vec;                          // 16-byte loads allowed (Cin % 16 == 0, x aligned)
+    int x_dw;                           // NCHW word loads allowed (W % 4 == 0, x aligned, image < 2 GiB)
     int vq_buf;                         // tap planes below 4 GiB: buffer stores with a scalar base
     long long t_pad;                    // tile stride of a tap plane in Vq
     long long plane_bytes;              // bytes of one tap plane of Vq
@@ -129,6 +130,56 @@ __device__ __forceinline__ void k1_stage_band(uint32_t* lds, const int8_t* __res
                 }
             }
             *(uint4*)(lds + pix * K1_CS + 4 * part) = v;
+        }
+    } else if (g.x_dw) {
+        // NCHW with W % 4 == 0: an item moves 4 channels x 4 band columns of
+        // one band row.  The band starts at column M tx0 - 1, so a group of
+        // four columns straddles two aligned words of each channel's image
+        // row: two word loads and a byte alignment per channel, then a 4x4
+        // byte transpose (the four channels of a column into one word) and
+        // four LDS word stores.  A word left or right of the image row, in
+        // a row outside the image or of a channel >= Cin gets an offset past
+        // the image's bytes and reads as zero (with W % 4 == 0 a word is
+        // either wholly inside a row or wholly outside it).
+        constexpr int NQ = (COLS + 3) / 4;
+        constexpr int kOut = 0x7ffffff0;  // >= the image's bytes (checked on the host)
+        const int img_bytes = g.cin * g.h * g.w;
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(x + (long long)img * img_bytes), 0, img_bytes, 0x00020000);
+        for (int id = threadIdx.x; id < 16 * ROWS * NQ; id += THREADS) {
+            const int qc = id % NQ;
+            const int rest = id / NQ;
+            const int r = rest % ROWS, cq = rest / ROWS;
+            const int hh = h0 + r;
+            const int cc = w0 + 4 * qc;           // first column of the group
+            const int a = cc >> 2;                // its word (floor), then the next one
+            const int sh = cc & 3;                // byte offset of the group in word a
+            const bool rok = hh >= 0 && hh < g.h;
+            const bool ok0 = rok && a >= 0 && 4 * a < g.w;
+            const bool ok1 = rok && a + 1 >= 0 && 4 * (a + 1) < g.w;
+            const int hr = rok ? hh : 0;
+            uint32_t v[4];
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                const int ci = ci0 + 4 * cq + kk;
+                const bool cok = ci < g.cin;
+                const int base = ((cok ? ci : 0) * g.h + hr) * g.w + 4 * a;
+                const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b32(rs, cok && ok0 ? base : kOut, 0, 0);
+                const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b32(rs, cok && ok1 ? base + 4 : kOut, 0, 0);
+                v[kk] = __builtin_amdgcn_alignbyte(hi, lo, (uint32_t)sh);
+            }
+            // v[k] byte j = channel k, column j  ->  col[j] byte k
+            const uint32_t ab_lo = __builtin_amdgcn_perm(v[1], v[0], 0x05010400u);
+            const uint32_t ab_hi = __builtin_amdgcn_perm(v[1], v[0], 0x07030602u);
+            const uint32_t cd_lo = __builtin_amdgcn_perm(v[3], v[2], 0x05010400u);
+            const uint32_t cd_hi = __builtin_amdgcn_perm(v[3], v[2], 0x07030602u);
+            const uint32_t col[4] = {__builtin_amdgcn_perm(cd_lo, ab_lo, 0x05040100u),
+                                     __builtin_amdgcn_perm(cd_lo, ab_lo, 0x07060302u),
+                                     __builtin_amdgcn_perm(cd_hi, ab_hi, 0x05040100u),
+                                     __builtin_amdgcn_perm(cd_hi, ab_hi, 0x07060302u)};
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (4 * qc + j < COLS) lds[(r * COLS + 4 * qc + j) * K1_CS + cq] = col[j];
         }
     } else {
         uint8_t* lb = (uint8_t*)lds;
@@ -1068,6 +1119,7 @@ K1Args k1_args(const Geometry& g, int cin, int cin_pad, const TapTables& tab, in
     a.plane_bytes = g.t_pad * cin_pad * kbytes_per_channel(bits);
     a.vq_buf = a.plane_bytes < 0x7fffffffLL;
     a.x_vec = 0;
+    a.x_dw = 0;
     return a;
 }
 
@@ -1087,6 +1139,8 @@ wino_status launch_k1_tx(const K1Args& a, wino_layout layout, const int8_t* x, i
     if (blocks == 0) return WINO_OK;
     if (blocks > 0x7fffffffll) return WINO_EUNSUPPORTED;
     args.x_vec = (a.cin % 16 == 0) && (((uintptr_t)x & 15) == 0);
+    args.x_dw = layout == WINO_NCHW && a.w % 4 == 0 && (((uintptr_t)x & 3) == 0) &&
+                (long long)a.cin * a.h * a.w < 0x7ffffff0ll;
 #define K1_LAUNCH(L, S)                                                                                      \
     hipLaunchKernelGGL((wino_input_xform<M, L, MODE, Q, TX, S>), dim3((unsigned)blocks), dim3(16 * TX), 0, stream, \
                        x, vq, tapmax, args)
