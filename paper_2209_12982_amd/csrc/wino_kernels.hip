@@ -132,54 +132,62 @@ __device__ __forceinline__ void k1_stage_band(uint32_t* lds, const int8_t* __res
             *(uint4*)(lds + pix * K1_CS + 4 * part) = v;
         }
     } else if (g.x_dw) {
-        // NCHW with W % 4 == 0: an item moves 4 channels x 4 band columns of
+        // NCHW with W % 4 == 0: an item moves 4 channels x 8 band columns of
         // one band row.  The band starts at column M tx0 - 1, so a group of
-        // four columns straddles two aligned words of each channel's image
-        // row: two word loads and a byte alignment per channel, then a 4x4
-        // byte transpose (the four channels of a column into one word) and
-        // four LDS word stores.  A word left or right of the image row, in
-        // a row outside the image or of a channel >= Cin gets an offset past
-        // the image's bytes and reads as zero (with W % 4 == 0 a word is
+        // eight columns straddles three aligned words of each channel's image
+        // row: three word loads and two byte alignments per channel, then two
+        // 4x4 byte transposes (the four channels of a column into one word)
+        // and eight LDS word stores.  A word left or right of the image row,
+        // in a row outside the image or of a channel >= Cin gets an offset
+        // past the image's bytes and reads as zero (with W % 4 == 0 a word is
         // either wholly inside a row or wholly outside it).
-        constexpr int NQ = (COLS + 3) / 4;
+        constexpr int NG = (COLS + 7) / 8;
         constexpr int kOut = 0x7ffffff0;  // >= the image's bytes (checked on the host)
         const int img_bytes = g.cin * g.h * g.w;
         const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
             (void*)(x + (long long)img * img_bytes), 0, img_bytes, 0x00020000);
-        for (int id = threadIdx.x; id < 16 * ROWS * NQ; id += THREADS) {
-            const int qc = id % NQ;
-            const int rest = id / NQ;
+        for (int id = threadIdx.x; id < 16 * ROWS * NG; id += THREADS) {
+            const int gc = id % NG;
+            const int rest = id / NG;
             const int r = rest % ROWS, cq = rest / ROWS;
             const int hh = h0 + r;
-            const int cc = w0 + 4 * qc;           // first column of the group
-            const int a = cc >> 2;                // its word (floor), then the next one
+            const int cc = w0 + 8 * gc;           // first column of the group
+            const int a = cc >> 2;                // its word (floor), then the next two
             const int sh = cc & 3;                // byte offset of the group in word a
             const bool rok = hh >= 0 && hh < g.h;
             const bool ok0 = rok && a >= 0 && 4 * a < g.w;
             const bool ok1 = rok && a + 1 >= 0 && 4 * (a + 1) < g.w;
+            const bool ok2 = rok && a + 2 >= 0 && 4 * (a + 2) < g.w;
             const int hr = rok ? hh : 0;
-            uint32_t v[4];
+            uint32_t v[2][4];
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk) {
                 const int ci = ci0 + 4 * cq + kk;
                 const bool cok = ci < g.cin;
                 const int base = ((cok ? ci : 0) * g.h + hr) * g.w + 4 * a;
-                const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b32(rs, cok && ok0 ? base : kOut, 0, 0);
-                const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b32(rs, cok && ok1 ? base + 4 : kOut, 0, 0);
-                v[kk] = __builtin_amdgcn_alignbyte(hi, lo, (uint32_t)sh);
+                const uint32_t w0_ = __builtin_amdgcn_raw_buffer_load_b32(rs, cok && ok0 ? base : kOut, 0, 0);
+                const uint32_t w1_ = __builtin_amdgcn_raw_buffer_load_b32(rs, cok && ok1 ? base + 4 : kOut, 0, 0);
+                const uint32_t w2_ = __builtin_amdgcn_raw_buffer_load_b32(rs, cok && ok2 ? base + 8 : kOut, 0, 0);
+                v[0][kk] = __builtin_amdgcn_alignbyte(w1_, w0_, (uint32_t)sh);
+                v[1][kk] = __builtin_amdgcn_alignbyte(w2_, w1_, (uint32_t)sh);
             }
-            // v[k] byte j = channel k, column j  ->  col[j] byte k
-            const uint32_t ab_lo = __builtin_amdgcn_perm(v[1], v[0], 0x05010400u);
-            const uint32_t ab_hi = __builtin_amdgcn_perm(v[1], v[0], 0x07030602u);
-            const uint32_t cd_lo = __builtin_amdgcn_perm(v[3], v[2], 0x05010400u);
-            const uint32_t cd_hi = __builtin_amdgcn_perm(v[3], v[2], 0x07030602u);
-            const uint32_t col[4] = {__builtin_amdgcn_perm(cd_lo, ab_lo, 0x05040100u),
-                                     __builtin_amdgcn_perm(cd_lo, ab_lo, 0x07060302u),
-                                     __builtin_amdgcn_perm(cd_hi, ab_hi, 0x05040100u),
-                                     __builtin_amdgcn_perm(cd_hi, ab_hi, 0x07060302u)};
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (4 * qc + j < COLS) lds[(r * COLS + 4 * qc + j) * K1_CS + cq] = col[j];
+            for (int hf = 0; hf < 2; ++hf) {
+                // v[hf][k] byte j = channel k, column 4 hf + j  ->  col[j] byte k
+                const uint32_t ab_lo = __builtin_amdgcn_perm(v[hf][1], v[hf][0], 0x05010400u);
+                const uint32_t ab_hi = __builtin_amdgcn_perm(v[hf][1], v[hf][0], 0x07030602u);
+                const uint32_t cd_lo = __builtin_amdgcn_perm(v[hf][3], v[hf][2], 0x05010400u);
+                const uint32_t cd_hi = __builtin_amdgcn_perm(v[hf][3], v[hf][2], 0x07030602u);
+                const uint32_t col[4] = {__builtin_amdgcn_perm(cd_lo, ab_lo, 0x05040100u),
+                                         __builtin_amdgcn_perm(cd_lo, ab_lo, 0x07060302u),
+                                         __builtin_amdgcn_perm(cd_hi, ab_hi, 0x05040100u),
+                                         __builtin_amdgcn_perm(cd_hi, ab_hi, 0x07060302u)};
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int c = 8 * gc + 4 * hf + j;
+                    if (c < COLS) lds[(r * COLS + c) * K1_CS + cq] = col[j];
+                }
+            }
         }
     } else {
         uint8_t* lb = (uint8_t*)lds;
