@@ -300,8 +300,10 @@ size_t wino_f4_workspace_bytes(wino_f4_plan_t plan, int32_t n, int32_t h, int32_
  *              (ignored for FUSED; may be NULL then); contents are scratch.
  *   stream     all work is enqueued on this stream; no host synchronization.
  * A plan may be used concurrently on several streams with separate
- * workspaces.  Errors: WINO_EINVAL, WINO_EUNSUPPORTED, WINO_EWORKSPACE,
- * WINO_EHIP (launch failure reported by hipGetLastError).
+ * workspaces.  The device current at the call must be the one the plan was
+ * made on (WINO_EINVAL otherwise; the same holds for every call below that
+ * takes a plan and device data).  Errors: WINO_EINVAL, WINO_EUNSUPPORTED,
+ * WINO_EWORKSPACE, WINO_EHIP (launch failure reported by hipGetLastError).
  */
 wino_status wino_f4_conv_int8(wino_f4_plan_t plan, const int8_t* x, int8_t* y, int32_t n,
                               int32_t h, int32_t w, wino_layout layout, wino_variant variant,

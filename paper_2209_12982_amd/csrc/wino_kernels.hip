@@ -1331,6 +1331,11 @@ wino_status check_common(const wino_f4_plan_s* p, const void* x, int32_t n, int3
                          wino_layout layout, Geometry& g) {
     if (!p || !x) return WINO_EINVAL;
     if (layout != WINO_NCHW && layout != WINO_NHWC) return WINO_EINVAL;
+    // the plan's tables live on the device that was current when it was
+    // made; a launch on another device would read them from the wrong one
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return WINO_EHIP;
+    if (dev != p->device) return WINO_EINVAL;
     return geometry(n, h, w, p->m, g);
 }
 
