@@ -465,6 +465,41 @@ def main():
                     "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
                     "frac": tap_ops / (ms * 1e-3) / 1e12 / PEAK_INT8_TOPS, "traffic": None}
 
+    # the chip's rates measured in this run: int8 MFMA loops (both shapes;
+    # the tap GEMM issues 16x16x64) and a 1 GiB device copy (HBM-bound)
+    measured = {}
+    sink = torch.zeros(4, dtype=torch.int32, device="cuda")
+    blocks = 2 * torch.cuda.get_device_properties(0).multi_processor_count
+    for shape in (32, 16):
+        W.wino_probe_mfma_int8(shape, 100, blocks, sink)
+        best = None
+        for _ in range(3):
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s.record()
+            ops_probe = W.wino_probe_mfma_int8(shape, 20000, blocks, sink)
+            e.record()
+            torch.cuda.synchronize()
+            t = s.elapsed_time(e)
+            best = t if best is None else min(best, t)
+        name = "int8_mfma_32x32x32_TOPS" if shape == 32 else "int8_mfma_16x16x64_TOPS"
+        measured[name] = ops_probe / (best * 1e-3) / 1e12
+    src = torch.ones(1 << 30, dtype=torch.int8, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    best = None
+    for _ in range(3):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        dst.copy_(src)
+        e.record()
+        torch.cuda.synchronize()
+        best = s.elapsed_time(e) if best is None else min(best, s.elapsed_time(e))
+    measured["hbm_copy_GBs"] = 2.0 * src.numel() / (best * 1e-3) / 1e9
+    del src, dst
+    if variant == W.SPLIT and args.bits == 8:
+        kernels[k2_name]["frac_of_measured_16x16x64"] = kernels[k2_name]["TOP/s"] / measured["int8_mfma_16x16x64_TOPS"]
+        kernels[k1_name]["frac_of_measured_copy"] = kernels[k1_name]["GB/s"] / measured["hbm_copy_GBs"]
+
     direct = None
     if not args.no_direct:
         wq, _ = W.direct_conv_quantize_weights(f)
@@ -510,6 +545,7 @@ def main():
         "tap_gemm_mfma_frac_of_step": tap_ops / (ms * 1e-3) / 1e12 / k2_peak,
         "cold": {"step_ms": cold["step_ms"], "TOPS": direct_ops / (cold["step_ms"] * 1e-3) / 1e12,
                  "calls": ncold, "flush": "1 GiB read before each call (L2 and MALL evicted, clean)"},
+        "measured_peaks": measured,
         "direct_conv": direct,
         "cpu_baseline": cpu,
         "plan_ms": plan_ms,

@@ -432,6 +432,20 @@ wino_status wino_f4_conv_float(const int8_t* x, const float* w_oihw, float* y, i
                                int32_t cin, int32_t cout, int32_t h, int32_t w,
                                wino_layout layout, hipStream_t stream);
 
+/*
+ * wino_probe_mfma_int8 -- measurement probe, not part of the convolution:
+ * `blocks` workgroups of four waves issue independent int8 MFMAs only
+ * (shape 16: v_mfma_i32_16x16x64_i8, eight chains per wave; shape 32:
+ * v_mfma_i32_32x32x32_i8, four chains), `iters` rounds each, so that a
+ * caller timing the launch measures the int8 matrix-core rate at the run's
+ * clock.  *ops (host) receives the launch's operation count (2 per
+ * multiply-add).  sink: device int32, never written in practice (it keeps
+ * the results live).  Asynchronous on `stream`; WINO_EINVAL for a bad shape
+ * or count or a NULL pointer.
+ */
+wino_status wino_probe_mfma_int8(int32_t shape, int32_t iters, int32_t blocks, int32_t* sink,
+                                 int64_t* ops, hipStream_t stream);
+
 /* Static description of a status code; never NULL. */
 const char* wino_strerror(wino_status status);
 

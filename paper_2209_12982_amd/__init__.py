@@ -21,5 +21,5 @@ from .binding import (  # noqa: F401
     wino_f4_input_transform, wino_f4_tap_gemm,
     wino_f4_calibrate_input, wino_f4_calibrate_output,
     wino_f4_debug_input_transform, wino_f4_debug_tap_gemm,
-    direct_conv_quantize_weights, direct_conv_int8, wino_f4_conv_float, wino_strerror,
+    direct_conv_quantize_weights, direct_conv_int8, wino_f4_conv_float, wino_probe_mfma_int8, wino_strerror,
 )

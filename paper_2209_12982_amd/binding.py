@@ -27,7 +27,7 @@ EXPORTS = [
     "wino_f4_workspace_bytes",
     "wino_f4_conv_int8", "wino_f4_input_transform", "wino_f4_tap_gemm", "wino_f4_calibrate_input", "wino_f4_calibrate_output",
     "wino_f4_debug_input_transform", "wino_f4_debug_tap_gemm",
-    "direct_conv_quantize_weights", "direct_conv_int8", "wino_f4_conv_float", "wino_strerror",
+    "direct_conv_quantize_weights", "direct_conv_int8", "wino_f4_conv_float", "wino_probe_mfma_int8", "wino_strerror",
 ]
 
 
@@ -96,6 +96,7 @@ def load_library():
         "direct_conv_quantize_weights": (I32, [P, I32, I32, P, P]),
         "direct_conv_int8": (I32, [P, P, P, P, I32, I32, I32, I32, I32, I32, I32, I32, P]),
         "wino_f4_conv_float": (I32, [P, P, P, I32, I32, I32, I32, I32, I32, P]),
+        "wino_probe_mfma_int8": (I32, [I32, I32, I32, P, P, P]),
         "wino_strerror": (ctypes.c_char_p, [I32]),
     }
     for name, (res, args) in sig.items():
@@ -441,3 +442,13 @@ def wino_f4_conv_float(x, w_oihw, y, n, cin, cout, h, w, layout=NCHW, stream=Non
     lib = load_library()
     st = lib.wino_f4_conv_float(_ptr(x), _ptr(w_oihw), _ptr(y), n, cin, cout, h, w, layout, _stream(stream))
     _check(st, "wino_f4_conv_float")
+
+
+def wino_probe_mfma_int8(shape, iters, blocks, sink, stream=None):
+    """Launch the int8 matrix-core rate probe (measurement only); returns the
+    launch's operation count.  sink: a device int32 tensor of >= 1 element."""
+    ops = ctypes.c_int64()
+    st = load_library().wino_probe_mfma_int8(int(shape), int(iters), int(blocks), _ptr(sink), ctypes.byref(ops),
+                                             _stream(stream))
+    _check(st, "wino_probe_mfma_int8")
+    return ops.value

@@ -12,7 +12,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libwinof4.so")
-SOURCES = ["plan.cpp", "plan_device.hip", "wino_kernels.hip", "wino_fused.hip", "direct_conv.hip", "wino_float.hip"]
+SOURCES = ["plan.cpp", "plan_device.hip", "wino_kernels.hip", "wino_fused.hip", "direct_conv.hip", "wino_float.hip", "probe.hip"]
 ARCH = "gfx950"
 # Packed fp32 instructions are disabled for every HIP translation unit; the
 # host pass prints a harmless note that it does not know the feature.

@@ -69,3 +69,15 @@ def test_deep_channels_bitexact(make, m):
     ref = tapwise.conv_int8(x, tapwise.make_plan(f, eb, bias=b, out_shift=11, m=m, bits=bits))
     for layout in (W.NCHW, W.NHWC):
         assert (run_conv(plan, x, layout) == ref).all()
+
+
+@pytest.mark.parametrize("shape,macs", [(16, 8 * 16 * 16 * 64), (32, 4 * 32 * 32 * 32)])
+def test_mfma_probe_counts_its_operations(shape, macs):
+    """The matrix-core probe the bench times reports 2 operations per
+    multiply-add of its launch and never writes its sink."""
+    torch = torch_dev()
+    sink = torch.full((4,), 5, dtype=torch.int32, device="cuda")
+    ops = W.wino_probe_mfma_int8(shape, 3, 2, sink)
+    torch.cuda.synchronize()
+    assert ops == 2 * macs * 4 * 2 * 3
+    assert (sink.cpu().numpy() == 5).all()

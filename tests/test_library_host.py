@@ -187,6 +187,11 @@ def test_invalid_arguments_return_status():
     assert lib.wino_f4_conv_float(x.ctypes.data, fw.ctypes.data, yf.ctypes.data, 1, 0, 1, 4, 4, 0, None) == -1
     assert lib.wino_f4_conv_float(x.ctypes.data, fw.ctypes.data, yf.ctypes.data, 1, 1, 1, 4, 4, 7, None) == -1
     assert lib.wino_f4_conv_float(x.ctypes.data, fw.ctypes.data, yf.ctypes.data, 1, 70000, 1, 4, 4, 0, None) == -2
+    # the matrix-core probe checks its arguments before launching
+    ops = ctypes.c_int64()
+    assert lib.wino_probe_mfma_int8(7, 10, 1, x.ctypes.data, ctypes.byref(ops), None) == -1
+    assert lib.wino_probe_mfma_int8(16, 0, 1, x.ctypes.data, ctypes.byref(ops), None) == -1
+    assert lib.wino_probe_mfma_int8(32, 10, 1, None, ctypes.byref(ops), None) == -1
     lib.wino_f4_plan_destroy(None)
     assert W.wino_strerror(-5).startswith("workspace")
 
