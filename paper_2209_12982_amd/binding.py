@@ -132,6 +132,45 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _dptr(t, dtype, need=0, what="tensor"):
+    """Device pointer of a contiguous torch GPU tensor of `dtype` (any dtype
+    if None) holding at least `need` elements, or None for None.  The C ABI
+    takes plain pointers and cannot tell a host array or a short buffer from
+    device memory; a kernel reading either would fault, so the binding checks
+    before passing the pointer on."""
+    if t is None:
+        return None
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{what}: expected a torch tensor on the GPU, got {type(t).__name__}")
+    if not t.is_cuda:
+        raise ValueError(f"{what}: must be a GPU tensor (the kernels read and write device memory)")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{what}: expected {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what}: must be contiguous")
+    if need > 0 and t.numel() < need:
+        raise ValueError(f"{what}: holds {t.numel()} elements, the call reads or writes {need}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _tiles(n, h, w, m):
+    """Number of m x m output tiles of a batch, 0 for empty or negative sizes."""
+    if min(n, h, w) <= 0:
+        return 0
+    return int(n) * ((int(h) + m - 1) // m) * ((int(w) + m - 1) // m)
+
+
+def _elems(*dims):
+    """Product of the sizes, 0 if any is negative (the C ABI rejects those)."""
+    p = 1
+    for d in dims:
+        if d < 0:
+            return 0
+        p *= int(d)
+    return p
+
+
 def _stream(stream):
     if stream is None:
         import torch
@@ -344,22 +383,28 @@ def wino_f4_workspace_bytes(plan, n, h, w, variant=SPLIT):
 def wino_f4_conv_int8(plan, x, y, n, h, w, layout=NCHW, variant=SPLIT, workspace=None, stream=None):
     lib = load_library()
     ws_bytes = _nbytes(workspace)
-    st = lib.wino_f4_conv_int8(plan.handle, _ptr(x), _ptr(y), n, h, w, layout, variant,
-                               _ptr(workspace), ws_bytes, _stream(stream))
+    import torch
+    st = lib.wino_f4_conv_int8(plan.handle, _dptr(x, torch.int8, _elems(n, plan.cin, h, w), "x"),
+                               _dptr(y, torch.int8, _elems(n, plan.cout, h, w), "y"), n, h, w, layout, variant,
+                               _dptr(workspace, None, 0, "workspace"), ws_bytes, _stream(stream))
     _check(st, "wino_f4_conv_int8")
 
 
 def wino_f4_input_transform(plan, x, n, h, w, layout, workspace, stream=None):
     lib = load_library()
     ws_bytes = _nbytes(workspace)
-    _check(lib.wino_f4_input_transform(plan.handle, _ptr(x), n, h, w, layout, _ptr(workspace), ws_bytes,
-                                       _stream(stream)), "wino_f4_input_transform")
+    import torch
+    _check(lib.wino_f4_input_transform(plan.handle, _dptr(x, torch.int8, _elems(n, plan.cin, h, w), "x"), n, h, w,
+                                       layout, _dptr(workspace, None, 0, "workspace"), ws_bytes, _stream(stream)),
+           "wino_f4_input_transform")
 
 
 def wino_f4_tap_gemm(plan, workspace, y, n, h, w, layout, stream=None):
     lib = load_library()
     ws_bytes = _nbytes(workspace)
-    _check(lib.wino_f4_tap_gemm(plan.handle, _ptr(workspace), ws_bytes, _ptr(y), n, h, w, layout,
+    import torch
+    _check(lib.wino_f4_tap_gemm(plan.handle, _dptr(workspace, None, 0, "workspace"), ws_bytes,
+                                _dptr(y, torch.int8, _elems(n, plan.cout, h, w), "y"), n, h, w, layout,
                                 _stream(stream)), "wino_f4_tap_gemm")
 
 
@@ -367,8 +412,9 @@ def _calibrate_input(fn, m, x, n, cin, h, w, layout, stream):
     ntap = (m + 2) * (m + 2)
     amax = np.zeros(ntap, np.int32)
     eb = np.zeros(ntap, np.int8)
-    st = getattr(load_library(), fn)(_ptr(x), n, cin, h, w, layout, amax.ctypes.data, eb.ctypes.data,
-                                     _stream(stream))
+    import torch
+    st = getattr(load_library(), fn)(_dptr(x, torch.int8, _elems(n, cin, h, w), "x"), n, cin, h, w, layout,
+                                     amax.ctypes.data, eb.ctypes.data, _stream(stream))
     _check(st, fn)
     return eb.astype(int).tolist(), amax.astype(int).tolist()
 
@@ -394,7 +440,9 @@ def wino_f4_calibrate_output(plan, x, n, h, w, layout=NCHW, workspace=None, stre
     ws_bytes = _nbytes(workspace)
     zmax = ctypes.c_int64()
     shift = ctypes.c_int32()
-    st = lib.wino_f4_calibrate_output(plan.handle, _ptr(x), n, h, w, layout, _ptr(workspace), ws_bytes,
+    import torch
+    st = lib.wino_f4_calibrate_output(plan.handle, _dptr(x, torch.int8, _elems(n, plan.cin, h, w), "x"), n, h, w,
+                                      layout, _dptr(workspace, None, 0, "workspace"), ws_bytes,
                                       ctypes.byref(zmax), ctypes.byref(shift), _stream(stream))
     _check(st, "wino_f4_calibrate_output")
     return shift.value, zmax.value
@@ -403,16 +451,23 @@ def wino_f4_calibrate_output(plan, x, n, h, w, layout=NCHW, workspace=None, stre
 def wino_f4_debug_input_transform(plan, x, n, h, w, layout, vq, workspace, stream=None):
     lib = load_library()
     ws_bytes = _nbytes(workspace)
-    st = lib.wino_f4_debug_input_transform(plan.handle, _ptr(x), n, h, w, layout, _ptr(vq), _ptr(workspace),
-                                           ws_bytes, _stream(stream))
+    import torch
+    st = lib.wino_f4_debug_input_transform(plan.handle, _dptr(x, torch.int8, _elems(n, plan.cin, h, w), "x"),
+                                           n, h, w, layout,
+                                           _dptr(vq, torch.float16 if plan.bits == 10 else torch.int8,
+                                                 plan.ntap * _tiles(n, h, w, plan.m) * plan.cin, "vq"),
+                                           _dptr(workspace, None, 0, "workspace"), ws_bytes, _stream(stream))
     _check(st, "wino_f4_debug_input_transform")
 
 
 def wino_f4_debug_tap_gemm(plan, x, n, h, w, layout, m, workspace, stream=None):
     lib = load_library()
     ws_bytes = _nbytes(workspace)
-    st = lib.wino_f4_debug_tap_gemm(plan.handle, _ptr(x), n, h, w, layout, _ptr(m), _ptr(workspace),
-                                    ws_bytes, _stream(stream))
+    import torch
+    st = lib.wino_f4_debug_tap_gemm(plan.handle, _dptr(x, torch.int8, _elems(n, plan.cin, h, w), "x"),
+                                    n, h, w, layout,
+                                    _dptr(m, torch.int32, plan.ntap * _tiles(n, h, w, plan.m) * plan.cout, "m"),
+                                    _dptr(workspace, None, 0, "workspace"), ws_bytes, _stream(stream))
     _check(st, "wino_f4_debug_tap_gemm")
 
 
@@ -431,7 +486,11 @@ def direct_conv_quantize_weights(w_oihw):
 def direct_conv_int8(x, w_ohwi, bias, y, n, cin, cout, h, w, layout=NCHW, out_shift=0, relu=False,
                      stream=None):
     lib = load_library()
-    st = lib.direct_conv_int8(_ptr(x), _ptr(w_ohwi), _ptr(bias), _ptr(y), n, cin, cout, h, w, layout,
+    import torch
+    st = lib.direct_conv_int8(_dptr(x, torch.int8, _elems(n, cin, h, w), "x"),
+                              _dptr(w_ohwi, torch.int8, _elems(9, cin, cout), "w_ohwi"),
+                              _dptr(bias, torch.int32, _elems(cout), "bias"),
+                              _dptr(y, torch.int8, _elems(n, cout, h, w), "y"), n, cin, cout, h, w, layout,
                               int(out_shift), int(bool(relu)), _stream(stream))
     _check(st, "direct_conv_int8")
 
@@ -440,7 +499,11 @@ def wino_f4_conv_float(x, w_oihw, y, n, cin, cout, h, w, layout=NCHW, stream=Non
     """Unquantized fp32 Winograd F(4x4,3x3) (reference stage): x int8, w_oihw
     fp32 [cout][cin][3][3], y fp32 in x's layout, all torch device tensors."""
     lib = load_library()
-    st = lib.wino_f4_conv_float(_ptr(x), _ptr(w_oihw), _ptr(y), n, cin, cout, h, w, layout, _stream(stream))
+    import torch
+    st = lib.wino_f4_conv_float(_dptr(x, torch.int8, _elems(n, cin, h, w), "x"),
+                                _dptr(w_oihw, torch.float32, _elems(cout, cin, 9), "w_oihw"),
+                                _dptr(y, torch.float32, _elems(n, cout, h, w), "y"), n, cin, cout, h, w, layout,
+                                _stream(stream))
     _check(st, "wino_f4_conv_float")
 
 
@@ -448,7 +511,8 @@ def wino_probe_mfma_int8(shape, iters, blocks, sink, stream=None):
     """Launch the int8 matrix-core rate probe (measurement only); returns the
     launch's operation count.  sink: a device int32 tensor of >= 1 element."""
     ops = ctypes.c_int64()
-    st = load_library().wino_probe_mfma_int8(int(shape), int(iters), int(blocks), _ptr(sink), ctypes.byref(ops),
-                                             _stream(stream))
+    import torch
+    st = load_library().wino_probe_mfma_int8(int(shape), int(iters), int(blocks), _dptr(sink, torch.int32, 1, "sink"),
+                                             ctypes.byref(ops), _stream(stream))
     _check(st, "wino_probe_mfma_int8")
     return ops.value

@@ -34,12 +34,18 @@ def test_empty_input_writes_nothing(name, make, ntap, layout, n, h, w):
 
 
 def test_limits_and_workspace_are_refused():
+    """The C ABI's own checks, called directly with buffers far smaller than
+    the sizes (nothing may be launched)."""
+    import ctypes
     torch = torch_dev()
     f = np.zeros((4, 4, 3, 3), np.float32)
     plan = W.wino_f4_plan(f, [0] * 36)
     x = torch.zeros(16, dtype=torch.int8, device="cuda")
     y = torch.zeros(16, dtype=torch.int8, device="cuda")
     ws = torch.zeros(16, dtype=torch.int8, device="cuda")
+    lib = W.load_library()
+    P = ctypes.c_void_p
+    st = torch.cuda.current_stream().cuda_stream
     cases = [
         ((1, 65537, 8), -2),          # image side beyond 65536
         ((1, 32768, 32768), -2),      # 2^26 tiles
@@ -47,14 +53,41 @@ def test_limits_and_workspace_are_refused():
         ((1, 64, 64), -5),            # workspace of 16 bytes
     ]
     for (n, h, w), status in cases:
-        with pytest.raises(W.WinoError) as e:
-            W.wino_f4_conv_int8(plan, x, y, n, h, w, W.NHWC, W.SPLIT, ws)
-        assert e.value.status == status, (n, h, w)
-    with pytest.raises(W.WinoError) as e:
-        W.wino_f4_conv_int8(plan, x, y, 1, 8, 8, 7, W.SPLIT, ws)              # unknown layout
-    assert e.value.status == -1
+        got = lib.wino_f4_conv_int8(plan.handle, P(x.data_ptr()), P(y.data_ptr()), n, h, w, W.NHWC, W.SPLIT,
+                                    P(ws.data_ptr()), 16, P(st))
+        assert got == status, (n, h, w)
+    assert lib.wino_f4_conv_int8(plan.handle, P(x.data_ptr()), P(y.data_ptr()), 1, 8, 8, 7, W.SPLIT,
+                                 P(ws.data_ptr()), 16, P(st)) == -1               # unknown layout
     torch.cuda.synchronize()
     assert (y.cpu().numpy() == 0).all()
+
+
+def test_binding_refuses_buffers_a_kernel_cannot_use():
+    """Host tensors, wrong dtypes, non-contiguous views and buffers shorter
+    than the call's sizes are refused by the binding before the C ABI sees
+    a pointer."""
+    torch = torch_dev()
+    f = np.zeros((4, 4, 3, 3), np.float32)
+    plan = W.wino_f4_plan(f, [0] * 36)
+    n, h, w = 1, 8, 8
+    x = torch.zeros((n, 4, h, w), dtype=torch.int8, device="cuda")
+    y = torch.full((n, 4, h, w), 7, dtype=torch.int8, device="cuda")
+    ws = torch.empty(W.wino_f4_workspace_bytes(plan, n, h, w), dtype=torch.int8, device="cuda")
+    bad_inputs = [
+        x.cpu(),                                          # host memory
+        x.to(torch.int32),                                # wrong dtype
+        torch.zeros((n, 4, h, 2 * w), dtype=torch.int8, device="cuda")[..., ::2],   # strided view
+        torch.zeros(16, dtype=torch.int8, device="cuda"),  # too short
+    ]
+    for bad in bad_inputs:
+        with pytest.raises(ValueError):
+            W.wino_f4_conv_int8(plan, bad, y, n, h, w, W.NCHW, W.SPLIT, ws)
+        with pytest.raises(ValueError):
+            W.wino_f4_conv_int8(plan, x, bad, n, h, w, W.NCHW, W.SPLIT, ws)
+    with pytest.raises(ValueError):
+        W.direct_conv_int8(x, torch.zeros(8, dtype=torch.int8, device="cuda"), None, y, n, 4, 4, h, w)
+    torch.cuda.synchronize()
+    assert (y.cpu().numpy() == 7).all()
 
 
 @pytest.mark.parametrize("make,m", [(W.wino_f4_plan, 4), (W.wino_f2_plan, 2), (W.wino_f4_plan_i10, 4)])
