@@ -15,6 +15,7 @@ figures, the direct int8 convolution of the same library on the same layer
 (speed-up), and the CPU oracle timed on a bounded sample.
 """
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -55,6 +56,10 @@ def parse():
                     help="C3 only: time the four layers as one chained step (each layer's input the previous "
                          "layer's GPU output, 2x2 max-pooled where the stage halves the image), eager and as a "
                          "replayed HIP graph, with the algorithm wino_select_algorithm picks per layer")
+    ap.add_argument("--share-batch", type=int, default=0,
+                    help="one GPU's share of a batch-sharded layer: the first N images of the workload")
+    ap.add_argument("--share-cout", type=int, default=0,
+                    help="one GPU's share of an output-channel-sharded layer: the first C output channels")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 256 MiB device-to-device copy (scale reference for HBM counters)")
     return ap.parse_args()
@@ -327,6 +332,17 @@ def main():
     if args.layer > 0:
         x = workloads.draw_activations(np.random.default_rng(1000 + args.layer), (x.shape[0], spec.cin, spec.h, spec.w),
                                        wl.act, wl.zero_frac)
+    share = None
+    if args.share_batch > 0:
+        # batch sharding: every GPU runs its images with the whole plan
+        x = np.ascontiguousarray(x[:args.share_batch])
+        share = f"images 0..{x.shape[0] - 1} of {wl.n} (batch split)"
+    if args.share_cout > 0:
+        # output-channel sharding: every GPU holds the plan of its channels
+        # and reads the whole input
+        f, bias = f[:args.share_cout], bias[:args.share_cout]
+        spec = dataclasses.replace(spec, cout=f.shape[0])
+        share = (share + "; " if share else "") + f"output channels 0..{f.shape[0] - 1} (channel split)"
     n, cin, cout, h, w = x.shape[0], spec.cin, spec.cout, spec.h, spec.w
     xa = x if layout == W.NCHW else np.ascontiguousarray(x.transpose(0, 2, 3, 1))
     xd = torch.from_numpy(xa).cuda()
@@ -534,7 +550,8 @@ def main():
         "metric": METRIC, "value": value, "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "int8" if args.bits == 8 else "int8/int10", "data": "synthetic",
-        "config": {"workload": f"{args.config}: {wl.desc}" + (f" (layer {args.layer})" if args.layer else ""),
+        "config": {"workload": f"{args.config}: {wl.desc}" + (f" (layer {args.layer})" if args.layer else "")
+                   + (f", one GPU's share: {share}" if share else ""),
                    "n": n, "cin": cin, "cout": cout, "h": h, "w": w,
                    "layout": args.layout, "variant": args.variant, "transform": args.transform,
                    "winograd_bits": args.bits, "tiles": T,
