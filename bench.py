@@ -176,7 +176,7 @@ def kernel_ms(torch, fn, calls):
     return min(med, time_loop(torch, fn, calls)), p10, p90
 
 
-def cpu_baseline(x, layers_plan, n_img, spec, target_s=10.0):
+def cpu_baseline(x, layers_plan, n_img, spec, layers_plan_f, target_s=10.0):
     """The oracle's online path (a-1 .. a-6, plan excluded) on images of the
     same workload, one at a time and cycling through the batch: n_img images
     if n_img > 0, else as many as fill target_s seconds of CPU work."""
@@ -196,7 +196,21 @@ def cpu_baseline(x, layers_plan, n_img, spec, target_s=10.0):
         dt += time.perf_counter() - t0
         done += 1
     ops = 2.0 * 9 * done * spec.h * spec.w * spec.cin * spec.cout
+    # the oracle's direct int8 convolution on the same images, a shorter sample
+    from oracle import direct
+    wq, _ = direct.quantize_weights_pow2(layers_plan_f)
+    ddone, ddt = 0, 0.0
+    while ddt < target_s / 4:
+        xs = np.ascontiguousarray(x[ddone % n:ddone % n + 1])
+        t0 = time.perf_counter()
+        direct.conv_int8(xs, wq, None, 8, False)
+        ddt += time.perf_counter() - t0
+        ddone += 1
+    dops = 2.0 * 9 * ddone * spec.h * spec.w * spec.cin * spec.cout
     return {"value": ops / dt / 1e12, "unit": "TOPS", "cores": int(threads), "kind": "oracle",
+            "direct_int8": {"value": dops / ddt / 1e12, "unit": "TOPS",
+                            "sample": f"{ddone} single-image passes of the oracle's direct int8 convolution "
+                                      f"(numpy int64), {ddt:.2f} s"},
             "sample": f"{done} single-image passes cycling over the {n} images of the same layer, full online "
                       f"path (numpy int64 transforms, float64 BLAS tap GEMM), {dt:.2f} s",
             "seconds": dt, "host_cpus": os.cpu_count(),
@@ -453,6 +467,14 @@ def main():
     eb_bytes = 2 if args.bits == 10 else 1                       # Vq / Uq element: int8 or fp16
     k1_bytes = n * h * w * cin + eb_bytes * ntap * T * cin      # read x, write Vq
     k2_bytes = eb_bytes * (ntap * T * cin + ntap * cin * cout) + n * h * w * cout + 4 * cout
+    # the whole layer against the HBM roofline: the bytes any implementation
+    # must move (x, y, Uq, bias) and the SPLIT path's extra Vq round trip
+    fused_min = n * h * w * cin + n * h * w * cout + eb_bytes * ntap * cin * cout + 4 * cout
+    split_bytes = fused_min + 2 * eb_bytes * ntap * T * cin
+    layer_hbm = {"alg_bytes_min": fused_min, "alg_bytes_split": split_bytes,
+                 "GB/s_split": split_bytes / (ms * 1e-3) / 1e9,
+                 "frac_split": split_bytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                 "frac_min": fused_min / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
     kernels = {}
     cfg_tag = args.config + (f"L{args.layer}" if args.layer else "") + ("_i10" if args.bits == 10 else "")
     if k1_ms is not None:
@@ -536,7 +558,7 @@ def main():
     if not args.no_cpu_baseline:
         from oracle import tapwise
         oplan = tapwise.make_plan(f, eb, bias=bias, out_shift=out_shift, relu=spec.relu)
-        cpu = cpu_baseline(x, oplan, args.cpu_images, spec)
+        cpu = cpu_baseline(x, oplan, args.cpu_images, spec, f)
 
     if args.copy_probe:
         src = torch.empty(256 << 20, dtype=torch.int8, device="cuda").fill_(1)
@@ -560,6 +582,7 @@ def main():
         "roofline": roofline,
         "kernels": kernels,
         "tap_gemm_mfma_frac_of_step": tap_ops / (ms * 1e-3) / 1e12 / k2_peak,
+        "layer_hbm": layer_hbm,
         "cold": {"step_ms": cold["step_ms"], "TOPS": direct_ops / (cold["step_ms"] * 1e-3) / 1e12,
                  "calls": ncold, "flush": "1 GiB read before each call (L2 and MALL evicted, clean)"},
         "measured_peaks": measured,
