@@ -430,9 +430,9 @@ def main():
     k1_sat = "true" if all(0 <= e <= 16 - args.bits for e in eb) else "false"
     if layout == W.NHWC and cin % 4 == 0:
         # NHWC with whole 4-channel words: the transform reads global memory directly
-        # tiles per block: 8 when that leaves fewer idle tiles per row than 16
+        # tiles per block: 8 unless 16 leaves fewer idle tiles per row
         twt = (w + mt - 1) // mt
-        k1_tx = 8 if (-twt) % 8 < (-twt) % 16 else 16
+        k1_tx = 8 if (-twt) % 8 <= (-twt) % 16 else 16
         k1_name, k1_inst = "wino_input_xform_nhwc", f"wino_input_xform_nhwc<{mt},{args.bits},{k1_tx},{k1_sat}>"
     else:
         k1_name, k1_inst = "wino_input_xform", f"wino_input_xform<{mt},{lay},0,{args.bits},16,{k1_sat}>"
