@@ -250,7 +250,7 @@ def run_chain(args):
                 torch.maximum(cols[:, :, :, 0], cols[:, :, :, 1], out=dst)
             pool()
             cur = dst
-        algo = W.wino_select_algorithm(n, spec.cin, spec.cout, spec.h, spec.w)
+        algo = W.wino_select_algorithm(n, spec.cin, spec.cout, spec.h, spec.w, W.NHWC)
         mt = 4 if algo == W.ALGO_F4 else 2
         picked.append({W.ALGO_F4: "f4", W.ALGO_F2: "f2", W.ALGO_DIRECT: "direct (ran f2)"}[algo])
         calibrate = W.wino_f4_calibrate_input if mt == 4 else W.wino_f2_calibrate_input

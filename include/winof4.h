@@ -142,15 +142,18 @@ wino_status wino_f4_plan_set_tap_kernel(wino_f4_plan_t plan, int32_t kind);
  * transforms and direct convolution (the paper's point that the best
  * algorithm depends on the layer, Sec. V: F2 for small spatial sizes, F4 for
  * large ones).  Host only, no device work; a fixed rule from measurements on
- * MI355X: DIRECT for layers below 2^27 direct-equivalent operations (there
- * the two Winograd launches cost more than the whole direct convolution);
- * F4 when its 64x64 row-streamed blocks, (Cout/64) x (tiles/64), fill the
- * device's compute units; F2 otherwise.
- *   algo: host int32 out, one of wino_algo.
- * Errors: WINO_EINVAL (null algo, sizes < 0 or channels < 1).
+ * MI355X: DIRECT for NHWC layers below 2^27 direct-equivalent operations
+ * (there the two Winograd launches cost more than the whole direct
+ * convolution; in NCHW the direct convolution runs a simple kernel that F2
+ * beats, so NCHW never gets DIRECT); F4 when its 64x64 row-streamed blocks,
+ * (Cout/64) x (tiles/64), fill the device's compute units; F2 otherwise.
+ *   layout: the activations' layout.
+ *   algo:   host int32 out, one of wino_algo.
+ * Errors: WINO_EINVAL (null algo, sizes < 0, channels < 1, unknown layout).
  */
 typedef enum wino_algo { WINO_ALGO_DIRECT = 0, WINO_ALGO_F2 = 2, WINO_ALGO_F4 = 4 } wino_algo;
-wino_status wino_select_algorithm(int32_t n, int32_t cin, int32_t cout, int32_t h, int32_t w, int32_t* algo);
+wino_status wino_select_algorithm(int32_t n, int32_t cin, int32_t cout, int32_t h, int32_t w,
+                                  wino_layout layout, int32_t* algo);
 
 /*
  * wino_f4_tap_kernel_choice -- the tap-GEMM kernel (WINO_TAP_ROWS or one of

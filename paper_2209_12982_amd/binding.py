@@ -84,7 +84,7 @@ def load_library():
         "wino_f4_plan_info": (I32, [P, P, P, P, P, P, P, P]),
         "wino_f4_plan_set_tap_kernel": (I32, [P, I32]),
         "wino_f4_tap_kernel_choice": (I32, [P, I32, I32, I32, P]),
-        "wino_select_algorithm": (I32, [I32, I32, I32, I32, I32, P]),
+        "wino_select_algorithm": (I32, [I32, I32, I32, I32, I32, I32, P]),
         "wino_f4_workspace_bytes": (SZ, [P, I32, I32, I32, I32]),
         "wino_f4_conv_int8": (I32, [P, P, P, I32, I32, I32, I32, I32, P, SZ, P]),
         "wino_f4_input_transform": (I32, [P, P, I32, I32, I32, I32, P, SZ, P]),
@@ -369,10 +369,11 @@ def wino_f4_tap_kernel_choice(plan, n, h, w):
     return kind.value
 
 
-def wino_select_algorithm(n, cin, cout, h, w):
-    """ALGO_DIRECT, ALGO_F2 or ALGO_F4 for a 3x3 layer of this shape."""
+def wino_select_algorithm(n, cin, cout, h, w, layout=NHWC):
+    """ALGO_DIRECT, ALGO_F2 or ALGO_F4 for a 3x3 layer of this shape and layout."""
     algo = ctypes.c_int32()
-    _check(load_library().wino_select_algorithm(n, cin, cout, h, w, ctypes.byref(algo)), "wino_select_algorithm")
+    _check(load_library().wino_select_algorithm(n, cin, cout, h, w, layout, ctypes.byref(algo)),
+           "wino_select_algorithm")
     return algo.value
 
 

@@ -137,8 +137,15 @@ def test_select_algorithm_on_configs():
         wl = workloads.WORKLOADS[name]
         got = [W.wino_select_algorithm(wl.n, s.cin, s.cout, s.h, s.w) for s in wl.layers]
         assert got == algos, name
+    # NCHW: the direct convolution there is the simple kernel, so small layers take F2
+    wl = workloads.WORKLOADS["C1"]
+    s = wl.layers[0]
+    assert W.wino_select_algorithm(wl.n, s.cin, s.cout, s.h, s.w, W.NCHW) == W.ALGO_F2
+    assert W.wino_select_algorithm(8, 64, 64, 56, 56, W.NCHW) == W.ALGO_F2
     with pytest.raises(W.WinoError):
         W.wino_select_algorithm(1, 0, 4, 8, 8)
+    with pytest.raises(W.WinoError):
+        W.wino_select_algorithm(1, 4, 4, 8, 8, 7)
 
 
 def test_direct_weight_quantization_matches_oracle():
