@@ -172,10 +172,10 @@ wino_status wino_f4_tap_kernel_choice(wino_f4_plan_t plan, int32_t n, int32_t h,
  * and exactness as for the F4 functions, except that in_exp, w_exp, e_g and
  * sh have 16 entries and uq is [16][cin][cout].  The resulting plan runs 4x4
  * input tiles at stride 2 and 2x2 output tiles through the same execution
- * entry points (wino_f4_conv_int8 SPLIT, wino_f4_workspace_bytes,
+ * entry points (wino_f4_conv_int8 SPLIT and FUSED, wino_f4_workspace_bytes,
  * wino_f4_input_transform, wino_f4_tap_gemm, wino_f4_calibrate_output, the
  * debug exports and wino_f4_plan_info, whose table arguments then hold 16
- * entries); the FUSED variant returns WINO_EUNSUPPORTED for it.
+ * entries).
  */
 wino_status wino_f2_plan(wino_f4_plan_t* out, const float* w_oihw, int32_t cin, int32_t cout,
                          const int8_t* in_exp, const int8_t* w_exp, const int32_t* bias,

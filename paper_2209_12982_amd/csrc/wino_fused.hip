@@ -1,19 +1,22 @@
-// FUSED variant of the online path: one launch per convolution.  Each
-// workgroup (8 waves, 64 output channels x 32 tiles) computes its tiles'
-// Winograd-domain input in the GEMM prologue, so the tap-major Vq never goes
-// to memory (the input transform of Sec. IV-B2's operator dataflow feeding
-// the Cube from on-chip memory).  Per 64-channel k step:
-//   1. each thread takes two (tile, channel pair) items: it loads the 6x6
+// FUSED variant of the online path: one launch per convolution, for F4 and
+// F2 plans.  Each workgroup (8 waves, 64 output channels x 32 tiles) computes
+// its tiles' Winograd-domain input in the GEMM prologue, so the tap-major Vq
+// never goes to memory (the input transform of Sec. IV-B2's operator dataflow
+// feeding the Cube from on-chip memory).  Per 64-channel k step:
+//   1. each thread takes two (tile, channel pair) items: it loads the N x N
 //      window of two channels, computes B^T d B in two 16-bit lanes and the
-//      tap-wise requantization, and writes the 36 resulting byte pairs into
-//      the LDS Vq block [36 taps][32 tiles][64 B] (two channels at a time
-//      keeps the transform next to the 144 accumulators within 256 VGPRs);
-//   2. the 36 tap MFMAs read Vq from LDS and Uq from a three-stage ring that
-//      the direct-to-LDS load keeps filled (the ring also loads while step 1
+//      tap-wise requantization, and writes the NTAP resulting byte pairs into
+//      the LDS Vq block [NTAP taps][32 tiles][64 B] (two channels at a time
+//      keeps the transform next to the accumulators: 144 registers for F4's
+//      36 taps, 64 for F2's 16);
+//   2. the tap MFMAs read Vq from LDS and Uq from a three-stage ring that the
+//      direct-to-LDS load keeps filled (the ring also loads while step 1
 //      runs);
 // then the same fused output-transform epilogue as the SPLIT tap GEMM.
 // The input transform is recomputed once per 64-output-channel block
-// (Cout/64 times in all), so this variant pays off when Cout is small.
+// (Cout/64 times in all), so this variant pays off when Cout is small.  F2's
+// workgroup needs 80 KB of LDS and at most 128 registers a lane, so two run
+// on a CU.
 #include "wino_device.h"
 
 using namespace winof4;
@@ -24,14 +27,22 @@ constexpr int K4_CO = 64;
 constexpr int K4_TL = 32;
 constexpr int K4_THREADS = 512;
 constexpr int K4_WAVES = K4_THREADS / 64;
-constexpr int K4_G = 6;                                  // taps per A stage
-constexpr int K4_A_STAGE = K4_G * K4_CO * 64;            // 24 KB
 constexpr int K4_NBUF = 3;
-constexpr int K4_B_BYTES = kTaps * K4_TL * 64;           // 72 KB
-constexpr int K4_LPW = K4_A_STAGE / 1024 / K4_WAVES;     // 3
-static_assert(K4_A_STAGE / 1024 % K4_WAVES == 0, "A stage loads split evenly");
-static_assert(K4_B_BYTES + K4_NBUF * K4_A_STAGE <= 160 * 1024, "LDS");
 static_assert(K4_TL * 32 == 2 * K4_THREADS, "two (tile, channel pair) items per thread per k step");
+
+template <int M>
+struct K4Cfg {
+    static constexpr int N = Wino<M>::N, NT = Wino<M>::NTAP;
+    static constexpr int G = M == 4 ? 6 : 4;                 // taps per Uq ring stage
+    static constexpr int A_STAGE = G * K4_CO * 64;           // 24 KB (F4), 16 KB (F2)
+    static constexpr int B_BYTES = NT * K4_TL * 64;          // Vq block: 72 KB, 32 KB
+    static constexpr int LPW = A_STAGE / 1024 / K4_WAVES;    // 1-KB loads per wave per stage
+    static constexpr int LDS = B_BYTES + K4_NBUF * A_STAGE;
+    static constexpr int WAVES_PER_EU = M == 4 ? 1 : 4;     // F2: two workgroups per CU
+    static_assert(NT % G == 0 && A_STAGE / 1024 % K4_WAVES == 0, "stages tile the taps; loads split evenly");
+    static_assert(K4_WAVES * LPW == 4 * G, "wave -> (tap, 16-row group) map of the ring loads");
+    static_assert(LDS <= 160 * 1024 && (M == 4 || 2 * LDS <= 160 * 1024), "LDS");
+};
 
 struct K4Args {
     int cin, cin_pad, cout, cout_pad;
@@ -66,13 +77,16 @@ __device__ __forceinline__ v2s load_pair(const int8_t* __restrict__ x, const K4A
     return __builtin_bit_cast(v2s, __builtin_amdgcn_perm(0u, u, 0x010c000cu)) >> splat(8);
 }
 
-template <int LAYOUT, int EPI>
-__global__ __launch_bounds__(K4_THREADS) void wino_fused(const int8_t* __restrict__ x, const int8_t* __restrict__ uq,
-                                                         const int32_t* __restrict__ bias, int8_t* __restrict__ y,
-                                                         K4Args g) {
-    __shared__ __attribute__((aligned(1024))) uint8_t lds[K4_B_BYTES + K4_NBUF * K4_A_STAGE];
+template <int M, int LAYOUT, int EPI>
+__global__ __launch_bounds__(K4_THREADS, K4Cfg<M>::WAVES_PER_EU) void wino_fused(const int8_t* __restrict__ x,
+                                                                               const int8_t* __restrict__ uq,
+                                                                               const int32_t* __restrict__ bias,
+                                                                               int8_t* __restrict__ y, K4Args g) {
+    using C = K4Cfg<M>;
+    constexpr int N = C::N, NT = C::NT, G = C::G, NGRP = NT / G;
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[C::LDS];
     uint8_t* const ldsB = lds;
-    uint8_t* const ldsA = lds + K4_B_BYTES;
+    uint8_t* const ldsA = lds + C::B_BYTES;
     const int lbid = xcd_remap(blockIdx.x, g.nblocks);
     const int bco = lbid % g.nbco, btl = lbid / g.nbco;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -100,26 +114,27 @@ __global__ __launch_bounds__(K4_THREADS) void wino_fused(const int8_t* __restric
         it_off[k] = tl * 64 + 16 * lds_slot(tl, (2 * pr) >> 4) + ((2 * pr) & 15);
     }
 
-    // Uq ring: this wave's three 1-KB load instructions per stage
+    // Uq ring: this wave's 1-KB load instructions per stage; load j copies
+    // 16 rows (group j % 4) of the stage's tap j / 4
     const long long sa = (long long)g.cout_pad * g.cin_pad;   // tap stride
     const long long ka = (long long)g.cout_pad * kKStep;      // k-block stride
-    const int8_t* src[K4_LPW];
-    int dst[K4_LPW];
+    const int8_t* src[C::LPW];
+    int dst[C::LPW];
 #pragma unroll
-    for (int i = 0; i < K4_LPW; ++i) {
+    for (int i = 0; i < C::LPW; ++i) {
         const int j = wave + K4_WAVES * i;
         const int u = j >> 2, row = 16 * (j & 3) + (lane >> 2);
         src[i] = uq + u * sa + (long long)(co_blk + row) * kKStep + 16 * lds_slot(row, lane & 3);
         dst[i] = j * 1024;
     }
     const int nkc = g.cin_pad / kKStep;
-    const int nst = nkc * (kTaps / K4_G);
+    const int nst = nkc * NGRP;
     auto issue = [&](int st) {
-        const int kc = st / (kTaps / K4_G), grp = st - kc * (kTaps / K4_G);
-        const long long off = (long long)(K4_G * grp) * sa + kc * ka;
-        uint8_t* base = ldsA + (st % K4_NBUF) * K4_A_STAGE;
+        const int kc = st / NGRP, grp = st - kc * NGRP;
+        const long long off = (long long)(G * grp) * sa + kc * ka;
+        uint8_t* base = ldsA + (st % K4_NBUF) * C::A_STAGE;
 #pragma unroll
-        for (int i = 0; i < K4_LPW; ++i)
+        for (int i = 0; i < C::LPW; ++i)
             __builtin_amdgcn_global_load_lds((const void*)(src[i] + off),
                                              (__attribute__((address_space(3))) void*)(base + dst[i]), 16, 0, 0);
     };
@@ -128,9 +143,9 @@ __global__ __launch_bounds__(K4_THREADS) void wino_fused(const int8_t* __restric
     const int frag_a = row_a * 64 + 16 * lds_slot(row_a, lk);
     const int frag_b = row_b * 64 + 16 * lds_slot(row_b, lk);
 
-    v4i acc[kTaps];
+    v4i acc[NT];
 #pragma unroll
-    for (int t = 0; t < kTaps; ++t) acc[t] = (v4i){0, 0, 0, 0};
+    for (int t = 0; t < NT; ++t) acc[t] = (v4i){0, 0, 0, 0};
 
     issue(0);
     if (nst > 1) issue(1);
@@ -139,53 +154,53 @@ __global__ __launch_bounds__(K4_THREADS) void wino_fused(const int8_t* __restric
         // (one item at a time: only one window's registers live next to acc)
 #pragma unroll 1
         for (int k = 0; k < 2; ++k) {
-            v2s v[6][6];
+            v2s v[N][N];
 #pragma unroll
-            for (int r = 0; r < 6; ++r)
+            for (int r = 0; r < N; ++r)
 #pragma unroll
-                for (int c = 0; c < 6; ++c)
-                    v[r][c] = it_ok[k] ? load_pair<LAYOUT>(x, g, it_img[k], 4 * it_ty[k] - 1 + r, 4 * it_tx[k] - 1 + c,
+                for (int c = 0; c < N; ++c)
+                    v[r][c] = it_ok[k] ? load_pair<LAYOUT>(x, g, it_img[k], M * it_ty[k] - 1 + r, M * it_tx[k] - 1 + c,
                                                            kc * kKStep + it_c[k])
                                        : splat(0);
             const v2s two = splat(2), four = splat(4);
 #pragma unroll
-            for (int c = 0; c < 6; ++c) {      // columns: B^T d
-                v2s col[6], res[6];
+            for (int c = 0; c < N; ++c) {      // columns: B^T d
+                v2s col[N], res[N];
 #pragma unroll
-                for (int r = 0; r < 6; ++r) col[r] = v[r][c];
-                bt_1d(col, res, two, four);
+                for (int r = 0; r < N; ++r) col[r] = v[r][c];
+                Wino<M>::bt(col, res, two, four);
 #pragma unroll
-                for (int r = 0; r < 6; ++r) v[r][c] = res[r];
+                for (int r = 0; r < N; ++r) v[r][c] = res[r];
             }
 #pragma unroll
-            for (int r = 0; r < 6; ++r) {      // rows: (B^T d) B
-                v2s res[6];
-                bt_1d(v[r], res, two, four);
+            for (int r = 0; r < N; ++r) {      // rows: (B^T d) B
+                v2s res[N];
+                Wino<M>::bt(v[r], res, two, four);
 #pragma unroll
-                for (int c = 0; c < 6; ++c) v[r][c] = res[c];
+                for (int c = 0; c < N; ++c) v[r][c] = res[c];
             }
 #pragma unroll
-            for (int t = 0; t < kTaps; ++t) {
+            for (int t = 0; t < NT; ++t) {
                 const int e = g.tab.eb[t];
-                v2s q = (v[t / 6][t % 6] + splat(e ? (1 << (e - 1)) : 0)) >> splat(e);
+                v2s q = (v[t / N][t % N] + splat(e ? (1 << (e - 1)) : 0)) >> splat(e);
                 q = __builtin_elementwise_min(__builtin_elementwise_max(q, splat(-128)), splat(127));
                 *(uint16_t*)(ldsB + t * K4_TL * 64 + it_off[k]) =
                     (uint16_t)__builtin_amdgcn_perm(0u, __builtin_bit_cast(uint32_t, q), 0x0c0c0200u);
             }
         }
         __syncthreads();
-        // 2. the 36 tap MFMAs of this k step
+        // 2. the tap MFMAs of this k step
 #pragma unroll
-        for (int grp = 0; grp < kTaps / K4_G; ++grp) {
-            const int st = kc * (kTaps / K4_G) + grp;
-            if (st + 1 < nst) WINO_WAIT_VM(K4_LPW);   // stage st done, st + 1 may be in flight
+        for (int grp = 0; grp < NGRP; ++grp) {
+            const int st = kc * NGRP + grp;
+            if (st + 1 < nst) WINO_WAIT_VM(C::LPW);   // stage st done, st + 1 may be in flight
             else WINO_WAIT_VM(0);
             ring_barrier();
             if (st + 2 < nst) issue(st + 2);
-            const uint8_t* abase = ldsA + (st % K4_NBUF) * K4_A_STAGE;
+            const uint8_t* abase = ldsA + (st % K4_NBUF) * C::A_STAGE;
 #pragma unroll
-            for (int u = 0; u < K4_G; ++u) {
-                const int t = K4_G * grp + u;
+            for (int u = 0; u < G; ++u) {
+                const int t = G * grp + u;
                 v4i av = *(const v4i*)(abase + frag_a + u * K4_CO * 64);
                 v4i bv = *(const v4i*)(ldsB + frag_b + t * K4_TL * 64);
                 acc[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bv, acc[t], 0, 0, 0);
@@ -193,7 +208,23 @@ __global__ __launch_bounds__(K4_THREADS) void wino_fused(const int8_t* __restric
         }
         __syncthreads();   // every wave is done with this Vq block
     }
-    tap_epilogue<4, LAYOUT, EPI, 0>(acc, g, bias, y, nullptr, co_blk + 16 * cw, tl_blk + 16 * tw, lane);
+    tap_epilogue<M, LAYOUT, EPI, 0>(acc, g, bias, y, nullptr, co_blk + 16 * cw, tl_blk + 16 * tw, lane);
+}
+
+template <int M>
+void launch_fused(wino_layout layout, int epi_bits, dim3 grid, dim3 block, hipStream_t stream, const int8_t* x,
+                  const wino_f4_plan_s* p, int8_t* y, const K4Args& a) {
+    if (layout == WINO_NHWC) {
+        if (epi_bits == 32)
+            hipLaunchKernelGGL((wino_fused<M, WINO_NHWC, 32>), grid, block, 0, stream, x, p->uq_dev, p->bias_dev, y, a);
+        else
+            hipLaunchKernelGGL((wino_fused<M, WINO_NHWC, 64>), grid, block, 0, stream, x, p->uq_dev, p->bias_dev, y, a);
+    } else {
+        if (epi_bits == 32)
+            hipLaunchKernelGGL((wino_fused<M, WINO_NCHW, 32>), grid, block, 0, stream, x, p->uq_dev, p->bias_dev, y, a);
+        else
+            hipLaunchKernelGGL((wino_fused<M, WINO_NCHW, 64>), grid, block, 0, stream, x, p->uq_dev, p->bias_dev, y, a);
+    }
 }
 
 }  // namespace
@@ -208,8 +239,9 @@ wino_status wino_f4_conv_fused(const wino_f4_plan_s* p, const int8_t* x, int8_t*
     a.n = n;
     a.h = h;
     a.w = w;
-    a.th = (h + 3) / 4;
-    a.tw = (w + 3) / 4;
+    const int m = p->m;
+    a.th = (h + m - 1) / m;
+    a.tw = (w + m - 1) / m;
     a.ntiles = (long long)n * a.th * a.tw;
     if (a.ntiles == 0) return WINO_OK;
     a.dimg = make_fastdiv((uint32_t)(a.th * a.tw));
@@ -226,16 +258,7 @@ wino_status wino_f4_conv_fused(const wino_f4_plan_s* p, const int8_t* x, int8_t*
         a.tab.sh[i] = p->sh[i];
     }
     dim3 grid((unsigned)blocks), block(K4_THREADS);
-    if (layout == WINO_NHWC) {
-        if (p->epi_bits == 32)
-            hipLaunchKernelGGL((wino_fused<WINO_NHWC, 32>), grid, block, 0, stream, x, p->uq_dev, p->bias_dev, y, a);
-        else
-            hipLaunchKernelGGL((wino_fused<WINO_NHWC, 64>), grid, block, 0, stream, x, p->uq_dev, p->bias_dev, y, a);
-    } else {
-        if (p->epi_bits == 32)
-            hipLaunchKernelGGL((wino_fused<WINO_NCHW, 32>), grid, block, 0, stream, x, p->uq_dev, p->bias_dev, y, a);
-        else
-            hipLaunchKernelGGL((wino_fused<WINO_NCHW, 64>), grid, block, 0, stream, x, p->uq_dev, p->bias_dev, y, a);
-    }
+    if (m == 4) launch_fused<4>(layout, p->epi_bits, grid, block, stream, x, p, y, a);
+    else launch_fused<2>(layout, p->epi_bits, grid, block, stream, x, p, y, a);
     return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
 }

@@ -1411,7 +1411,7 @@ extern "C" wino_status wino_f4_conv_int8(wino_f4_plan_t p, const int8_t* x, int8
     if (variant != WINO_SPLIT && variant != WINO_FUSED) return WINO_EINVAL;
     if (g.ntiles == 0) return WINO_OK;
     if (variant == WINO_FUSED) {
-        if (p->m != 4 || p->bits != 8) return WINO_EUNSUPPORTED;
+        if (p->bits != 8) return WINO_EUNSUPPORTED;
         return wino_f4_conv_fused(p, x, y, n, h, w, layout, stream);
     }
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;

@@ -93,7 +93,8 @@ def test_binding_refuses_buffers_a_kernel_cannot_use():
 @pytest.mark.parametrize("make,m", [(W.wino_f4_plan, 4), (W.wino_f2_plan, 2), (W.wino_f4_plan_i10, 4)])
 def test_deep_channels_bitexact(make, m):
     """2048 input channels (32 k-chunks) and 96 output channels on a ragged
-    9 x 7 image: long accumulations and padded output channels."""
+    9 x 7 image: long accumulations and padded output channels, SPLIT and
+    (8-bit plans) FUSED."""
     n, cin, cout, h, w = 1, 2048, 96, 9, 7
     x, f, b = workloads.random_case(71, n, cin, cout, h, w, signed=True)
     bits = 10 if make is W.wino_f4_plan_i10 else 8
@@ -102,6 +103,8 @@ def test_deep_channels_bitexact(make, m):
     ref = tapwise.conv_int8(x, tapwise.make_plan(f, eb, bias=b, out_shift=11, m=m, bits=bits))
     for layout in (W.NCHW, W.NHWC):
         assert (run_conv(plan, x, layout) == ref).all()
+        if bits == 8:
+            assert (run_conv(plan, x, layout, W.FUSED) == ref).all()
 
 
 @pytest.mark.parametrize("shape,macs", [(16, 8 * 16 * 16 * 64), (32, 4 * 32 * 32 * 32)])

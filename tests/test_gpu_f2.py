@@ -1,5 +1,6 @@
 """GPU parity of the F(2x2, 3x3) path (plans from wino_f2_plan) through the C
-ABI against the oracle's F2 pipeline, bit for bit."""
+ABI against the oracle's F2 pipeline, bit for bit, for both variants (SPLIT:
+input transform to a workspace, then the tap GEMM; FUSED: one kernel)."""
 import numpy as np
 import pytest
 
@@ -65,29 +66,31 @@ def test_f2_tap_gemm_bitexact(shape, layout):
     assert (m.cpu().numpy().astype(np.int64) == ref).all()
 
 
+@pytest.mark.parametrize("variant", [W.SPLIT, W.FUSED])
 @pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("shape", SHAPES)
 @pytest.mark.parametrize("relu,out_shift", [(False, 7), (True, 10), (False, 0)])
-def test_f2_conv_bitexact_random(shape, layout, relu, out_shift):
+def test_f2_conv_bitexact_random(shape, layout, relu, out_shift, variant):
     n, cin, cout, h, w = shape
     x, f, b = workloads.random_case(25, n, cin, cout, h, w, signed=True)
     eb = tapwise.calibrate_input_exps(x, m=2)
     gp, op = _pair(f, eb, b, out_shift, relu)
     assert W.wino_f4_plan_info(gp)["epilogue_bits"] == 32
-    y = run_conv(gp, x, layout)
+    y = run_conv(gp, x, layout, variant)
     ref = tapwise.conv_int8(x, op)
     assert (y == ref).all(), f"{(y != ref).sum()} mismatches"
 
 
+@pytest.mark.parametrize("variant", [W.SPLIT, W.FUSED])
 @pytest.mark.parametrize("layout", LAYOUTS)
-def test_f2_conv_int64_epilogue(layout):
+def test_f2_conv_int64_epilogue(layout, variant):
     n, cin, cout, h, w = 1, 20, 24, 11, 10
     x, f, b = workloads.random_case(26, n, cin, cout, h, w, signed=True)
     eb = [0] * 16
     eb[15], eb[0] = 15, 14
     gp, op = _pair(f, eb, b, 20, False)
     assert W.wino_f4_plan_info(gp)["epilogue_bits"] == 64
-    assert (run_conv(gp, x, layout) == tapwise.conv_int8(x, op)).all()
+    assert (run_conv(gp, x, layout, variant) == tapwise.conv_int8(x, op)).all()
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
@@ -114,18 +117,22 @@ def test_f2_calibrate_output_matches_oracle(layout):
     assert s == tapwise.calibrate_out_shift(x, op)
 
 
-def test_f2_fused_is_unsupported():
+def test_f2_i10_fused_is_unsupported():
+    """The FUSED kernel has no 10-bit form; an int8/10 F2 plan is refused
+    before any launch and the output is left alone."""
     torch = torch_dev()
     f = np.zeros((4, 4, 3, 3), np.float32)
-    gp = W.wino_f2_plan(f, [0] * 16)
+    gp = W.wino_f2_plan_i10(f, [0] * 16)
     x = torch.zeros((1, 4, 8, 8), dtype=torch.int8, device="cuda")
-    y = torch.zeros((1, 4, 8, 8), dtype=torch.int8, device="cuda")
+    y = torch.full((1, 4, 8, 8), 7, dtype=torch.int8, device="cuda")
     with pytest.raises(W.WinoError) as e:
         W.wino_f4_conv_int8(gp, x, y, 1, 8, 8, W.NCHW, W.FUSED)
     assert e.value.status == -2
+    torch.cuda.synchronize()
+    assert (y.cpu().numpy() == 7).all()
 
 
-def _config_layer(x, f, b, spec, layout):
+def _config_layer(x, f, b, spec, layout, variant=W.SPLIT):
     """Calibrate (GPU) and run one layer with an F2 plan; returns GPU output
     and the oracle's for the same tables."""
     torch = torch_dev()
@@ -144,22 +151,25 @@ def _config_layer(x, f, b, spec, layout):
     op = tapwise.make_plan(f, eb, bias=b, out_shift=s, relu=spec.relu, m=2)
     shape = (n, spec.cout, h, w) if layout == W.NCHW else (n, h, w, spec.cout)
     y = torch.full(shape, 77, dtype=torch.int8, device="cuda")
-    W.wino_f4_conv_int8(plan, xd, y, n, h, w, layout, W.SPLIT, workspace(plan, n, h, w))
+    ws = workspace(plan, n, h, w) if variant == W.SPLIT else None
+    W.wino_f4_conv_int8(plan, xd, y, n, h, w, layout, variant, ws)
     torch.cuda.synchronize()
     return from_device_nchw(y, layout), tapwise.conv_int8(x, op)
 
 
+@pytest.mark.parametrize("variant", [W.SPLIT, W.FUSED])
 @pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("name", ["C1", "C2"])
-def test_f2_config_bitexact(name, layout):
+def test_f2_config_bitexact(name, layout, variant):
     x, layers = workloads.generate(name)
     f, b, spec = layers[0]
-    y, ref = _config_layer(x, f, b, spec, layout)
+    y, ref = _config_layer(x, f, b, spec, layout, variant)
     assert (y == ref).all()
 
 
+@pytest.mark.parametrize("variant", [W.SPLIT, W.FUSED])
 @pytest.mark.parametrize("layout", LAYOUTS)
-def test_f2_c3_chain_bitexact(layout):
+def test_f2_c3_chain_bitexact(layout, variant):
     """The four chained C3 layers with F2 plans, each fed the GPU's own
     previous output (max-pooled where the stage halves the image)."""
     x, layers = workloads.generate("C3")
@@ -167,6 +177,6 @@ def test_f2_c3_chain_bitexact(layout):
     for k, (f, b, spec) in enumerate(layers):
         if k > 0:
             cur = workloads.next_layer_input(cur, spec)
-        y, ref = _config_layer(cur, f, b, spec, layout)
+        y, ref = _config_layer(cur, f, b, spec, layout, variant)
         assert (y == ref).all(), f"layer {k}"
         cur = y
