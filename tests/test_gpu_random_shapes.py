@@ -21,7 +21,7 @@ pytestmark = pytest.mark.gpu
 KERNELS_F4 = [W.TAP_AUTO, W.TAP_ROWS, W.TAP_RESIDENT_64X32, W.TAP_RESIDENT_32X32, W.TAP_RESIDENT_16X16]
 
 
-@settings(max_examples=80, deadline=None, derandomize=True)
+@settings(max_examples=160, deadline=None, derandomize=True)
 @given(n=st.integers(1, 3), cin=st.integers(1, 150), cout=st.integers(1, 140), h=st.integers(1, 37),
        w=st.integers(1, 37), layout=st.sampled_from([W.NCHW, W.NHWC]), m=st.sampled_from([4, 2]),
        variant=st.sampled_from([W.SPLIT, W.FUSED]), kernel=st.sampled_from(KERNELS_F4), relu=st.booleans(),
