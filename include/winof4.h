@@ -67,15 +67,19 @@ typedef struct wino_f4_plan_s* wino_f4_plan_t;   /* opaque, immutable after crea
  * 64 channels x 32 tiles (RESIDENT, RESIDENT_64X32), 32 x 32 or 16 x 16 (the
  * _NxM values force a shape).  ROWS streams the taps one row of the 6x6 tile
  * at a time and folds each row into the output as it completes, which allows
- * 64 x 64 blocks.  AUTO picks ROWS when its blocks fill the device and the
- * 32-bit epilogue applies, else RESIDENT_64X32.                             */
+ * 64 x 64 blocks.  WAVES (F4, 8-bit, 32-bit epilogue; forced only) splits a
+ * 64 x 64 block between four 32x32x32-MFMA waves and eight waves that copy
+ * operands and keep the output rows, persistent over the blocks.  AUTO picks
+ * ROWS when its blocks fill the device and the 32-bit epilogue applies, else
+ * RESIDENT_64X32.                                                            */
 typedef enum wino_tap_kernel {
     WINO_TAP_AUTO = 0,
     WINO_TAP_RESIDENT = 1,
     WINO_TAP_ROWS = 2,
     WINO_TAP_RESIDENT_64X32 = 3,
     WINO_TAP_RESIDENT_32X32 = 4,
-    WINO_TAP_RESIDENT_16X16 = 5
+    WINO_TAP_RESIDENT_16X16 = 5,
+    WINO_TAP_WAVES = 6
 } wino_tap_kernel;
 
 /*
@@ -156,8 +160,8 @@ wino_status wino_select_algorithm(int32_t n, int32_t cin, int32_t cout, int32_t 
                                   wino_layout layout, int32_t* algo);
 
 /*
- * wino_f4_tap_kernel_choice -- the tap-GEMM kernel (WINO_TAP_ROWS or one of
- * the WINO_TAP_RESIDENT_* shapes) that a SPLIT wino_f4_conv_int8 runs for an
+ * wino_f4_tap_kernel_choice -- the tap-GEMM kernel (WINO_TAP_ROWS, WINO_TAP_WAVES
+ * or one of the WINO_TAP_RESIDENT_* shapes) that a SPLIT wino_f4_conv_int8 runs for an
  * n x h x w input, under the plan's wino_f4_plan_set_tap_kernel setting.
  * Host only, no device work.  kind: host int32 out.
  * Errors: WINO_EINVAL (null plan or kind, negative sizes), WINO_EUNSUPPORTED

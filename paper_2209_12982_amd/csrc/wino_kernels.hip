@@ -389,6 +389,7 @@ struct K2Args {
     int y_staged;              // row-streamed kernel: stage NHWC output through LDS
     FastDiv dimg, dtw;         // division by th * tw and by tw (tile coordinates)
     TapTables tab;
+    uint32_t shrow[6];         // sh of row a's six taps, 5 bits each (wave-specialized kernel)
 };
 
 // MODE 0: store y.  MODE 1: max |Y + bias| into *zmax (calibration).
@@ -876,6 +877,8 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
     for (int tb = 0; tb < KR_TB; ++tb) store_tile<LAYOUT>(yv[tb], g, y, co0, tl_blk + 16 * (KR_TB * tw + tb) + lr);
 }
 
+#include "wino_tap_ws.h"
+
 // ---------------------------------------------------------------------------
 // K2W wino_tap_gemm_rows_wide: the row-streamed scheme of wino_tap_gemm_rows
 // for the int8/10 operands (Q = 10: fp16 holding 10-bit integers, 32
@@ -1215,10 +1218,27 @@ int tap_kernel_for(const wino_f4_plan_s* p, const Geometry& g, int mode) {
     // F2: its own 64x32 configuration
     if (mode != 0 || p->m != 4 || p->bits != 8) return WINO_TAP_RESIDENT_64X32;
     if (k == WINO_TAP_RESIDENT_64X32 || k == WINO_TAP_RESIDENT_32X32 || k == WINO_TAP_RESIDENT_16X16) return k;
+    // the wave-specialized kernel (forced only: measured slower than ROWS on
+    // every layer here) packs the alignment shifts in 5 bits, which the
+    // 32-bit epilogue bound keeps far below 32
+    if (p->epi_bits == 32 && k == WINO_TAP_WAVES) {
+        bool sh5 = true;
+        for (int t = 0; t < p->ntap; ++t) sh5 = sh5 && p->sh[t] >= 0 && p->sh[t] < 32;
+        return sh5 ? WINO_TAP_WAVES : WINO_TAP_ROWS;
+    }
     if (p->epi_bits == 32 && k != WINO_TAP_RESIDENT &&
         (k == WINO_TAP_ROWS || (long long)(p->cout_pad / KR_CO) * (g.t_pad / KR_TL) >= num_cus()))
         return WINO_TAP_ROWS;
     return WINO_TAP_RESIDENT_64X32;
+}
+
+// 64-channel chunks per ring stage of the wave-specialized kernel: the
+// largest of 4, 3, 2, 1 that divides the padded input channels' chunks
+int ws_chunks_per_stage(int cin_pad) {
+    const int nkc = cin_pad / kKStep;
+    for (int nk = 4; nk > 1; --nk)
+        if (nkc % nk == 0) return nk;
+    return 1;
 }
 
 template <class C, int M, int MODE, int Q = 8>
@@ -1284,6 +1304,10 @@ wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout la
     a.dimg = make_fastdiv((uint32_t)(g.th * g.tw));
     a.dtw = make_fastdiv((uint32_t)g.tw);
     a.tab = tables_of(p);
+    for (int r = 0; r < 6; ++r) {
+        a.shrow[r] = 0;
+        for (int b = 0; b < 6 && 6 * r + b < p->ntap; ++b) a.shrow[r] |= (uint32_t)(p->sh[6 * r + b] & 31) << (5 * b);
+    }
     if (p->bits == 10) {
         if (p->m == 2) return launch_resident<K2F2_10, 2, MODE, 10>(p, g, layout, vq, y, aux, a, stream);
         switch (tap_kernel_for(p, g, MODE)) {
@@ -1315,6 +1339,34 @@ wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout la
                 hipLaunchKernelGGL(wino_tap_gemm_rows<WINO_NCHW>, dim3((unsigned)rblocks), dim3(KR_THREADS), 0,
                                    stream, p->uq_dev, vq, p->bias_dev, y, a);
             return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
+        }
+        case WINO_TAP_WAVES: {
+            const long long wblocks = (long long)(p->cout_pad / WS_CO) * (g.t_pad / WS_TL);
+            if (wblocks > 0x7fffffffll) return WINO_EUNSUPPORTED;
+            a.nbco = p->cout_pad / WS_CO;
+            a.nblocks = (int)wblocks;
+            // persistent: at most one workgroup per CU, each walking its blocks
+            const dim3 grid((unsigned)std::min<long long>(wblocks, num_cus())), block(WS_THREADS);
+#define WS_LAUNCH(L, NK) \
+    hipLaunchKernelGGL((wino_tap_gemm_ws<L, NK>), grid, block, 0, stream, p->uq_dev, vq, p->bias_dev, y, a)
+#define WS_LAUNCH_NK(L)                            \
+    switch (ws_chunks_per_stage(p->cin_pad)) {     \
+        case 4: WS_LAUNCH(L, 4); break;            \
+        case 3: WS_LAUNCH(L, 3); break;            \
+        case 2: WS_LAUNCH(L, 2); break;            \
+        default: WS_LAUNCH(L, 1); break;           \
+    }
+            if constexpr (MODE == 0) {
+                if (layout == WINO_NHWC) {
+                    WS_LAUNCH_NK(WINO_NHWC);
+                } else {
+                    WS_LAUNCH_NK(WINO_NCHW);
+                }
+#undef WS_LAUNCH_NK
+#undef WS_LAUNCH
+                return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
+            }
+            break;
         }
         case WINO_TAP_RESIDENT_32X32:
             if constexpr (MODE == 0) return launch_resident<K2Mid, 4, MODE>(p, g, layout, vq, y, aux, a, stream);

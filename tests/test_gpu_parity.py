@@ -141,6 +141,38 @@ def test_conv_rows_kernel_bitexact(shape, layout, relu, out_shift):
     assert (y == ref).all(), f"{(y != ref).sum()} mismatches"
 
 
+# shapes for the wave-specialized tap GEMM: ring stages of 1..4 k-chunks
+# (input channels 64, 128, 192, 256 padded), several stages per tap (320:
+# five one-chunk stages, 512: two four-chunk stages), ragged tiles and
+# channel counts that leave partial 64-blocks, images smaller than a tile
+WAVES_SHAPES = SHAPES + [
+    (1, 256, 200, 21, 26),
+    (2, 192, 64, 9, 40),
+    (1, 320, 128, 16, 16),
+    (3, 128, 72, 14, 14),
+    (1, 512, 64, 12, 20),
+    (2, 64, 130, 3, 2),
+    (1, 33, 256, 40, 8),
+]
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("shape", WAVES_SHAPES)
+@pytest.mark.parametrize("relu,out_shift", [(False, 9), (True, 12), (False, 0)])
+def test_conv_waves_kernel_bitexact(shape, layout, relu, out_shift):
+    """The wave-specialized tap GEMM (MFMA waves + fold waves), forced on
+    every shape."""
+    n, cin, cout, h, w = shape
+    x, f, b = workloads.random_case(7, n, cin, cout, h, w, signed=True)
+    eb = tapwise.calibrate_input_exps(x)
+    gp, op = _plan_pair(f, eb, b, out_shift, relu)
+    W.wino_f4_plan_set_tap_kernel(gp, W.TAP_WAVES)
+    assert W.wino_f4_tap_kernel_choice(gp, n, h, w) == W.TAP_WAVES
+    y = run_conv(gp, x, layout, W.SPLIT)
+    ref = tapwise.conv_int8(x, op)
+    assert (y == ref).all(), f"{(y != ref).sum()} mismatches"
+
+
 def test_tap_kernel_choice():
     torch_dev()
     f = np.random.default_rng(9).normal(0, 0.05, (256, 256, 3, 3)).astype(np.float32)
@@ -152,6 +184,9 @@ def test_tap_kernel_choice():
     assert W.wino_f4_tap_kernel_choice(plan, 4, 160, 160) == W.TAP_RESIDENT_64X32
     W.wino_f4_plan_set_tap_kernel(plan, W.TAP_ROWS)
     assert W.wino_f4_tap_kernel_choice(plan, 1, 56, 56) == W.TAP_ROWS
+    assert W.wino_f4_tap_kernel_choice(plan, 4, 160, 160) == W.TAP_ROWS
+    W.wino_f4_plan_set_tap_kernel(plan, W.TAP_WAVES)
+    assert W.wino_f4_tap_kernel_choice(plan, 1, 56, 56) == W.TAP_WAVES
     for kind in (W.TAP_RESIDENT_64X32, W.TAP_RESIDENT_32X32, W.TAP_RESIDENT_16X16):
         W.wino_f4_plan_set_tap_kernel(plan, kind)
         assert W.wino_f4_tap_kernel_choice(plan, 4, 160, 160) == kind
@@ -162,8 +197,9 @@ def test_tap_kernel_choice():
     eb[35], eb[0] = 15, 14
     p64 = W.wino_f4_plan(f[:24, :20], eb, bias=None, out_shift=20)
     assert W.wino_f4_plan_info(p64)["epilogue_bits"] == 64
-    W.wino_f4_plan_set_tap_kernel(p64, W.TAP_ROWS)
-    assert W.wino_f4_tap_kernel_choice(p64, 4, 160, 160) == W.TAP_RESIDENT_64X32
+    for kind in (W.TAP_ROWS, W.TAP_WAVES):
+        W.wino_f4_plan_set_tap_kernel(p64, kind)
+        assert W.wino_f4_tap_kernel_choice(p64, 4, 160, 160) == W.TAP_RESIDENT_64X32
 
 
 @pytest.mark.parametrize("kind", [W.TAP_RESIDENT_32X32, W.TAP_RESIDENT_16X16])

@@ -18,7 +18,8 @@ from hypothesis import given, settings, strategies as st  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
-KERNELS_F4 = [W.TAP_AUTO, W.TAP_ROWS, W.TAP_RESIDENT_64X32, W.TAP_RESIDENT_32X32, W.TAP_RESIDENT_16X16]
+KERNELS_F4 = [W.TAP_AUTO, W.TAP_ROWS, W.TAP_WAVES, W.TAP_RESIDENT_64X32, W.TAP_RESIDENT_32X32,
+              W.TAP_RESIDENT_16X16]
 
 
 @settings(max_examples=160, deadline=None, derandomize=True)
