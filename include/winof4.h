@@ -317,6 +317,28 @@ wino_status wino_f4_conv_int8(wino_f4_plan_t plan, const int8_t* x, int8_t* y, i
                               void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * wino_f4_conv_int8_noalloc -- wino_f4_conv_int8 (SPLIT) for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  It allocates nothing and takes no
+ * workspace: the input-transform workspace is a file-scope device array of
+ * WINO_NOALLOC_SCRATCH_BYTES (64 MiB) that each GPU the library runs on holds
+ * until the process ends; its address is looked up once per device, on the
+ * first call made with that device current.
+ *
+ *   plan, x, y, n, h, w, layout, stream: as for wino_f4_conv_int8.
+ * Every call on one GPU shares that GPU's array and leaves its contents
+ * behind (nothing in it needs clearing): calls that overlap on one GPU, e.g.
+ * on two streams without ordering between them, race and must not be made.
+ * Errors: as for wino_f4_conv_int8 (SPLIT), and WINO_EWORKSPACE when the
+ * layer's workspace, wino_f4_workspace_bytes(plan, n, h, w, WINO_SPLIT),
+ * exceeds WINO_NOALLOC_SCRATCH_BYTES (checked before any device work);
+ * WINO_EHIP if the array's address cannot be obtained.
+ */
+#define WINO_NOALLOC_SCRATCH_BYTES (64u << 20)
+wino_status wino_f4_conv_int8_noalloc(wino_f4_plan_t plan, const int8_t* x, int8_t* y, int32_t n,
+                                      int32_t h, int32_t w, wino_layout layout, hipStream_t stream);
+
+/*
  * The two launches of the SPLIT variant as separate calls, for callers that
  * schedule or time them individually; wino_f4_conv_int8(SPLIT) equals
  * wino_f4_input_transform followed by wino_f4_tap_gemm on the same stream.

@@ -17,7 +17,7 @@ from .binding import (  # noqa: F401
     wino_f4_plan_i10, wino_f2_plan_i10, wino_f4_plan_tables_i10, wino_f2_plan_tables_i10,
     wino_f4_calibrate_input_i10, wino_f2_calibrate_input_i10,
     wino_f4_plan_set_tap_kernel, wino_f4_tap_kernel_choice, wino_select_algorithm,
-    wino_f4_workspace_bytes, wino_f4_conv_int8,
+    wino_f4_workspace_bytes, wino_f4_conv_int8, wino_f4_conv_int8_noalloc, NOALLOC_SCRATCH_BYTES,
     wino_f4_input_transform, wino_f4_tap_gemm,
     wino_f4_calibrate_input, wino_f4_calibrate_output,
     wino_f4_debug_input_transform, wino_f4_debug_tap_gemm,

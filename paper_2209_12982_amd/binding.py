@@ -13,6 +13,7 @@ SPLIT, FUSED = 0, 1
 TAP_AUTO, TAP_RESIDENT, TAP_ROWS = 0, 1, 2
 TAP_RESIDENT_64X32, TAP_RESIDENT_32X32, TAP_RESIDENT_16X16 = 3, 4, 5
 TAP_WAVES = 6
+NOALLOC_SCRATCH_BYTES = 64 << 20   # WINO_NOALLOC_SCRATCH_BYTES
 ALGO_DIRECT, ALGO_F2, ALGO_F4 = 0, 2, 4
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -26,7 +27,7 @@ EXPORTS = [
     "wino_f4_calibrate_input_i10", "wino_f2_calibrate_input_i10",
     "wino_f4_plan_set_tap_kernel", "wino_f4_tap_kernel_choice", "wino_select_algorithm",
     "wino_f4_workspace_bytes",
-    "wino_f4_conv_int8", "wino_f4_input_transform", "wino_f4_tap_gemm", "wino_f4_calibrate_input", "wino_f4_calibrate_output",
+    "wino_f4_conv_int8", "wino_f4_conv_int8_noalloc", "wino_f4_input_transform", "wino_f4_tap_gemm", "wino_f4_calibrate_input", "wino_f4_calibrate_output",
     "wino_f4_debug_input_transform", "wino_f4_debug_tap_gemm",
     "direct_conv_quantize_weights", "direct_conv_int8", "wino_f4_conv_float", "wino_probe_mfma_int8", "wino_strerror",
 ]
@@ -88,6 +89,7 @@ def load_library():
         "wino_select_algorithm": (I32, [I32, I32, I32, I32, I32, I32, P]),
         "wino_f4_workspace_bytes": (SZ, [P, I32, I32, I32, I32]),
         "wino_f4_conv_int8": (I32, [P, P, P, I32, I32, I32, I32, I32, P, SZ, P]),
+        "wino_f4_conv_int8_noalloc": (I32, [P, P, P, I32, I32, I32, I32, P]),
         "wino_f4_input_transform": (I32, [P, P, I32, I32, I32, I32, P, SZ, P]),
         "wino_f4_tap_gemm": (I32, [P, P, SZ, P, I32, I32, I32, I32, P]),
         "wino_f4_calibrate_input": (I32, [P, I32, I32, I32, I32, I32, P, P, P]),
@@ -390,6 +392,17 @@ def wino_f4_conv_int8(plan, x, y, n, h, w, layout=NCHW, variant=SPLIT, workspace
                                _dptr(y, torch.int8, _elems(n, plan.cout, h, w), "y"), n, h, w, layout, variant,
                                _dptr(workspace, None, 0, "workspace"), ws_bytes, _stream(stream))
     _check(st, "wino_f4_conv_int8")
+
+
+def wino_f4_conv_int8_noalloc(plan, x, y, n, h, w, layout=NCHW, stream=None):
+    """SPLIT convolution with the library's own device scratch (allocates
+    nothing; workspace up to NOALLOC_SCRATCH_BYTES)."""
+    lib = load_library()
+    import torch
+    st = lib.wino_f4_conv_int8_noalloc(plan.handle, _dptr(x, torch.int8, _elems(n, plan.cin, h, w), "x"),
+                                       _dptr(y, torch.int8, _elems(n, plan.cout, h, w), "y"), n, h, w, layout,
+                                       _stream(stream))
+    _check(st, "wino_f4_conv_int8_noalloc")
 
 
 def wino_f4_input_transform(plan, x, n, h, w, layout, workspace, stream=None):

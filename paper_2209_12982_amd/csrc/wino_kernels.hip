@@ -24,6 +24,7 @@
 // otherwise in 64-bit.
 #include <algorithm>
 #include <atomic>
+#include <mutex>
 #include "wino_device.h"
 
 using namespace winof4;
@@ -1467,6 +1468,56 @@ extern "C" wino_status wino_f4_conv_int8(wino_f4_plan_t p, const int8_t* x, int8
         return wino_f4_conv_fused(p, x, y, n, h, w, layout, stream);
     }
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
+    int8_t* vq = (int8_t*)ws;
+    st = run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p), p->bits), layout, x, vq, nullptr, stream);
+    if (st != WINO_OK) return st;
+    return launch_k2<0>(p, g, layout, vq, y, nullptr, stream);
+}
+
+// ---------------------------------------------------------------------------
+// The SPLIT convolution without allocation: the input-transform workspace
+// (Vq) lives in a file-scope device array instead of caller memory.  Each
+// device holds its own copy of the array for the life of the process; its
+// address is looked up once per device (first call on that device, with the
+// device current) and kept.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) uint8_t scratch[WINO_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+std::mutex g_scratch_mu;
+std::atomic<void*> g_scratch_ptr[64];   // per device id
+
+wino_status scratch_for_device(int dev, void** out) {
+    if (dev < 0 || dev >= 64) return WINO_EUNSUPPORTED;
+    void* q = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (!q) {
+        std::lock_guard<std::mutex> lk(g_scratch_mu);
+        q = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+        if (!q) {
+            // the device current now is `dev` (the caller checked it)
+            if (hipGetSymbolAddress(&q, HIP_SYMBOL(scratch)) != hipSuccess || !q) return WINO_EHIP;
+            g_scratch_ptr[dev].store(q, std::memory_order_release);
+        }
+    }
+    *out = q;
+    return WINO_OK;
+}
+}  // namespace
+
+extern "C" wino_status wino_f4_conv_int8_noalloc(wino_f4_plan_t p, const int8_t* x, int8_t* y, int32_t n,
+                                                 int32_t h, int32_t w, wino_layout layout, hipStream_t stream) {
+    Geometry g;
+    wino_status st = check_common(p, x, n, h, w, layout, g);
+    if (st != WINO_OK) return st;
+    if (!y) return WINO_EINVAL;
+    if (g.ntiles == 0) return WINO_OK;
+    if (vq_bytes(p, g) > (size_t)WINO_NOALLOC_SCRATCH_BYTES) return WINO_EWORKSPACE;
+    void* ws = nullptr;
+    st = scratch_for_device(p->device, &ws);
+    if (st != WINO_OK) return st;
+    // K1 writes every Vq byte that K2 reads into a nonzero product (padded
+    // channels meet zero Uq rows, padded tiles are never stored), so the
+    // scratch needs no clearing between calls
     int8_t* vq = (int8_t*)ws;
     st = run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p), p->bits), layout, x, vq, nullptr, stream);
     if (st != WINO_OK) return st;
