@@ -276,7 +276,10 @@ void wino_f4_plan_destroy(wino_f4_plan_t plan);
  * wino_f4_plan_info -- the plan's tables, for inspection and parity tests.
  * Any output pointer may be NULL.  e_g, sh: host int8 [36]; e_o: host int32;
  * epilogue_bits: 32 or 64; uq: host int8 [36][cin][cout] (tap-major,
- * Uq[t][ci][co]); cin/cout: the plan's channel counts.
+ * Uq[t][ci][co]); cin/cout: the plan's channel counts.  The last two outputs
+ * extend the six-argument form: a caller holding only the handle (a plan made
+ * on the device, or by another module) can size the uq buffer from them
+ * before asking for it.
  */
 wino_status wino_f4_plan_info(wino_f4_plan_t plan, int8_t* e_g, int8_t* sh, int32_t* e_o,
                               int32_t* epilogue_bits, int8_t* uq, int32_t* cin, int32_t* cout);
@@ -433,6 +436,11 @@ wino_status direct_conv_quantize_weights(const float* w_oihw, int32_t cout, int3
  * 2^out_shift), -128, 127), optional ReLU.  Same geometry and layouts as
  * wino_f4_conv_int8.
  *   w_ohwi  device int8 [cout][3][3][cin];  bias: device int32 [cout] or NULL.
+ *           OHWI rather than OIHW: the implicit GEMM's reduction index is
+ *           (ky, kx, ci), so each output channel's 9*cin weights are one
+ *           contiguous row that the kernel streams in 16-byte pieces next to
+ *           NHWC pixels.  direct_conv_quantize_weights writes this order from
+ *           fp32 OIHW; an OIHW int8 tensor becomes it by a permute (0, 2, 3, 1).
  *   1 <= cin <= 8192 (keeps the int32 accumulator exact), 1 <= cout <= 65536,
  *   out_shift in [0, 31], relu 0|1.  Asynchronous on `stream`.
  */
@@ -460,20 +468,6 @@ wino_status direct_conv_int8(const int8_t* x, const int8_t* w_ohwi, const int32_
 wino_status wino_f4_conv_float(const int8_t* x, const float* w_oihw, float* y, int32_t n,
                                int32_t cin, int32_t cout, int32_t h, int32_t w,
                                wino_layout layout, hipStream_t stream);
-
-/*
- * wino_probe_mfma_int8 -- measurement probe, not part of the convolution:
- * `blocks` workgroups of four waves issue independent int8 MFMAs only
- * (shape 16: v_mfma_i32_16x16x64_i8, eight chains per wave; shape 32:
- * v_mfma_i32_32x32x32_i8, four chains), `iters` rounds each, so that a
- * caller timing the launch measures the int8 matrix-core rate at the run's
- * clock.  *ops (host) receives the launch's operation count (2 per
- * multiply-add).  sink: device int32, never written in practice (it keeps
- * the results live).  Asynchronous on `stream`; WINO_EINVAL for a bad shape
- * or count or a NULL pointer.
- */
-wino_status wino_probe_mfma_int8(int32_t shape, int32_t iters, int32_t blocks, int32_t* sink,
-                                 int64_t* ops, hipStream_t stream);
 
 /* Static description of a status code; never NULL. */
 const char* wino_strerror(wino_status status);

@@ -29,8 +29,10 @@ EXPORTS = [
     "wino_f4_workspace_bytes",
     "wino_f4_conv_int8", "wino_f4_conv_int8_noalloc", "wino_f4_input_transform", "wino_f4_tap_gemm", "wino_f4_calibrate_input", "wino_f4_calibrate_output",
     "wino_f4_debug_input_transform", "wino_f4_debug_tap_gemm",
-    "direct_conv_quantize_weights", "direct_conv_int8", "wino_f4_conv_float", "wino_probe_mfma_int8", "wino_strerror",
+    "direct_conv_quantize_weights", "direct_conv_int8", "wino_f4_conv_float", "wino_strerror",
 ]
+# include/winof4_probe.h: the measurement probe, outside the method's interface.
+PROBE_EXPORTS = ["wino_probe_mfma_int8"]
 
 
 class LibraryNotBuilt(RuntimeError):

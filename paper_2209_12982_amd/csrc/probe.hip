@@ -5,7 +5,7 @@
 
 #include <cstdint>
 
-#include "winof4.h"
+#include "winof4_probe.h"
 
 namespace {
 

@@ -339,6 +339,45 @@ def test_config_c1_bitexact(layout):
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
+def test_config_c1_calibrated_shift_bitexact(layout):
+    """C1 with the output shift calibrated like C2-C5 (max |Y + bias| on the
+    layer's own input) instead of the literal 8: the GPU's calibration must
+    pick the oracle's shift and the layer must match byte for byte."""
+    x, layers = workloads.generate("C1")
+    f, b, spec = layers[0]
+    n = x.shape[0]
+    xd = to_device(x, layout)
+    eb, _ = W.wino_f4_calibrate_input(xd, n, spec.cin, spec.h, spec.w, layout)
+    assert eb == tapwise.calibrate_input_exps(x)
+    gp0 = W.wino_f4_plan(f, eb, bias=b)
+    s, _ = W.wino_f4_calibrate_output(gp0, xd, n, spec.h, spec.w, layout, workspace(gp0, n, spec.h, spec.w))
+    s_ref = tapwise.calibrate_out_shift(x, tapwise.make_plan(f, eb, bias=b, out_shift=0))
+    assert s == s_ref and s != 8
+    gp, op = _plan_pair(f, eb, b, s, False)
+    y = run_conv(gp, x, layout)
+    assert (y == tapwise.conv_int8(x, op)).all()
+
+
+def test_tap_gemm_export_full_channels():
+    """The raw tap-GEMM result M (no output transform) on one image of the
+    C5 layer, all 256 -> 256 channels: every int32 of the 36 x 1600 x 256
+    export against the oracle's tap-major GEMM."""
+    torch = torch_dev()
+    x, layers = workloads.generate("C5")
+    f, b, spec = layers[0]
+    x1 = np.ascontiguousarray(x[:1])
+    eb = tapwise.calibrate_input_exps(x1)
+    gp, op = _plan_pair(f, eb, b, 0, False)
+    h, w = spec.h, spec.w
+    th, tw = tapwise.tile_grid(h, w)
+    m = torch.empty((36, th * tw, spec.cout), dtype=torch.int32, device="cuda")
+    W.wino_f4_debug_tap_gemm(gp, to_device(x1, W.NHWC), 1, h, w, W.NHWC, m, workspace(gp, 1, h, w))
+    torch.cuda.synchronize()
+    ref = tapwise.tap_gemm(tapwise.input_taps_quantized(x1, eb), op["uq"])
+    assert (m.cpu().numpy().astype(np.int64) == ref).all()
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
 def test_config_c2_bitexact(layout):
     x, layers = workloads.generate("C2")
     f, b, spec = layers[0]

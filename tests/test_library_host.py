@@ -22,14 +22,25 @@ def _lib():
         pytest.skip("library not built")
 
 
+def _declared(header):
+    hdr = open(os.path.join(ROOT, "include", header)).read()
+    return re.findall(r"^\s*(?:wino_status|size_t|void|const char\*)\s+(\w+)\s*\(", hdr, re.M)
+
+
 def test_exports_every_declared_symbol():
+    """The method's header and the binding's EXPORTS list the same functions,
+    the measurement header and PROBE_EXPORTS likewise, the two sets are
+    disjoint, every header under include/ is one of the two, and the built
+    library resolves every name."""
     lib = _lib()
-    hdr = open(os.path.join(ROOT, "include", "winof4.h")).read()
-    declared = re.findall(r"^\s*(?:wino_status|size_t|void|const char\*)\s+(\w+)\s*\(", hdr, re.M)
-    assert len(declared) >= 12
-    for name in declared:
+    assert sorted(os.listdir(os.path.join(ROOT, "include"))) == ["winof4.h", "winof4_probe.h"]
+    method, probe = _declared("winof4.h"), _declared("winof4_probe.h")
+    assert len(method) >= 12 and probe
+    assert sorted(method) == sorted(W.binding.EXPORTS)
+    assert sorted(probe) == sorted(W.binding.PROBE_EXPORTS)
+    assert not set(method) & set(probe)
+    for name in method + probe:
         assert hasattr(lib, name), name
-    assert sorted(declared) == sorted(W.binding.EXPORTS)
 
 
 @pytest.mark.parametrize("name", ["C1", "C2", "C3"])
