@@ -97,6 +97,16 @@ def draw_weights(rng, spec):
     return f.astype(np.float32)
 
 
+def channel_scaled(f, seed, sigma=0.5):
+    """The weights f [cout, cin, 3, 3] with each output channel multiplied by
+    its own log-normal factor exp(N(0, sigma^2)), drawn from default_rng(seed)
+    in channel order.  Trained networks' output channels differ in scale, the
+    property channel-wise quantization exploits; i.i.d. draws lack it."""
+    rng = np.random.default_rng(seed)
+    k = np.exp(rng.normal(0.0, sigma, f.shape[0]))
+    return (f.astype(np.float64) * k[:, None, None, None]).astype(np.float32)
+
+
 def draw_bias(rng, spec):
     return rng.integers(-spec.bias_range, spec.bias_range + 1, spec.cout).astype(np.int32)
 
