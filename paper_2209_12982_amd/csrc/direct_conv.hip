@@ -154,30 +154,51 @@ __global__ __launch_bounds__(DC_THREADS) void direct_conv_kernel(const int8_t* _
 }
 
 // ---------------------------------------------------------------------------
-// Fast path (NHWC, Cin % 64 == 0): 32x32x32 int8 MFMA implicit GEMM.
-// Rows = output channels (A = weights [cout][9][cin]), columns = pixels (B =
-// the implicit im2col), k = (kernel position, 64-channel block).  A
-// workgroup (8 waves) computes 128 channels x 256 pixels; wave w owns
-// channels 64*(w%2).. and pixels 64*(w/2).. as 2x2 blocks of 32x32.  Each k
-// step's A (128 rows x 64 B) and B (256 rows x 64 B) slices are copied
-// global -> LDS with buffer loads straight into LDS, four stages in flight.
-// A pixel outside the image (the 3x3 halo's zero padding) or beyond the
-// batch gets an offset past the buffer's end, which the buffer load turns
-// into zeros; the same holds for channels beyond Cout in the weights.
-// LDS rows hold their 16-byte parts at slot p ^ ((row >> 1) & 3).
+// Fast path (NHWC, Cin % 64 == 0): 32x32x32 int8 MFMA implicit GEMM over
+// spatial tiles.
+// Rows = output channels (A = weights [cout][9][cin]), columns = the pixels
+// of an 8 x 32 output tile (B = the implicit im2col), k = (64-channel block,
+// kernel position).  A workgroup computes 256 channels x 256 pixels: per k
+// step 4.2 M multiply-adds.  The nine kernel positions read the same input
+// pixels shifted by (dr, ds), so B is not copied per position: the tile's
+// 10 x 34 input window (its 3x3 halo) is copied into LDS once per
+// 64-channel block and each position reads its 8 x 32 pixels at the shifted
+// window rows.  Per block and channel block that moves 16 KB of weights per
+// position plus one 21 KB window, against 9 x (16 + 16) KB when every
+// position copies its own pixel slice.
+//
+// LDS: a ring of four 16-KB weight slices (three in flight) and two input
+// windows (the next channel block's window lands while the current one is
+// read).  Wave w owns channels 64*(w%4).. and tile rows 2*(w/4), 2*(w/4)+1 as
+// 2 x 2 blocks of 32x32.  Window pixels outside the image (the zero
+// padding) and channels beyond Cout in the weights get an offset past the
+// buffer's end, which the buffer load turns into zeros.  LDS rows (64 B)
+// hold their 16-byte parts at slot p ^ ((row >> 1) & 3).
 // ---------------------------------------------------------------------------
-constexpr int DF_CO = 128, DF_PX = 256, DF_THREADS = 512, DF_NBUF = 4, DF_LPW = 3;
-constexpr int DF_A = DF_CO * 64;
-constexpr int DF_B = DF_PX * 64;
-constexpr int DF_STAGE = DF_A + DF_B;
+constexpr int DF_CO = 256, DF_TH = 8, DF_TW = 32, DF_PX = DF_TH * DF_TW;
+constexpr int DF_WH = DF_TH + 2, DF_WW = DF_TW + 2, DF_WROWS = DF_WH * DF_WW;     // input window: 10 x 34
+constexpr int DF_WAVES = 16, DF_THREADS = 64 * DF_WAVES;
+constexpr int DF_ABUF = 4;                                                       // weight slices
+constexpr int DF_A = DF_CO * 64;                                                 // one slice, 16 KB
+constexpr int DF_WINSTR = (DF_WROWS + 15) / 16;                                  // 1-KB loads per window: 22
+constexpr int DF_WLPW = (DF_WINSTR + DF_WAVES - 1) / DF_WAVES;                   // per wave: 2
+constexpr int DF_WIN = DF_WINSTR * 1024;                                         // window bytes (22 KB)
+constexpr int DF_JUNK = DF_ABUF * DF_A + 2 * DF_WIN;                             // sink of the spare window loads
+constexpr int DF_BIAS = DF_JUNK + 1024;                                         // the block's bias, int32 [256]
+constexpr int DF_NARROW = DF_BIAS + 4 * DF_CO;                                   // per channel: bias fits 32 bits
+constexpr int DF_LDS = DF_NARROW + DF_CO;
+static_assert(DF_A / 1024 == DF_WAVES, "one weight load per wave and stage");
+static_assert(DF_LDS <= 160 * 1024, "LDS");
+static_assert((DF_CO / 64) * (DF_PX / 64) == DF_WAVES, "waves tile the block");
 
 typedef int v16i __attribute__((ext_vector_type(16)));
 
 struct DFArgs {
     int n, cin, cout, h, w;
-    int npix, nbco, nblocks, nkb;
+    int tiles_x, tiles_y, nbco, nblocks, nkb;
     int out_shift, relu;
     int x_bytes, w_bytes;
+    int bias_lim;   // acc + bias + rounding fits int32 when |bias| <= bias_lim (-1: never)
 };
 
 __device__ __forceinline__ int df_slot(int row, int part) { return part ^ ((row >> 1) & 3); }
@@ -187,98 +208,113 @@ __device__ __forceinline__ void df_barrier() {
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
 }
-#define DF_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(0x0f70 | (n))
+#define DF_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(0x0070 | (n))   // vmcnt(n) lgkmcnt(0)
 
 __global__ __launch_bounds__(DF_THREADS) void direct_conv_nhwc_mfma(const int8_t* __restrict__ x,
                                                                    const int8_t* __restrict__ wt,
                                                                    const int32_t* __restrict__ bias,
                                                                    int8_t* __restrict__ y, DFArgs g) {
-    __shared__ __attribute__((aligned(1024))) uint8_t lds[DF_NBUF * DF_STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[DF_LDS];
     const int lbid = xcd_remap(blockIdx.x, g.nblocks);
-    const int bco = lbid % g.nbco, bpx = lbid / g.nbco;
+    const int bco = lbid % g.nbco, bt = lbid / g.nbco;
+    const int tiles = g.tiles_x * g.tiles_y;
+    const int img = bt / tiles, trem = bt - img * tiles;
+    const int ty0 = (trem / g.tiles_x) * DF_TH, tx0 = (trem % g.tiles_x) * DF_TW;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int co_blk = bco * DF_CO, px_blk = bpx * DF_PX;
+    const int co_blk = bco * DF_CO;
     const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc((void*)x, 0, g.x_bytes, 0x00020000);
     const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc((void*)wt, 0, g.w_bytes, 0x00020000);
     const int wrow = 9 * g.cin;
+    const int rr = lane >> 2, sl = lane & 3;
 
-    // this wave's three 1-KB load instructions per stage
-    int rowi[DF_LPW], parti[DF_LPW], dsti[DF_LPW];
-    bool isa[DF_LPW];
-    int pimg[DF_LPW], ph[DF_LPW], pw_[DF_LPW];
+    // weight slice: this wave copies rows 16 w .. 16 w + 15 of the 256
+    const int arow = 16 * wave + rr;
+    const int acol = 16 * df_slot(arow, sl);
+    const int aoff = co_blk + arow < g.cout ? (co_blk + arow) * wrow + acol : -1;
+
+    // input window: load i of this wave covers window rows 16 j .. 16 j + 15,
+    // j = w + 16 i; loads past the window's 22 write zeros to a junk row
+    int woff[DF_WLPW], wdst[DF_WLPW];
 #pragma unroll
-    for (int i = 0; i < DF_LPW; ++i) {
-        const int j = wave + 8 * i;                   // 0..23
-        const int rr = lane >> 2, slot = lane & 3;
-        isa[i] = j < DF_A / 1024;
-        const int row = isa[i] ? 16 * j + rr : 16 * (j - DF_A / 1024) + rr;
-        rowi[i] = row;
-        parti[i] = df_slot(row, slot);
-        dsti[i] = j * 1024;
-        const int p = px_blk + row;
-        const int pp = p < g.npix ? p : 0;
-        pimg[i] = pp / (g.h * g.w);
-        const int rem = pp - pimg[i] * g.h * g.w;
-        ph[i] = p < g.npix ? rem / g.w : -100000;      // marks a pixel beyond the batch
-        pw_[i] = rem - (rem / g.w) * g.w;
+    for (int i = 0; i < DF_WLPW; ++i) {
+        const int j = wave + DF_WAVES * i;
+        const int row = 16 * j + rr;
+        wdst[i] = j < DF_WINSTR ? 1024 * j : -1;
+        const int wy = row / DF_WW, wx = row - (row / DF_WW) * DF_WW;
+        const int iy = ty0 - 1 + wy, ix = tx0 - 1 + wx;
+        const bool ok = row < DF_WROWS && iy >= 0 && iy < g.h && ix >= 0 && ix < g.w;
+        woff[i] = ok ? ((img * g.h + iy) * g.w + ix) * g.cin + 16 * df_slot(row, sl) : -1;
     }
-    const int nst = 9 * g.nkb;
-    auto issue = [&](int st) {
-        const int rs = st / g.nkb, cb = st - rs * g.nkb;
-        const int dr = rs / 3 - 1, ds = rs % 3 - 1;
-        const int ci0 = cb * 64;
-        uint8_t* base = lds + (st & (DF_NBUF - 1)) * DF_STAGE;
+    // the block's 256 bias values, read once here: loaded in the epilogue they
+    // would cost a global round trip per channel group after the main loop
+    if (tid < DF_CO) {
+        const int co = co_blk + tid;
+        const int bv = bias && co < g.cout ? bias[co] : 0;
+        ((int*)(lds + DF_BIAS))[tid] = bv;
+        lds[DF_NARROW + tid] = bv >= -g.bias_lim && bv <= g.bias_lim;
+    }
+    const int nst = 9 * g.nkb;                 // stage t: channel block t / 9, position t % 9
+    auto issue = [&](int t) {
+        const int kb = t / 9, rs = t - 9 * kb;
+        uint8_t* abuf = lds + (t & (DF_ABUF - 1)) * DF_A;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (__attribute__((address_space(3))) void*)(abuf + 1024 * wave), 16,
+                                                 aoff >= 0 ? aoff + rs * g.cin + kb * 64 : 0x7fffffff, 0, 0, 0);
+        if (rs == 0) {
+            uint8_t* wbuf = lds + DF_ABUF * DF_A + (kb & 1) * DF_WIN;
 #pragma unroll
-        for (int i = 0; i < DF_LPW; ++i) {
-            int off;
-            if (isa[i]) {
-                const int co = co_blk + rowi[i];
-                off = co < g.cout ? co * wrow + rs * g.cin + ci0 + 16 * parti[i] : 0x7fffffff;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (__attribute__((address_space(3))) void*)(base + dsti[i]),
-                                                         16, off, 0, 0, 0);
-            } else {
-                const int hh = ph[i] + dr, ww = pw_[i] + ds;
-                const bool ok = hh >= 0 && hh < g.h && ww >= 0 && ww < g.w;
-                off = ok ? ((pimg[i] * g.h + hh) * g.w + ww) * g.cin + ci0 + 16 * parti[i] : 0x7fffffff;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (__attribute__((address_space(3))) void*)(base + dsti[i]),
-                                                         16, off, 0, 0, 0);
-            }
+            for (int i = 0; i < DF_WLPW; ++i)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rx, (__attribute__((address_space(3))) void*)(wdst[i] >= 0 ? wbuf + wdst[i] : lds + DF_JUNK), 16,
+                    woff[i] >= 0 ? woff[i] + kb * 64 : 0x7fffffff, 0, 0, 0);
         }
     };
+    auto loads_of = [&](int t) { return t >= nst ? 0 : (t % 9 == 0 ? 1 + DF_WLPW : 1); };
 
-    const int cw = wave & 1, pwv = wave >> 1;
+    const int cw = wave & 3, pwv = wave >> 2;
     const int l32 = lane & 31, lh = lane >> 5;
     v16i acc[2][2];
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
         for (int b = 0; b < 2; ++b) acc[a][b] = (v16i){};
-    int fa[2][2], fb[2][2];                   // [block][k half] LDS offsets
+    int fa[2][2];                              // [block][k half] offsets in a weight slice
 #pragma unroll
     for (int q = 0; q < 2; ++q)
 #pragma unroll
         for (int kh = 0; kh < 2; ++kh) {
-            const int ra = 64 * cw + 32 * q + l32, rb = 64 * pwv + 32 * q + l32;
+            const int ra = 64 * cw + 32 * q + l32;
             fa[q][kh] = ra * 64 + 16 * df_slot(ra, 2 * kh + lh);
-            fb[q][kh] = DF_A + rb * 64 + 16 * df_slot(rb, 2 * kh + lh);
         }
+    // window row of this lane's pixel in block q at position (0, 0)
+    int wr0[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) wr0[q] = (2 * pwv + q) * DF_WW + l32;
 
-    for (int st = 0; st < DF_NBUF - 1 && st < nst; ++st) issue(st);
-    for (int st = 0; st < nst; ++st) {
-        const int ahead = nst - 1 - st;
-        if (ahead >= 2) DF_WAIT_VM(2 * DF_LPW);
-        else if (ahead == 1) DF_WAIT_VM(DF_LPW);
-        else DF_WAIT_VM(0);
+    for (int t = 0; t < 3 && t < nst; ++t) issue(t);
+    for (int t = 0; t < nst; ++t) {
+        // stage t's loads have landed once only stages t+1, t+2 are pending
+        const int later = loads_of(t + 1) + loads_of(t + 2);
+        switch (later) {
+            case 0: DF_WAIT_VM(0); break;
+            case 1: DF_WAIT_VM(1); break;
+            case 2: DF_WAIT_VM(2); break;
+            case 3: DF_WAIT_VM(3); break;
+            default: DF_WAIT_VM(4); break;
+        }
         df_barrier();
-        if (st + DF_NBUF - 1 < nst) issue(st + DF_NBUF - 1);
-        const uint8_t* base = lds + (st & (DF_NBUF - 1)) * DF_STAGE;
+        if (t + 3 < nst) issue(t + 3);
+        const int kb = t / 9, rs = t - 9 * kb;
+        const int dr = rs / 3, ds = rs - 3 * (rs / 3);           // window offsets 0..2
+        const uint8_t* abuf = lds + (t & (DF_ABUF - 1)) * DF_A;
+        const uint8_t* wbuf = lds + DF_ABUF * DF_A + (kb & 1) * DF_WIN;
 #pragma unroll
         for (int kh = 0; kh < 2; ++kh) {
             v4i av[2], bv[2];
 #pragma unroll
             for (int q = 0; q < 2; ++q) {
-                av[q] = *(const v4i*)(base + fa[q][kh]);
-                bv[q] = *(const v4i*)(base + fb[q][kh]);
+                av[q] = *(const v4i*)(abuf + fa[q][kh]);
+                const int row = wr0[q] + dr * DF_WW + ds;
+                bv[q] = *(const v4i*)(wbuf + row * 64 + 16 * df_slot(row, 2 * kh + lh));
             }
 #pragma unroll
             for (int a = 0; a < 2; ++a)
@@ -288,38 +324,68 @@ __global__ __launch_bounds__(DF_THREADS) void direct_conv_nhwc_mfma(const int8_t
         }
     }
 
-    // accumulator layout (32x32 block): lane holds column l32 (a pixel) and
-    // rows 8*(r/4) + 4*lh + r%4 (output channels) for r = 0..15
+    // Epilogue.  The accumulator of a 32x32 block gives each lane one pixel
+    // (column l32) and 16 channels 8*(r/4) + 4*lh + r%4; stored from there,
+    // one instruction would touch 32 pixels' lines with 8 bytes each.  The
+    // block's 256 x 256 output bytes are staged in LDS instead (pixel-major,
+    // 272-byte pitch against bank conflicts) and leave as 16-byte pieces, 16
+    // lanes per pixel: whole 256-byte pixel rows of NHWC.
     const int s = g.out_shift;
     const int rnd = s > 0 ? 1 << (s - 1) : 0;
     const int lo = g.relu ? 0 : -128;
+    constexpr int OP = 272;
+    static_assert(DF_PX * OP <= DF_LDS, "output staging fits the ring");
+    // whether every bias of the block keeps acc + bias + rounding inside
+    // int32 (|acc| <= 9 cin 2^14), so that the requantization can run in
+    // 32-bit arithmetic: one byte per channel, written before the main loop's
+    // barriers; lane l reads channels 4l .. 4l+3
+    const bool narrow = __ballot(*(const uint32_t*)(lds + DF_NARROW + 4 * lane) != 0x01010101u) == 0;
+    __syncthreads();                            // every wave is done reading the ring
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-        const int p = px_blk + 64 * pwv + 32 * b + l32;
-        if (p >= g.npix) continue;
-        int8_t* yp = y + (long long)p * g.cout;
+    for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+        for (int r4 = 0; r4 < 4; ++r4) {
+            const int cl = 64 * cw + 32 * a + 8 * r4 + 4 * lh;      // block-local channel
+            const v4i bv4 = *(const v4i*)(lds + DF_BIAS + 4 * cl);
 #pragma unroll
-            for (int r4 = 0; r4 < 4; ++r4) {
-                const int co0 = co_blk + 64 * cw + 32 * a + 8 * r4 + 4 * lh;
+            for (int b = 0; b < 2; ++b) {
                 int qv[4];
+                if (narrow) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int co = co0 + e;
-                    const int z = acc[a][b][4 * r4 + e] + (bias && co < g.cout ? bias[co] : 0) + rnd;
-                    int v = z >> s;
-                    v = v < lo ? lo : (v > 127 ? 127 : v);
-                    qv[e] = v;
-                }
-                if (co0 + 3 < g.cout && (g.cout & 3) == 0) {
-                    *(uint32_t*)(yp + co0) = __builtin_amdgcn_perm((uint32_t)qv[1], (uint32_t)qv[0], 0x0c0c0400u) |
-                                             (__builtin_amdgcn_perm((uint32_t)qv[3], (uint32_t)qv[2], 0x0c0c0400u) << 16);
+                    for (int e = 0; e < 4; ++e) {
+                        const int v = (acc[a][b][4 * r4 + e] + bv4[e] + rnd) >> s;
+                        qv[e] = v < lo ? lo : (v > 127 ? 127 : v);
+                    }
                 } else {
-                    for (int e = 0; e < 4; ++e)
-                        if (co0 + e < g.cout) yp[co0 + e] = (int8_t)qv[e];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const long long v = ((long long)acc[a][b][4 * r4 + e] + bv4[e] + rnd) >> s;
+                        qv[e] = v < lo ? lo : (v > 127 ? 127 : (int)v);
+                    }
                 }
+                const int pl = 32 * (2 * pwv + b) + l32;               // block-local pixel
+                *(uint32_t*)(lds + pl * OP + cl) =
+                    __builtin_amdgcn_perm((uint32_t)qv[1], (uint32_t)qv[0], 0x0c0c0400u) |
+                    (__builtin_amdgcn_perm((uint32_t)qv[3], (uint32_t)qv[2], 0x0c0c0400u) << 16);
             }
+        }
+    __syncthreads();
+    // lane = 16-byte piece q of pixel 4 * it + lane / 16 of this wave's 16 pixels
+    const int q = lane & 15;
+    const bool vec = (g.cout & 15) == 0 && ((uintptr_t)y & 15) == 0;
+#pragma unroll
+    for (int it = 0; it < DF_PX / (4 * DF_WAVES); ++it) {
+        const int pl = (DF_PX / DF_WAVES) * wave + 4 * it + (lane >> 4);
+        const int oy = ty0 + pl / DF_TW, ox = tx0 + pl % DF_TW;
+        if (oy >= g.h || ox >= g.w) continue;
+        int8_t* yp = y + ((long long)(img * g.h + oy) * g.w + ox) * g.cout + co_blk + 16 * q;
+        const int nco = g.cout - co_blk - 16 * q;                    // channels of this piece inside Cout
+        if (nco <= 0) continue;
+        if (vec && nco >= 16) {
+            *(v4i*)yp = *(const v4i*)(lds + pl * OP + 16 * q);
+        } else {
+            for (int e = 0; e < 16 && e < nco; ++e) yp[e] = (int8_t)lds[pl * OP + 16 * q + e];
+        }
     }
 }
 
@@ -358,16 +424,19 @@ extern "C" wino_status direct_conv_int8(const int8_t* x, const int8_t* w_ohwi, c
         f.cout = cout;
         f.h = h;
         f.w = w;
-        f.npix = (int)a.npix;
+        f.tiles_x = (w + DF_TW - 1) / DF_TW;
+        f.tiles_y = (h + DF_TH - 1) / DF_TH;
         f.nbco = (cout + DF_CO - 1) / DF_CO;
         f.nkb = cin / 64;
-        long long nb = (a.npix + DF_PX - 1) / DF_PX * f.nbco;
+        long long nb = (long long)n * f.tiles_x * f.tiles_y * f.nbco;
         if (nb > 0x7fffffffll) return WINO_EUNSUPPORTED;
         f.nblocks = (int)nb;
         f.out_shift = out_shift;
         f.relu = relu;
         f.x_bytes = (int)xb;
         f.w_bytes = (int)wb;
+        const long long lim = 0x7fffffffll - 9ll * cin * 16384 - (out_shift > 0 ? 1ll << (out_shift - 1) : 0);
+        f.bias_lim = lim >= 0 ? (int)lim : -1;
         hipLaunchKernelGGL(direct_conv_nhwc_mfma, dim3((unsigned)nb), dim3(DF_THREADS), 0, stream, x, w_ohwi, bias,
                            y, f);
         return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;

@@ -309,7 +309,8 @@ def test_calibrate_output_matches_oracle(layout):
 @pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("shape", [(1, 16, 16, 32, 32), (2, 3, 5, 7, 9), (1, 70, 130, 9, 14),
                                    (2, 64, 130, 9, 14), (1, 128, 64, 17, 23), (3, 192, 40, 5, 7),
-                                   (1, 64, 256, 1, 1), (2, 256, 128, 16, 16)])
+                                   (1, 64, 256, 1, 1), (2, 256, 128, 16, 16), (1, 64, 320, 19, 70),
+                                   (2, 128, 96, 33, 40), (1, 64, 8, 8, 32)])
 def test_direct_conv_bitexact(shape, layout):
     torch = torch_dev()
     n, cin, cout, h, w = shape
@@ -323,6 +324,28 @@ def test_direct_conv_bitexact(shape, layout):
     torch.cuda.synchronize()
     ref = direct.conv_int8(x, wq_ref, b, 9, False)
     assert (from_device_nchw(y, layout) == ref).all()
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_direct_conv_wide_bias(layout):
+    """Biases near the int32 limits: acc + bias + rounding leaves int32 for
+    some channels, so the requantization must widen (the fast path keeps 32
+    bits only when every bias of a channel block leaves room); out_shift 31."""
+    torch = torch_dev()
+    n, cin, cout, h, w = 1, 64, 80, 11, 13
+    x, f, _ = workloads.random_case(12, n, cin, cout, h, w, signed=True)
+    b = np.random.default_rng(13).integers(-2 ** 31, 2 ** 31, cout).astype(np.int64)
+    b[::3] = 2 ** 31 - 1
+    b[1::3] = -2 ** 31
+    b = b.astype(np.int32)
+    w_ohwi, e = W.direct_conv_quantize_weights(f)
+    wq_ref, _ = direct.quantize_weights_pow2(f)
+    for shift in (31, 20):
+        y = empty_out(n, cout, h, w, layout)
+        W.direct_conv_int8(to_device(x, layout), torch.from_numpy(w_ohwi).cuda(), torch.from_numpy(b).cuda(), y,
+                           n, cin, cout, h, w, layout, shift, False)
+        torch.cuda.synchronize()
+        assert (from_device_nchw(y, layout) == direct.conv_int8(x, wq_ref, b, shift, False)).all(), shift
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
