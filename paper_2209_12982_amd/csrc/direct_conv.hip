@@ -174,6 +174,14 @@ __global__ __launch_bounds__(DC_THREADS) void direct_conv_kernel(const int8_t* _
 // padding) and channels beyond Cout in the weights get an offset past the
 // buffer's end, which the buffer load turns into zeros.  LDS rows (64 B)
 // hold their 16-byte parts at slot p ^ ((row >> 1) & 3).
+//
+// NCHW (W % 4 == 0): the same kernel with the window transposed on the way
+// in and the output on the way out.  A window's 64 channels x 10 rows are read
+// as 640 runs of 40 pixels (ten aligned 4-byte words from tx0 - 4, one run
+// per thread) into registers during the three stages before the window is
+// needed, and written byte by byte into the pixel-major rows at the start of
+// its first stage (one more barrier per channel block).  The output is staged channel-major and leaves
+// as the 32-pixel row pieces of NCHW.
 // ---------------------------------------------------------------------------
 constexpr int DF_CO = 256, DF_TH = 8, DF_TW = 32, DF_PX = DF_TH * DF_TW;
 constexpr int DF_WH = DF_TH + 2, DF_WW = DF_TW + 2, DF_WROWS = DF_WH * DF_WW;     // input window: 10 x 34
@@ -190,6 +198,9 @@ constexpr int DF_LDS = DF_NARROW + DF_CO;
 static_assert(DF_A / 1024 == DF_WAVES, "one weight load per wave and stage");
 static_assert(DF_LDS <= 160 * 1024, "LDS");
 static_assert((DF_CO / 64) * (DF_PX / 64) == DF_WAVES, "waves tile the block");
+constexpr int DF_NROWS = 64 * DF_WH;                                              // NCHW window: (channel, row) runs
+constexpr int DF_NWPT = 10;                                                      // 4-byte words per run: 40 pixels
+static_assert(DF_NROWS <= DF_THREADS && 4 * DF_NWPT >= DF_WW + 3, "one run per thread covers the window row");
 
 typedef int v16i __attribute__((ext_vector_type(16)));
 
@@ -210,7 +221,8 @@ __device__ __forceinline__ void df_barrier() {
 }
 #define DF_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(0x0070 | (n))   // vmcnt(n) lgkmcnt(0)
 
-__global__ __launch_bounds__(DF_THREADS) void direct_conv_nhwc_mfma(const int8_t* __restrict__ x,
+template <int LAYOUT>
+__global__ __launch_bounds__(DF_THREADS) void direct_conv_tile_mfma(const int8_t* __restrict__ x,
                                                                    const int8_t* __restrict__ wt,
                                                                    const int32_t* __restrict__ bias,
                                                                    int8_t* __restrict__ y, DFArgs g) {
@@ -236,7 +248,7 @@ __global__ __launch_bounds__(DF_THREADS) void direct_conv_nhwc_mfma(const int8_t
     // j = w + 16 i; loads past the window's 22 write zeros to a junk row
     int woff[DF_WLPW], wdst[DF_WLPW];
 #pragma unroll
-    for (int i = 0; i < DF_WLPW; ++i) {
+    for (int i = 0; i < (LAYOUT == WINO_NHWC ? DF_WLPW : 0); ++i) {
         const int j = wave + DF_WAVES * i;
         const int row = 16 * j + rr;
         wdst[i] = j < DF_WINSTR ? 1024 * j : -1;
@@ -253,6 +265,18 @@ __global__ __launch_bounds__(DF_THREADS) void direct_conv_nhwc_mfma(const int8_t
         ((int*)(lds + DF_BIAS))[tid] = bv;
         lds[DF_NARROW + tid] = bv >= -g.bias_lim && bv <= g.bias_lim;
     }
+    // NCHW window: thread t < 640 reads the run of channel c = t / 10, window
+    // row wy = t % 10: words j = 0..9 hold pixels tx0 - 4 + 4 j .. + 3 (all
+    // four inside the image or none, as W % 4 == 0).  Words outside the image
+    // and the threads past 640 read an out-of-range offset, which loads zero,
+    // so every wave issues the same number of loads and the zeros are the
+    // padding.
+    const int nc = tid / DF_WH, nwy = tid - (tid / DF_WH) * DF_WH;
+    const int niy = ty0 - 1 + nwy;
+    const bool nrow_ok = tid < DF_NROWS && niy >= 0 && niy < g.h;
+    uint32_t nword[DF_NWPT];
+#pragma unroll
+    for (int k = 0; k < DF_NWPT; ++k) nword[k] = 0;
     const int nst = 9 * g.nkb;                 // stage t: channel block t / 9, position t % 9
     auto issue = [&](int t) {
         const int kb = t / 9, rs = t - 9 * kb;
@@ -260,15 +284,46 @@ __global__ __launch_bounds__(DF_THREADS) void direct_conv_nhwc_mfma(const int8_t
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (__attribute__((address_space(3))) void*)(abuf + 1024 * wave), 16,
                                                  aoff >= 0 ? aoff + rs * g.cin + kb * 64 : 0x7fffffff, 0, 0, 0);
         if (rs == 0) {
-            uint8_t* wbuf = lds + DF_ABUF * DF_A + (kb & 1) * DF_WIN;
+            if constexpr (LAYOUT == WINO_NHWC) {
+                uint8_t* wbuf = lds + DF_ABUF * DF_A + (kb & 1) * DF_WIN;
 #pragma unroll
-            for (int i = 0; i < DF_WLPW; ++i)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    rx, (__attribute__((address_space(3))) void*)(wdst[i] >= 0 ? wbuf + wdst[i] : lds + DF_JUNK), 16,
-                    woff[i] >= 0 ? woff[i] + kb * 64 : 0x7fffffff, 0, 0, 0);
+                for (int i = 0; i < DF_WLPW; ++i)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                        rx, (__attribute__((address_space(3))) void*)(wdst[i] >= 0 ? wbuf + wdst[i] : lds + DF_JUNK),
+                        16, woff[i] >= 0 ? woff[i] + kb * 64 : 0x7fffffff, 0, 0, 0);
+            } else {
+                const int base = ((img * g.cin + kb * 64 + nc) * g.h + niy) * g.w + tx0 - 4;
+#pragma unroll
+                for (int k = 0; k < DF_NWPT; ++k) {
+                    const int ix = tx0 - 4 + 4 * k;
+                    const bool ok = nrow_ok && ix >= 0 && ix < g.w;
+                    nword[k] = __builtin_amdgcn_raw_buffer_load_b32(rx, ok ? base + 4 * k : 0x7fffffff, 0, 0);
+                }
+            }
         }
     };
-    auto loads_of = [&](int t) { return t >= nst ? 0 : (t % 9 == 0 ? 1 + DF_WLPW : 1); };
+    constexpr int WLOADS = LAYOUT == WINO_NHWC ? DF_WLPW : DF_NWPT;
+    static_assert(2 + WLOADS <= 12, "the wait below covers every count of later loads");
+    auto loads_of = [&](int t) { return t >= nst ? 0 : (t % 9 == 0 ? 1 + WLOADS : 1); };
+    // NCHW: the words of window kb, byte by byte into its pixel-major rows
+    // (window pixel wx = 4 j + p - 3)
+    auto put_window = [&](int kb) {
+        if (tid >= DF_NROWS) return;
+        // the row and slot terms, recomputed per window: the pin keeps the
+        // compiler from hoisting 34 byte addresses out of the main loop
+        int rowb = nwy * DF_WW, part = nc >> 4;
+        asm volatile("" : "+v"(rowb), "+v"(part));
+        uint8_t* wbuf = lds + DF_ABUF * DF_A + (kb & 1) * DF_WIN + (nc & 15);
+#pragma unroll
+        for (int k = 0; k < DF_NWPT; ++k)
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                const int wx = 4 * k + p - 3;
+                if (wx < 0 || wx >= DF_WW) continue;
+                const int row = rowb + wx;
+                wbuf[row * 64 + 16 * df_slot(row, part)] = (uint8_t)(nword[k] >> (8 * p));
+            }
+    };
 
     const int cw = wave & 3, pwv = wave >> 2;
     const int l32 = lane & 31, lh = lane >> 5;
@@ -299,11 +354,28 @@ __global__ __launch_bounds__(DF_THREADS) void direct_conv_nhwc_mfma(const int8_t
             case 1: DF_WAIT_VM(1); break;
             case 2: DF_WAIT_VM(2); break;
             case 3: DF_WAIT_VM(3); break;
-            default: DF_WAIT_VM(4); break;
+            case 4: DF_WAIT_VM(4); break;
+            case 5: DF_WAIT_VM(5); break;
+            case 6: DF_WAIT_VM(6); break;
+            case 7: DF_WAIT_VM(7); break;
+            case 8: DF_WAIT_VM(8); break;
+            case 9: DF_WAIT_VM(9); break;
+            case 10: DF_WAIT_VM(10); break;
+            case 11: DF_WAIT_VM(11); break;
+            default: DF_WAIT_VM(12); break;
         }
         df_barrier();
         if (t + 3 < nst) issue(t + 3);
         const int kb = t / 9, rs = t - 9 * kb;
+        if constexpr (LAYOUT == WINO_NCHW) {
+            if (rs == 0) {
+                // window kb's words are in (the wait above covered them); its
+                // buffer was last read by window kb - 2's stages
+                put_window(kb);
+                __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+                df_barrier();
+            }
+        }
         const int dr = rs / 3, ds = rs - 3 * (rs / 3);           // window offsets 0..2
         const uint8_t* abuf = lds + (t & (DF_ABUF - 1)) * DF_A;
         const uint8_t* wbuf = lds + DF_ABUF * DF_A + (kb & 1) * DF_WIN;
@@ -364,12 +436,38 @@ __global__ __launch_bounds__(DF_THREADS) void direct_conv_nhwc_mfma(const int8_t
                     }
                 }
                 const int pl = 32 * (2 * pwv + b) + l32;               // block-local pixel
-                *(uint32_t*)(lds + pl * OP + cl) =
-                    __builtin_amdgcn_perm((uint32_t)qv[1], (uint32_t)qv[0], 0x0c0c0400u) |
-                    (__builtin_amdgcn_perm((uint32_t)qv[3], (uint32_t)qv[2], 0x0c0c0400u) << 16);
+                if constexpr (LAYOUT == WINO_NHWC) {
+                    *(uint32_t*)(lds + pl * OP + cl) =
+                        __builtin_amdgcn_perm((uint32_t)qv[1], (uint32_t)qv[0], 0x0c0c0400u) |
+                        (__builtin_amdgcn_perm((uint32_t)qv[3], (uint32_t)qv[2], 0x0c0c0400u) << 16);
+                } else {
+                    // channel-major for NCHW: one byte per (channel, pixel)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) lds[(cl + e) * OP + pl] = (uint8_t)qv[e];
+                }
             }
         }
     __syncthreads();
+    if constexpr (LAYOUT == WINO_NCHW) {
+        // piece (co, tile row, half): 16 pixels of one output row of one
+        // channel; 256 x 8 x 2 pieces, four per thread
+        const bool vec = (g.w & 15) == 0 && ((uintptr_t)y & 15) == 0;
+#pragma unroll
+        for (int it = 0; it < 2 * DF_CO * DF_TH / DF_THREADS; ++it) {
+            const int piece = tid + DF_THREADS * it;
+            const int cl = piece >> 4, ty = (piece >> 1) & 7, hx = piece & 1;
+            const int co = co_blk + cl, oy = ty0 + ty, ox = tx0 + 16 * hx;
+            if (co >= g.cout || oy >= g.h || ox >= g.w) continue;
+            int8_t* yp = y + ((long long)(img * g.cout + co) * g.h + oy) * g.w + ox;
+            const uint8_t* src = lds + cl * OP + ty * DF_TW + 16 * hx;
+            if (vec) {
+                *(v4i*)yp = *(const v4i*)src;
+            } else {
+                for (int e = 0; e < 16 && ox + e < g.w; ++e) yp[e] = (int8_t)src[e];
+            }
+        }
+        return;
+    }
     // lane = 16-byte piece q of pixel 4 * it + lane / 16 of this wave's 16 pixels
     const int q = lane & 15;
     const bool vec = (g.cout & 15) == 0 && ((uintptr_t)y & 15) == 0;
@@ -416,8 +514,9 @@ extern "C" wino_status direct_conv_int8(const int8_t* x, const int8_t* w_ohwi, c
     a.vec = (cin % 16 == 0) && (((uintptr_t)x & 15) == 0) && (((uintptr_t)w_ohwi & 15) == 0);
     const long long xb = (long long)n * h * w * cin, wb = 9ll * cin * cout;
     // z = sum x w + bias + rounding must fit int32: |x w| <= 2^14, 9 cin <= 73728
-    if (layout == WINO_NHWC && cin % 64 == 0 && xb < 0x7fffffffll && wb < 0x7fffffffll &&
-        a.npix < 0x7fffffffll && (((uintptr_t)x & 15) == 0) && (((uintptr_t)w_ohwi & 15) == 0)) {
+    const bool tile_ok = layout == WINO_NHWC ? ((uintptr_t)x & 15) == 0 : (w % 4 == 0 && ((uintptr_t)x & 3) == 0);
+    if (tile_ok && cin % 64 == 0 && xb < 0x7fffffffll && wb < 0x7fffffffll && a.npix < 0x7fffffffll &&
+        (((uintptr_t)w_ohwi & 15) == 0)) {
         DFArgs f;
         f.n = n;
         f.cin = cin;
@@ -437,8 +536,12 @@ extern "C" wino_status direct_conv_int8(const int8_t* x, const int8_t* w_ohwi, c
         f.w_bytes = (int)wb;
         const long long lim = 0x7fffffffll - 9ll * cin * 16384 - (out_shift > 0 ? 1ll << (out_shift - 1) : 0);
         f.bias_lim = lim >= 0 ? (int)lim : -1;
-        hipLaunchKernelGGL(direct_conv_nhwc_mfma, dim3((unsigned)nb), dim3(DF_THREADS), 0, stream, x, w_ohwi, bias,
-                           y, f);
+        if (layout == WINO_NHWC)
+            hipLaunchKernelGGL(direct_conv_tile_mfma<WINO_NHWC>, dim3((unsigned)nb), dim3(DF_THREADS), 0, stream, x,
+                               w_ohwi, bias, y, f);
+        else
+            hipLaunchKernelGGL(direct_conv_tile_mfma<WINO_NCHW>, dim3((unsigned)nb), dim3(DF_THREADS), 0, stream, x,
+                               w_ohwi, bias, y, f);
         return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
     }
     if (layout == WINO_NHWC)

@@ -1432,8 +1432,10 @@ extern "C" wino_status wino_select_algorithm(int32_t n, int32_t cin, int32_t cou
     if (!algo || n < 0 || h < 0 || w < 0 || cin < 1 || cout < 1) return WINO_EINVAL;
     if (layout != WINO_NCHW && layout != WINO_NHWC) return WINO_EINVAL;
     const double ops = 2.0 * 9 * (double)n * h * w * (double)cin * cout;
-    // direct only in NHWC: NCHW direct convolution runs the simple MFMA
-    // kernel, which F2 beats on these small layers (C1: 14.3 against 31 us)
+    // direct only in NHWC: small NCHW layers (Cin not a multiple of 64, or
+    // W not a multiple of 4) run the simple MFMA kernel, which F2 beats
+    // (C1: 12.3 against 31 us), and the NCHW tile kernel's byte transposes
+    // leave it behind the Winograd paths on the large layers
     if (ops < (double)(1 << 27) && layout == WINO_NHWC) {
         *algo = WINO_ALGO_DIRECT;
         return WINO_OK;
