@@ -107,19 +107,21 @@ def check_output(torch, y, layout, args, share, layer=None):
     """SHA-256 of the timed step's output (NCHW order) against the oracle's
     record for this configuration and layer in tests/golden (written by
     tests/golden/make_golden.py from the oracle alone).  True / False, or
-    None where no record applies (a GPU's share of a layer, F2, the C3 layers
-    past the first, whose inputs are the previous layer's outputs)."""
+    None where no record applies (a GPU's share of a layer, the C3 layers
+    past the first, whose inputs are the previous layer's outputs, F2 at
+    10 bits)."""
     import hashlib
     if layer is None:
         layer = args.layer
         if args.config == "C3" and layer > 0:
             return None
-    if share or args.transform != "f4":
+    if share or (args.transform != "f4" and args.bits != 8):
         return None
     path = os.path.join(ROOT, "tests", "golden", "configs.json" if args.bits == 8 else "configs_i10.json")
     if not os.path.exists(path):
         return None
-    rec = json.load(open(path)).get(args.config, {}).get("layers", [])
+    key = "layers" if args.transform == "f4" else "f2_layers"
+    rec = json.load(open(path)).get(args.config, {}).get(key, [])
     if len(rec) <= layer or "sha256_nchw" not in rec[layer]:
         return None
     torch.cuda.synchronize()

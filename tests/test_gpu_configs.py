@@ -20,13 +20,15 @@ pytestmark = pytest.mark.gpu
 GOLDEN = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "configs.json")))
 
 
-def _run_layer(x, f, b, spec, rec, layout, variant=W.SPLIT, tap_kernel=W.TAP_AUTO):
+def _run_layer(x, f, b, spec, rec, layout, variant=W.SPLIT, tap_kernel=W.TAP_AUTO, m=4):
     torch = torch_dev()
     n, cin, h, w = x.shape
     xd = to_device(x, layout)
-    eb, amax = W.wino_f4_calibrate_input(xd, n, cin, h, w, layout)
+    calibrate = W.wino_f4_calibrate_input if m == 4 else W.wino_f2_calibrate_input
+    make_plan = W.wino_f4_plan if m == 4 else W.wino_f2_plan
+    eb, amax = calibrate(xd, n, cin, h, w, layout)
     assert eb == rec["e_b"], "input tap exponents differ from the oracle"
-    plan0 = W.wino_f4_plan(f, eb, bias=b, out_shift=0, relu=spec.relu)
+    plan0 = make_plan(f, eb, bias=b, out_shift=0, relu=spec.relu)
     info0 = W.wino_f4_plan_info(plan0)
     assert info0["e_g"] == rec["e_g"] and info0["sh"] == rec["sh"] and info0["e_o"] == rec["e_o"]
     if spec.out_shift is None:
@@ -34,7 +36,7 @@ def _run_layer(x, f, b, spec, rec, layout, variant=W.SPLIT, tap_kernel=W.TAP_AUT
         assert zmax == rec["zmax"] and s == rec["out_shift"]
     else:
         s = spec.out_shift
-    plan = W.wino_f4_plan(f, eb, bias=b, out_shift=s, relu=spec.relu)
+    plan = make_plan(f, eb, bias=b, out_shift=s, relu=spec.relu)
     W.wino_f4_plan_set_tap_kernel(plan, tap_kernel)
     shape = (n, spec.cout, h, w) if layout == W.NCHW else (n, h, w, spec.cout)
     y = torch.full(shape, 77, dtype=torch.int8, device="cuda")
@@ -60,6 +62,28 @@ def test_full_size_layer_bitexact(name, layout, variant, tap_kernel):
     x, layers = workloads.generate(name)
     f, b, spec = layers[0]
     _run_layer(x, f, b, spec, GOLDEN[name]["layers"][0], layout, variant, tap_kernel)
+
+
+@pytest.mark.parametrize("layout", [W.NCHW, W.NHWC])
+@pytest.mark.parametrize("name", ["C1", "C2"])
+def test_small_config_bitexact(name, layout):
+    """C1 (its literal out_shift 8) and C2 against their full records, SPLIT
+    and FUSED."""
+    x, layers = workloads.generate(name)
+    f, b, spec = layers[0]
+    for variant in (W.SPLIT, W.FUSED):
+        _run_layer(x, f, b, spec, GOLDEN[name]["layers"][0], layout, variant)
+
+
+@pytest.mark.parametrize("layout", [W.NCHW, W.NHWC])
+@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C4", "C5"])
+def test_f2_first_layer_bitexact(name, layout):
+    """F(2x2, 3x3) on every configuration's first layer at full size: the
+    GPU's F2 calibration, tables and every output byte against the oracle's
+    F2 record."""
+    x, layers = workloads.generate(name)
+    f, b, spec = layers[0]
+    _run_layer(x, f, b, spec, GOLDEN[name]["f2_layers"][0], layout, W.SPLIT, W.TAP_AUTO, m=2)
 
 
 @pytest.mark.parametrize("layout,variant,tap_kernel", RUNS)
