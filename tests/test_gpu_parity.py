@@ -328,6 +328,30 @@ def test_direct_conv_bitexact(shape, layout):
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("shape,relu,shift,with_bias", [
+    ((1, 64, 3, 9, 8), True, 0, True),          # three output channels, no shift
+    ((2, 128, 260, 5, 12), False, 14, False),   # no bias, a partial second channel block
+    ((1, 64, 64, 1, 4), True, 7, True),         # one output row, one four-pixel column group
+    ((3, 64, 32, 17, 64), False, 9, True),      # two tile columns, three images
+])
+def test_direct_conv_options(shape, relu, shift, with_bias, layout):
+    """The tile kernel's options and edges: ReLU, out_shift 0, a NULL bias,
+    Cout below four, a partial channel block, single rows and narrow images."""
+    torch = torch_dev()
+    n, cin, cout, h, w = shape
+    x, f, b = workloads.random_case(14, n, cin, cout, h, w, signed=True)
+    w_ohwi, _ = W.direct_conv_quantize_weights(f)
+    wq_ref, _ = direct.quantize_weights_pow2(f)
+    y = empty_out(n, cout, h, w, layout)
+    bd = torch.from_numpy(b).cuda() if with_bias else None
+    W.direct_conv_int8(to_device(x, layout), torch.from_numpy(w_ohwi).cuda(), bd, y, n, cin, cout, h, w, layout,
+                       shift, relu)
+    torch.cuda.synchronize()
+    ref = direct.conv_int8(x, wq_ref, b if with_bias else None, shift, relu)
+    assert (from_device_nchw(y, layout) == ref).all()
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
 def test_direct_conv_wide_bias(layout):
     """Biases near the int32 limits: acc + bias + rounding leaves int32 for
     some channels, so the requantization must widen (the fast path keeps 32
