@@ -26,9 +26,7 @@
 //
 // Ring stage = one tap x NK 64-channel chunks: per chunk 64 Uq rows (output
 // channels) and 64 Vq rows (tiles) of 64 bytes, 8 KB; four 32 KB buffers,
-// copies issued three stages ahead (96 KB in flight: the copies wait on
-// L2/Infinity-Cache latency, so the bytes in flight set their rate).  One
-// barrier per stage.  z_a is handed over in two halves (j = 0, 1 in the
+// copies issued three stages ahead (96 KB in flight).  One barrier per stage.  z_a is handed over in two halves (j = 0, 1 in the
 // first stage of the next row, j = 2, 3 two stages later: the next row's
 // first fold only touches j = 0, its second rewrites j = 1..3), so the
 // hand-over buffer is 8 KB per MFMA wave: 128 + 32 = 160 KB of LDS.
@@ -45,6 +43,12 @@
 // MFMA orientation: A = Uq (rows = output channels), B = Vq (columns =
 // tiles), so lane l holds tile l % 32 and, in accumulator register r, output
 // channel 8 (r / 4) + 4 (l / 32) + r % 4 of the wave's 32.
+//
+// Measured, it is slower than the row-streamed kernel (C5: 58 against 47 us;
+// C4: 28 against 20 us): its copies run at the same ~25 B/clk per CU as the
+// row-streamed ring's, and an MFMA wave and a fold wave on one SIMD mostly
+// take turns rather than overlap.  The automatic choice never picks it; it is
+// run only when forced (WINO_TAP_WAVES).
 // ---------------------------------------------------------------------------
 constexpr int WS_CO = 64;
 constexpr int WS_TL = 64;
@@ -54,9 +58,6 @@ constexpr int WS_NBUF = 4;
 constexpr int WS_BUF = 32 * 1024;
 constexpr int WS_ZHALF = 8 * 1024;
 constexpr int WS_LDS = WS_NBUF * WS_BUF + 4 * WS_ZHALF;
-// fold instructions placed after each MFMA of a stage (the MFMA occupies its
-// pipe for 32 cycles, a wave64 integer instruction 4)
-constexpr int WS_VALU_PER_MFMA = 8;
 static_assert(WS_LDS <= 160 * 1024, "LDS");
 static_assert((WS_NBUF & (WS_NBUF - 1)) == 0, "ring index by mask");
 static_assert(kTilePad % WS_TL == 0 && kCoutPad % WS_CO == 0, "blocks tile the padded sizes");
