@@ -277,6 +277,19 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
 // rows run 1.5x slower.
 __device__ __forceinline__ int lds_slot(int row, int part) { return part ^ ((row >> 1) & 3); }
 
+// Global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4) for a
+// ring whose stages the caller waits for explicitly (s_waitcnt vmcnt(n), then
+// a barrier).  Issued as inline assembly: with the builtin, the compiler has
+// to assume that any later LDS read may overlap a copy still in flight, and
+// it waits for every copy (vmcnt(0)) before each fragment read -- the copies
+// of the ring's next stages included.  M0, the LDS destination, is an input
+// operand the compiler sets; the s_nop is the one wait state an M0 write
+// needs before an LDS-DMA load.
+__device__ __forceinline__ void lds_copy16(const void* src, __attribute__((address_space(3))) void* dst) {
+    const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)dst);
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(m0) : "memory");
+}
+
 // Workgroup barrier without the implicit wait for outstanding global loads
 // that __syncthreads() carries: callers wait for exactly the loads they need
 // with s_waitcnt.  The empty asm statements keep the compiler from moving

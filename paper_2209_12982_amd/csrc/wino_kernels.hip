@@ -678,12 +678,17 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
                                                                  const int32_t* __restrict__ bias,
                                                                  int8_t* __restrict__ y, K2Args g) {
     __shared__ __attribute__((aligned(1024))) uint8_t lds[KR_NBUF * KR_STAGE];
+    __shared__ __attribute__((aligned(16))) int bias_blk[KR_CO];
     const int lbid = xcd_remap(blockIdx.x, g.nblocks);
     const int bco = lbid % g.nbco, btl = lbid / g.nbco;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int cw = wave & 3, tw = wave >> 2;
     const int co_blk = bco * KR_CO;
+    // the block's bias (padded to the plan's channel count) into LDS before the
+    // ring starts: read from global memory where row 1 uses it, its load would
+    // be waited for with every ring copy issued before it (vmcnt counts in order)
+    if (threadIdx.x < KR_CO) bias_blk[threadIdx.x] = bias[co_blk + threadIdx.x];
     const long long tl_blk = (long long)btl * KR_TL;
     const int lr = lane & 15, lk = lane >> 4;
     const int nkc = g.cin_pad / kKStep;
@@ -719,9 +724,8 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
         // the later readers go back to memory and cost 8%
 #pragma unroll
         for (int i = 0; i < KR_LPW; ++i)
-            __builtin_amdgcn_global_load_lds((const void*)(next_src + i * slice_step + lane_off),
-                                             (__attribute__((address_space(3))) void*)(d + step * i * KR_CHUNK), 16,
-                                             0, 0);
+            lds_copy16(next_src + i * slice_step + lane_off,
+                       (__attribute__((address_space(3))) void*)(d + step * i * KR_CHUNK));
         if (++next_kc == nkc) {
             next_kc = 0;
             next_src += row_adv;
@@ -758,7 +762,7 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
         // and column of A^T are all ones, so it reaches every output of the
         // tile once.  Loaded in the row that uses it.
         v4i bias_rnd = (v4i){0, 0, 0, 0};
-        if (a == 1) bias_rnd = *(const v4i*)(bias + co0) + rnd;
+        if (a == 1) bias_rnd = *(const v4i*)(bias_blk + (co0 - co_blk)) + rnd;
         v4i m[6][KR_TB];
         // one stage: the six taps of row a, 64 input channels; the first
         // k-chunk of the row starts the accumulators from zero
@@ -956,8 +960,7 @@ __global__ __launch_bounds__(KW_THREADS) void wino_tap_gemm_rows_wide(const int8
         if (row_end) next_kc = 0;
 #pragma unroll
         for (int i = 0; i < KW_LPW; ++i) {
-            __builtin_amdgcn_global_load_lds((const void*)(src[i] + lane_off),
-                                             (__attribute__((address_space(3))) void*)(d + dsto[i]), 16, 0, 0);
+            lds_copy16(src[i] + lane_off, (__attribute__((address_space(3))) void*)(d + dsto[i]));
             src[i] += row_end ? radv[i] : kadv[i];
         }
         next_buf = next_buf == KW_NBUF - 1 ? 0 : next_buf + 1;

@@ -312,8 +312,8 @@ __global__ __launch_bounds__(WS_THREADS) void wino_tap_gemm_ws(const int8_t* __r
             uint8_t* d = lds + (sglob & (WS_NBUF - 1)) * WS_BUF + fw * 1024;
 #pragma unroll
             for (int c = 0; c < NK; ++c)
-                __builtin_amdgcn_global_load_lds((const void*)(isrc + ((long long)is * NK + c) * kstride + lane_off),
-                                                 (__attribute__((address_space(3))) void*)(d + c * 8192), 16, 0, 0);
+                lds_copy16(isrc + ((long long)is * NK + c) * kstride + lane_off,
+                           (__attribute__((address_space(3))) void*)(d + c * 8192));
             if (++is == nstage) {
                 is = 0;
                 if (++ib < nblk) isrc = src_of(ib);
