@@ -47,7 +47,7 @@ def parse():
     ap.add_argument("--bits", type=int, default=8, choices=[8, 10],
                     help="Winograd-domain integer width: 8, or 10 for the int8/10 variant")
     ap.add_argument("--tap-kernel", default="auto",
-                    choices=["auto", "resident", "rows", "waves", "64x32", "32x32", "16x16"],
+                    choices=["auto", "resident", "rows", "rows_streamk", "waves", "64x32", "32x32", "16x16"],
                     help="force the tap-GEMM kernel (wino_f4_plan_set_tap_kernel)")
     ap.add_argument("--no-direct", action="store_true")
     ap.add_argument("--no-plan-timing", action="store_true", help="skip timing the on-device plan builds")
@@ -423,7 +423,7 @@ def main():
     plan_host_ms = (time.perf_counter() - t0) * 1e3
     info = W.wino_f4_plan_info(plan)
     W.wino_f4_plan_set_tap_kernel(plan, {"auto": W.TAP_AUTO, "resident": W.TAP_RESIDENT, "rows": W.TAP_ROWS,
-                                         "waves": W.TAP_WAVES, "64x32": W.TAP_RESIDENT_64X32,
+                                         "rows_streamk": W.TAP_ROWS_STREAMK, "waves": W.TAP_WAVES, "64x32": W.TAP_RESIDENT_64X32,
                                          "32x32": W.TAP_RESIDENT_32X32,
                                          "16x16": W.TAP_RESIDENT_16X16}[args.tap_kernel])
     plan_ms = {"host_exact": plan_host_ms}
@@ -461,7 +461,7 @@ def main():
     ntap = (mt + 2) ** 2
     lay = 1 if layout == W.NHWC else 0
     choice = W.wino_f4_tap_kernel_choice(plan, n, h, w)
-    rows = choice == W.TAP_ROWS
+    rows = choice in (W.TAP_ROWS, W.TAP_ROWS_STREAMK)   # the same kernel, split or not
     # kernel names as the profiler shows them (template arguments included;
     # the tap-resident kernel's block configuration is a class argument)
     # the one-instruction requantization serves plans whose e_B are all <= 16 - bits
@@ -477,6 +477,8 @@ def main():
     if rows and args.bits == 10:
         k2_name = "wino_tap_gemm_rows_wide"
         k2_inst = f"wino_tap_gemm_rows_wide<{lay},10,{'int' if info['epilogue_bits'] == 32 else 'longlong'}>"
+    elif choice == W.TAP_ROWS_STREAMK:
+        k2_name, k2_inst = "wino_tap_gemm_rows_sk", f"wino_tap_gemm_rows_sk<{lay}>"
     elif rows:
         k2_name, k2_inst = "wino_tap_gemm_rows", f"wino_tap_gemm_rows<{lay}>"
     elif choice == W.TAP_WAVES:
@@ -540,7 +542,8 @@ def main():
                             "TOP/s": tap_ops / (k2_ms * 1e-3) / 1e12,
                             "frac": tap_ops / (k2_ms * 1e-3) / 1e12 / k2_peak,
                             "GB/s_algorithmic": k2_bytes / (k2_ms * 1e-3) / 1e9,
-                            "traffic_bytes": counter_traffic(cfg_tag, args.layout, k2_inst, args.transform)}
+                            "traffic_bytes": counter_traffic(cfg_tag, args.layout, k2_inst, args.transform),
+                            "stream_k": choice == W.TAP_ROWS_STREAMK}
         # the input transform's HBM figures are taken cold (inputs in HBM,
         # caches flushed): warm, C5's 26 MB input sits in the 256 MB MALL
         k1c = cold["kernels_ms"][k1_name]

@@ -71,7 +71,12 @@ typedef struct wino_f4_plan_s* wino_f4_plan_t;   /* opaque, immutable after crea
  * 64 x 64 block between four 32x32x32-MFMA waves and eight waves that copy
  * operands and keep the output rows, persistent over the blocks.  AUTO picks
  * ROWS when its blocks fill the device and the 32-bit epilogue applies, else
- * RESIDENT_64X32.                                                            */
+ * RESIDENT_64X32.  ROWS_STREAMK (forced only: measured slower than ROWS)
+ * is ROWS with the blocks of its last, partial round of workgroups split by
+ * stages over every compute unit (stream-K): each workgroup runs an equal
+ * share of those blocks' stages, leaves partial sums in the workspace and the
+ * last to finish a block adds them up.  It needs the larger workspace that
+ * wino_f4_workspace_bytes then reports, and runs unsplit in a smaller one. */
 typedef enum wino_tap_kernel {
     WINO_TAP_AUTO = 0,
     WINO_TAP_RESIDENT = 1,
@@ -79,7 +84,8 @@ typedef enum wino_tap_kernel {
     WINO_TAP_RESIDENT_64X32 = 3,
     WINO_TAP_RESIDENT_32X32 = 4,
     WINO_TAP_RESIDENT_16X16 = 5,
-    WINO_TAP_WAVES = 6
+    WINO_TAP_WAVES = 6,
+    WINO_TAP_ROWS_STREAMK = 7
 } wino_tap_kernel;
 
 /*
@@ -287,8 +293,12 @@ wino_status wino_f4_plan_info(wino_f4_plan_t plan, int8_t* e_g, int8_t* sh, int3
 /*
  * Workspace bytes that wino_f4_conv_int8 needs for this plan, batch and image
  * size (SPLIT: the tap-major int8 Winograd-domain input, 36 x tiles x Cin
- * rounded up to the kernel's blocking; FUSED: 0).  Returns 0 for an invalid
- * plan or negative sizes.
+ * rounded up to the kernel's blocking, followed, when the plan forces the
+ * stream-K split (WINO_TAP_ROWS_STREAMK) and the shape leaves a partial last
+ * round of blocks, by that split's counters and partial sums: 512 KiB per
+ * compute unit; FUSED: 0).  A SPLIT workspace of at least the Vq part but
+ * smaller than this runs the same result without the split.  Returns 0 for
+ * an invalid plan or negative sizes.
  */
 size_t wino_f4_workspace_bytes(wino_f4_plan_t plan, int32_t n, int32_t h, int32_t w,
                                wino_variant variant);
@@ -332,10 +342,13 @@ wino_status wino_f4_conv_int8(wino_f4_plan_t plan, const int8_t* x, int8_t* y, i
  * Every call on one GPU shares that GPU's array and leaves its contents
  * behind (nothing in it needs clearing): calls that overlap on one GPU, e.g.
  * on two streams without ordering between them, race and must not be made.
+ * It never splits the tap GEMM's last round (WINO_TAP_ROWS_STREAMK): the
+ * array holds the input-transform workspace only.
  * Errors: as for wino_f4_conv_int8 (SPLIT), and WINO_EWORKSPACE when the
- * layer's workspace, wino_f4_workspace_bytes(plan, n, h, w, WINO_SPLIT),
- * exceeds WINO_NOALLOC_SCRATCH_BYTES (checked before any device work);
- * WINO_EHIP if the array's address cannot be obtained.
+ * layer's input-transform workspace (36 x tiles x Cin, each rounded up to a
+ * multiple of 64: wino_f4_workspace_bytes without a stream-K part) exceeds
+ * WINO_NOALLOC_SCRATCH_BYTES (checked before any device work); WINO_EHIP if
+ * the array's address cannot be obtained.
  */
 #define WINO_NOALLOC_SCRATCH_BYTES (64u << 20)
 wino_status wino_f4_conv_int8_noalloc(wino_f4_plan_t plan, const int8_t* x, int8_t* y, int32_t n,
@@ -349,13 +362,17 @@ wino_status wino_f4_conv_int8_noalloc(wino_f4_plan_t plan, const int8_t* x, int8
  *   Winograd-domain input: B^T d B and the tap-wise requantization).
  * wino_f4_tap_gemm: workspace -> y (the 36 tap GEMMs, alignment, A^T M A,
  *   bias, requantization, ReLU, store).  `workspace` must hold the Vq
- *   written by wino_f4_input_transform for the same plan, n, h, w.
+ *   written by wino_f4_input_transform for the same plan, n, h, w and
+ *   workspace_bytes; the tap GEMM leaves Vq unchanged, so it may run again on
+ *   it, and uses the part past Vq as scratch for a stream-K split (its
+ *   counters, which the input transform zeroes and every split launch leaves
+ *   at zero, and its partial sums).
  * Arguments, errors and stream semantics as for wino_f4_conv_int8.
  */
 wino_status wino_f4_input_transform(wino_f4_plan_t plan, const int8_t* x, int32_t n, int32_t h, int32_t w,
                                     wino_layout layout, void* workspace, size_t workspace_bytes,
                                     hipStream_t stream);
-wino_status wino_f4_tap_gemm(wino_f4_plan_t plan, const void* workspace, size_t workspace_bytes, int8_t* y,
+wino_status wino_f4_tap_gemm(wino_f4_plan_t plan, void* workspace, size_t workspace_bytes, int8_t* y,
                              int32_t n, int32_t h, int32_t w, wino_layout layout, hipStream_t stream);
 
 /*

@@ -8,7 +8,7 @@ an entry point without the built library raises ``LibraryNotBuilt``.
 """
 from .binding import (  # noqa: F401
     NCHW, NHWC, SPLIT, FUSED, TAPS, TAP_AUTO, TAP_RESIDENT, TAP_ROWS,
-    TAP_RESIDENT_64X32, TAP_RESIDENT_32X32, TAP_RESIDENT_16X16, TAP_WAVES, ALGO_DIRECT, ALGO_F2, ALGO_F4,
+    TAP_RESIDENT_64X32, TAP_RESIDENT_32X32, TAP_RESIDENT_16X16, TAP_WAVES, TAP_ROWS_STREAMK, ALGO_DIRECT, ALGO_F2, ALGO_F4,
     LibraryNotBuilt, WinoError, WinoF4Plan,
     library_path, load_library, exported_symbols,
     wino_f4_plan, wino_f4_plan_tables, wino_f4_plan_info,

@@ -13,6 +13,7 @@ SPLIT, FUSED = 0, 1
 TAP_AUTO, TAP_RESIDENT, TAP_ROWS = 0, 1, 2
 TAP_RESIDENT_64X32, TAP_RESIDENT_32X32, TAP_RESIDENT_16X16 = 3, 4, 5
 TAP_WAVES = 6
+TAP_ROWS_STREAMK = 7
 NOALLOC_SCRATCH_BYTES = 64 << 20   # WINO_NOALLOC_SCRATCH_BYTES
 ALGO_DIRECT, ALGO_F2, ALGO_F4 = 0, 2, 4
 
@@ -361,13 +362,14 @@ def wino_f4_plan_info(plan, with_uq=False):
 
 
 def wino_f4_plan_set_tap_kernel(plan, kind):
-    """TAP_AUTO, TAP_RESIDENT, TAP_ROWS, TAP_WAVES or a TAP_RESIDENT_* block shape: the
-    tap-GEMM kernel of later SPLIT convolutions with this plan."""
+    """TAP_AUTO, TAP_RESIDENT, TAP_ROWS, TAP_ROWS_STREAMK, TAP_WAVES or a TAP_RESIDENT_*
+    block shape: the tap-GEMM kernel of later SPLIT convolutions with this plan."""
     _check(load_library().wino_f4_plan_set_tap_kernel(plan.handle, int(kind)), "wino_f4_plan_set_tap_kernel")
 
 
 def wino_f4_tap_kernel_choice(plan, n, h, w):
-    """TAP_WAVES, TAP_ROWS or a TAP_RESIDENT_* shape: the tap-GEMM kernel a SPLIT convolution runs."""
+    """TAP_WAVES, TAP_ROWS, TAP_ROWS_STREAMK or a TAP_RESIDENT_* shape: the tap-GEMM kernel a
+    SPLIT convolution runs."""
     kind = ctypes.c_int32()
     _check(load_library().wino_f4_tap_kernel_choice(plan.handle, n, h, w, ctypes.byref(kind)),
            "wino_f4_tap_kernel_choice")

@@ -502,7 +502,7 @@ extern "C" void wino_f4_plan_destroy(wino_f4_plan_t p) {
 }
 
 extern "C" wino_status wino_f4_plan_set_tap_kernel(wino_f4_plan_t p, int32_t kind) {
-    if (!p || kind < WINO_TAP_AUTO || kind > WINO_TAP_WAVES) return WINO_EINVAL;
+    if (!p || kind < WINO_TAP_AUTO || kind > WINO_TAP_ROWS_STREAMK) return WINO_EINVAL;
     p->tap_kernel = kind;
     return WINO_OK;
 }

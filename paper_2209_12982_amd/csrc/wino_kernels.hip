@@ -59,7 +59,15 @@ struct K1Args {
     TapTables tab;
     uint32_t rnd2[kTaps];               // 2^(e_B - 1) (0 for e_B = 0) in both 16-bit halves
     int q_sat;                          // every e_B <= 16 - Q: one-instruction requantization
+    int* sk_cnt;                        // stream-K counters of the tap GEMM that follows, zeroed
+    int sk_ncnt;                        //   by workgroup 0 (MODE 0; none when sk_ncnt is 0)
 };
+
+// zero the stream-K counters of the tap GEMM that reads this Vq (workgroup 0)
+__device__ __forceinline__ void k1_zero_counters(const K1Args& g) {
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < g.sk_ncnt; i += blockDim.x) g.sk_cnt[i] = 0;
+}
 
 // Requantize the tile's taps and store them to the tap planes of Vq at byte
 // offset off (see the kernel); SAT: the one-instruction saturating form.
@@ -223,6 +231,7 @@ __global__ __launch_bounds__(16 * TX, 5) void wino_input_xform(const int8_t* __r
     // then tile row; consecutive logical ids are kept on one XCD (its L2),
     // so the channel groups sharing each 128-byte line of an NHWC pixel and
     // the tile rows sharing halo rows are read by concurrent workgroups.
+    if constexpr (MODE == 0) k1_zero_counters(g);
     int bid = xcd_remap((int)blockIdx.x, (int)gridDim.x);
     const int cgi = bid % g.ncg;
     bid /= g.ncg;
@@ -293,6 +302,7 @@ template <int M, int Q, int TX, bool SAT>
 __global__ __launch_bounds__(16 * TX, 80 / TX) void wino_input_xform_nhwc(const int8_t* __restrict__ x,
                                                                     int8_t* __restrict__ vq, K1Args g) {
     constexpr int N = Wino<M>::N;
+    k1_zero_counters(g);
     // the block order of wino_input_xform
     int bid = xcd_remap((int)blockIdx.x, (int)gridDim.x);
     const int cgi = bid % g.ncg;
@@ -388,6 +398,11 @@ struct K2Args {
     int nbco, nblocks;
     int out_shift, relu;
     int y_staged;              // row-streamed kernel: stage NHWC output through LDS
+    int n_dp;                  // row-streamed kernel: blocks run whole; the rest are split
+    int sk_groups;             // stream-K workgroups sharing the split blocks (0: none)
+    int sk_units;              // stages of the split blocks: their count x 6 cin_pad / 64
+    int* sk_cnt;               // per split block: pieces counted (zero between launches)
+    int* sk_part;              // partial Y, two slots of KR_SLOT int32 per stream-K workgroup
     FastDiv dimg, dtw;         // division by th * tw and by tw (tile coordinates)
     TapTables tab;
     uint32_t shrow[6];         // sh of row a's six taps, 5 bits each (wave-specialized kernel)
@@ -672,31 +687,66 @@ __device__ __forceinline__ void store_tile(const T (&q)[4][16], const G& g, int8
     }
 }
 
-template <int LAYOUT>
-__global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* __restrict__ uq,
-                                                                 const int8_t* __restrict__ vq,
-                                                                 const int32_t* __restrict__ bias,
-                                                                 int8_t* __restrict__ y, K2Args g) {
+// Stream-K over the last, partial round of row-streamed blocks.  A launch runs
+// n_dp blocks whole (logical blocks [0, n_dp)) and sk_groups workgroups that
+// share the stages of the remaining blocks: with U = those blocks x 6 nkc
+// stages in sequence (blocks in logical order, each block's stages in ring
+// order), workgroup g runs stages [g U / G, (g + 1) U / G), so one workgroup
+// may hold the end of one block and the start of the next.  Y is linear in
+// the stages (each stage's M folds into Y through the same row pass and
+// column update), so a block's Y is the sum of its pieces' partial Y; the
+// plan's bound on the sum of the terms' magnitudes also bounds every partial
+// sum, so int32 stays exact.  Each piece checks the block's counter: the piece
+// that finds every other piece counted adds their partial Y to its own and
+// runs the epilogue; any other piece stores its partial Y to its slot in the
+// workspace (2 per workgroup: for the first and the last piece of its range),
+// then counts itself, and the piece whose count completes the block finishes
+// it instead.  No workgroup ever waits for another.  The finisher resets the
+// counter, so counters stay zero between launches (the input transform zeroes
+// them before the first).
+constexpr int KR_SLOT = KR_THREADS * 64;   // int32 of one partial Y (64 per lane)
+static_assert(KR_TB == 1, "a partial Y slot holds one 16x16 block per wave");
+
+// first stage (counted from the first split block) of stream-K workgroup sk;
+// the host keeps sk_units * sk_groups below 2^31
+__device__ __forceinline__ int sk_start(int sk, const K2Args& g) { return sk * g.sk_units / g.sk_groups; }
+
+// the stream-K workgroup whose range holds stage u
+__device__ __forceinline__ int sk_owner(int u, const K2Args& g) {
+    int c = u * g.sk_groups / g.sk_units;
+    while (c + 1 < g.sk_groups && sk_start(c + 1, g) <= u) ++c;
+    while (c > 0 && sk_start(c, g) > u) --c;
+    return c;
+}
+
+// The row-streamed kernel's body; SK: with the stream-K split (the kernel
+// wino_tap_gemm_rows_sk), else every workgroup runs one whole block.
+template <int LAYOUT, bool SK>
+__device__ __forceinline__ void tap_gemm_rows_body(const int8_t* __restrict__ uq, const int8_t* __restrict__ vq,
+                                                   const int32_t* __restrict__ bias, int8_t* __restrict__ y,
+                                                   const K2Args& g) {
     __shared__ __attribute__((aligned(1024))) uint8_t lds[KR_NBUF * KR_STAGE];
     __shared__ __attribute__((aligned(16))) int bias_blk[KR_CO];
-    const int lbid = xcd_remap(blockIdx.x, g.nblocks);
-    const int bco = lbid % g.nbco, btl = lbid / g.nbco;
+    __shared__ int sk_last;
+    // the alignment shifts of the split kernel, read per row fold (from the
+    // kernel arguments the compiler would keep all 36 in scalar registers
+    // across its pieces)
+    __shared__ int sh_tab[SK ? kTaps : 1];
+    if constexpr (SK)
+        if (threadIdx.x < kTaps) sh_tab[threadIdx.x] = g.tab.sh[threadIdx.x];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int cw = wave & 3, tw = wave >> 2;
-    const int co_blk = bco * KR_CO;
-    // the block's bias (padded to the plan's channel count) into LDS before the
-    // ring starts: read from global memory where row 1 uses it, its load would
-    // be waited for with every ring copy issued before it (vmcnt counts in order)
-    if (threadIdx.x < KR_CO) bias_blk[threadIdx.x] = bias[co_blk + threadIdx.x];
-    const long long tl_blk = (long long)btl * KR_TL;
     const int lr = lane & 15, lk = lane >> 4;
     const int nkc = g.cin_pad / kKStep;
     const int nstage = 6 * nkc;
 
-    // copy side: k-blocked operands Uq[36][cin_pad/64][cout_pad][64] and
-    // Vq[36][cin_pad/64][t_pad][64]; this wave's 16 rows, this lane's 16 bytes
-    // of slices b0, b0 + step, ...
+    // stream-K workgroup index (-1: a whole block)
+    const int sk = !SK || (int)blockIdx.x < g.n_dp ? -1 : xcd_remap((int)blockIdx.x - g.n_dp, g.sk_groups);
+
+    // copy side, fixed parts: this wave's 16 rows, this lane's 16 bytes of
+    // slices b0, b0 + step, ... of a stage (k-blocked operands
+    // Uq[36][cin_pad/64][cout_pad][64] and Vq[36][cin_pad/64][t_pad][64])
     constexpr int step = KR_WAVES / 8;
     const int grp = wave & 7, b0 = wave >> 3;
     const bool copies_u = grp < 4;
@@ -704,186 +754,297 @@ __global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* _
     const uint32_t lane_off = (uint32_t)(rr * 64 + 16 * lds_slot(rr, lane & 3));
     const long long tap_stride = copies_u ? (long long)g.cout_pad * g.cin_pad : g.t_pad * g.cin_pad;
     const long long kc_stride = copies_u ? (long long)g.cout_pad * kKStep : g.t_pad * kKStep;
-    const int8_t* const src = (copies_u ? uq + (long long)(co_blk + 16 * grp) * kKStep
-                                        : vq + (tl_blk + 16 * (grp - 4)) * kKStep) +
-                              b0 * tap_stride;
     uint8_t* const dst = lds + 1024 * grp + b0 * KR_CHUNK;
     // The copy source advances by one k-chunk per stage and by a row of taps
     // (minus the chunks walked) at the end of a row: one 64-bit add per stage
     // instead of rebuilding the address from (row, chunk) products, which
     // cost ~50 scalar instructions per stage and wave.
-    const int8_t* next_src = src;
     const long long row_adv = 6 * tap_stride - (long long)(nkc - 1) * kc_stride;
     const long long slice_step = step * tap_stride;
-    int next_kc = 0, next_buf = 0;
-    auto issue_next = [&]() {
-        uint8_t* d = dst + next_buf * KR_STAGE;
-        // plain (temporal) loads for Vq too: the four channel blocks of one
-        // tile block run side by side on one XCD (consecutive logical ids)
-        // and share that L2's copy; measured, a non-temporal hint on Vq made
-        // the later readers go back to memory and cost 8%
-#pragma unroll
-        for (int i = 0; i < KR_LPW; ++i)
-            lds_copy16(next_src + i * slice_step + lane_off,
-                       (__attribute__((address_space(3))) void*)(d + step * i * KR_CHUNK));
-        if (++next_kc == nkc) {
-            next_kc = 0;
-            next_src += row_adv;
-        } else {
-            next_src += kc_stride;
-        }
-        next_buf = next_buf == KR_NBUF - 1 ? 0 : next_buf + 1;
-    };
 
     // compute side: fragment offsets within a slice
     const int row_a = 16 * cw + lr, row_b = KR_CO + 16 * KR_TB * tw + lr;
     const int frag_a = row_a * 64 + 16 * lds_slot(row_a, lk);
     const int frag_b = row_b * 64 + 16 * lds_slot(row_b, lk);   // block tb: + 16 tb rows
-
-    // the lane's four channels; the rounding constant of the final shift
-    const int co0 = co_blk + 16 * cw + 4 * lk;
+    // the rounding constant of the final shift
     const int rnd = g.out_shift > 0 ? 1 << (g.out_shift - 1) : 0;
 
-    // Y of the lane's KR_TB tiles x 4 channels, 4x4 each
-    int yv[KR_TB][4][16];
-#pragma unroll
-    for (int tb = 0; tb < KR_TB; ++tb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-#pragma unroll
-            for (int p = 0; p < 16; ++p) yv[tb][r][p] = 0;
+    // one piece: stages [sb, se) of logical block lbid; at_start: the piece
+    // opens this workgroup's range
+    auto piece = [&](const int lbid, const int sb, const int se, const bool at_start) {
+        const int nst = se - sb;
+        const int bco = lbid % g.nbco, btl = lbid / g.nbco;
+        const int co_blk = bco * KR_CO;
+        const long long tl_blk = (long long)btl * KR_TL;
+        // the block's bias (padded to the plan's channel count) into LDS before
+        // the ring starts: read from global memory where row 1 uses it, its
+        // load would be waited for with every ring copy issued before it
+        // (vmcnt counts in order)
+        if (threadIdx.x < KR_CO) bias_blk[threadIdx.x] = bias[co_blk + threadIdx.x];
+        const int co0 = co_blk + 16 * cw + 4 * lk;   // the lane's four channels
 
-    issue_next();
-    if (nstage > 1) issue_next();
-    int s = 0, buf = 0;
+        const int8_t* next_src = (copies_u ? uq + (long long)(co_blk + 16 * grp) * kKStep
+                                           : vq + (tl_blk + 16 * (grp - 4)) * kKStep) +
+                                 b0 * tap_stride + (long long)(sb / nkc) * 6 * tap_stride +
+                                 (long long)(sb % nkc) * kc_stride;
+        int next_kc = sb % nkc, next_buf = 0;
+        auto issue_next = [&]() {
+            uint8_t* d = dst + next_buf * KR_STAGE;
+            // plain (temporal) loads for Vq too: the four channel blocks of one
+            // tile block run side by side on one XCD (consecutive logical ids)
+            // and share that L2's copy; measured, a non-temporal hint on Vq made
+            // the later readers go back to memory and cost 8%
 #pragma unroll
-    for (int a = 0; a < 6; ++a) {
-        // bias plus rounding constant, injected through tap (1,1): its row
-        // and column of A^T are all ones, so it reaches every output of the
-        // tile once.  Loaded in the row that uses it.
-        v4i bias_rnd = (v4i){0, 0, 0, 0};
-        if (a == 1) bias_rnd = *(const v4i*)(bias_blk + (co0 - co_blk)) + rnd;
-        v4i m[6][KR_TB];
-        // one stage: the six taps of row a, 64 input channels; the first
-        // k-chunk of the row starts the accumulators from zero
-        auto stage = [&](bool first) {
-            // stage s has landed once only the next stage's loads are pending
-            if (s + 1 < nstage)
-                WINO_WAIT_VM_LDS(KR_LPW);
-            else
-                WINO_WAIT_VM_LDS(0);
-            ring_barrier();   // stage s visible; stage s-1 (same buffer as s+2) consumed
-            if (s + 2 < nstage) issue_next();
-            const uint8_t* base = lds + buf * KR_STAGE;
-            buf = buf == KR_NBUF - 1 ? 0 : buf + 1;
-            ++s;
-            // fragments of two taps in flight ahead of the MFMAs
-            v4i fa[2], fb[2][KR_TB];
-            auto frag = [&](int b) {
-                fa[b & 1] = *(const v4i*)(base + b * KR_CHUNK + frag_a);
-#pragma unroll
-                for (int tb = 0; tb < KR_TB; ++tb)
-                    fb[b & 1][tb] = *(const v4i*)(base + b * KR_CHUNK + frag_b + 16 * 64 * tb);
-            };
-            frag(0);
-            frag(1);
-            const v4i zero = (v4i){0, 0, 0, 0};
-#pragma unroll
-            for (int b = 0; b < 6; ++b) {
-#pragma unroll
-                for (int tb = 0; tb < KR_TB; ++tb)
-                    m[b][tb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[b & 1], fb[b & 1][tb], first ? zero : m[b][tb],
-                                                                     0, 0, 0);
-                if (b + 2 < 6) frag(b + 2);
+            for (int i = 0; i < KR_LPW; ++i)
+                lds_copy16(next_src + i * slice_step + lane_off,
+                           (__attribute__((address_space(3))) void*)(d + step * i * KR_CHUNK));
+            if (++next_kc == nkc) {
+                next_kc = 0;
+                next_src += row_adv;
+            } else {
+                next_src += kc_stride;
             }
-            // keep that order (masks: 0x100 LDS read, 0x008 MFMA)
-            __builtin_amdgcn_sched_group_barrier(0x100, 2 * (1 + KR_TB), 0);
-#pragma unroll
-            for (int b = 0; b < 4; ++b) {
-                __builtin_amdgcn_sched_group_barrier(0x008, KR_TB, 0);
-                __builtin_amdgcn_sched_group_barrier(0x100, 1 + KR_TB, 0);
-            }
-            __builtin_amdgcn_sched_group_barrier(0x008, 2 * KR_TB, 0);
+            next_buf = next_buf == KR_NBUF - 1 ? 0 : next_buf + 1;
         };
-        stage(true);
-        for (int kc = 1; kc < nkc; ++kc) stage(false);
 
-        // fold row a: z = (M'[a, :]) A, then Y += A^T[:, a] z
-#pragma unroll
-        for (int tb = 0; tb < KR_TB; ++tb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            int mv[6], z[4];
-#pragma unroll
-            for (int b = 0; b < 6; ++b) mv[b] = m[b][tb][r] << g.tab.sh[6 * a + b];
-            if (a == 1) mv[1] += bias_rnd[r];
-            at_1d(mv, z);
-            int* yr = yv[tb][r];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                // column a of A^T: 1 1 1 1 1 0 / 0 1 -1 2 -2 0 / 0 1 1 4 4 0 / 0 1 -1 8 -8 1
-                if (a < 5) yr[j] += z[j];
-                if (a == 1) { yr[4 + j] += z[j]; yr[8 + j] += z[j]; yr[12 + j] += z[j]; }
-                if (a == 2) { yr[4 + j] -= z[j]; yr[8 + j] += z[j]; yr[12 + j] -= z[j]; }
-                if (a == 3) { yr[4 + j] += z[j] << 1; yr[8 + j] += z[j] << 2; yr[12 + j] += z[j] << 3; }
-                if (a == 4) { yr[4 + j] -= z[j] << 1; yr[8 + j] += z[j] << 2; yr[12 + j] -= z[j] << 3; }
-                if (a == 5) yr[12 + j] += z[j];
-            }
-        }
-        // materialize Y here: Y is only read at the very end, and the
-        // compiler would otherwise sink the folds past the later rows and keep
-        // every row's accumulators live at once
+        // Y of the lane's KR_TB tiles x 4 channels, 4x4 each
+        int yv[KR_TB][4][16];
 #pragma unroll
         for (int tb = 0; tb < KR_TB; ++tb)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
 #pragma unroll
-                for (int p = 0; p < 16; ++p) asm volatile("" : "+v"(yv[tb][r][p]));
-    }
+                for (int p = 0; p < 16; ++p) yv[tb][r][p] = 0;
 
-    if (LAYOUT == WINO_NHWC && g.y_staged) {
-        // NHWC with whole 64-channel blocks: gather the block's output in
-        // LDS (the ring is idle now) so every pixel's 64 channel bytes leave
-        // as four 16-byte stores of adjacent lanes -- 64-byte write requests
-        // instead of 16-byte pieces scattered over 16 lines per instruction
-        constexpr int PITCH = 16 * 64 + 16;   // bytes per tile; the pad spreads lanes over banks
-        static_assert(KR_TL * PITCH <= KR_NBUF * KR_STAGE, "output staging fits the ring");
-        const int s = g.out_shift, lo = g.relu ? 0 : -128;
-        __syncthreads();                      // every wave is done reading the ring
+        issue_next();
+        if (nst > 1) issue_next();
+        int s = 0, buf = 0;
 #pragma unroll
-        for (int tb = 0; tb < KR_TB; ++tb) {
-            uint8_t* ot = lds + (16 * (KR_TB * tw + tb) + lr) * PITCH + 16 * cw + 4 * lk;
+        for (int a = 0; a < 6; ++a) {
+            // the piece's k-chunks of row a
+            const int klo = sb > a * nkc ? sb - a * nkc : 0;
+            const int khi = se < (a + 1) * nkc ? se - a * nkc : nkc;
+            if (klo >= khi) continue;
+            v4i m[6][KR_TB];
+            // one stage: the six taps of row a, 64 input channels; the first
+            // k-chunk of the row starts the accumulators from zero
+            auto stage = [&](bool first) {
+                // stage s has landed once only the next stage's loads are pending
+                if (s + 1 < nst)
+                    WINO_WAIT_VM_LDS(KR_LPW);
+                else
+                    WINO_WAIT_VM_LDS(0);
+                ring_barrier();   // stage s visible; stage s-1 (same buffer as s+2) consumed
+                if (s + 2 < nst) issue_next();
+                const uint8_t* base = lds + buf * KR_STAGE;
+                buf = buf == KR_NBUF - 1 ? 0 : buf + 1;
+                ++s;
+                // fragments of two taps in flight ahead of the MFMAs
+                v4i fa[2], fb[2][KR_TB];
+                auto frag = [&](int b) {
+                    fa[b & 1] = *(const v4i*)(base + b * KR_CHUNK + frag_a);
 #pragma unroll
-            for (int p = 0; p < 16; ++p) {
-                uint32_t pk = put_byte<0>(0u, (uint32_t)med3_i32(yv[tb][0][p] >> s, lo, 127));
-                pk = put_byte<1>(pk, (uint32_t)med3_i32(yv[tb][1][p] >> s, lo, 127));
-                pk = put_byte<2>(pk, (uint32_t)med3_i32(yv[tb][2][p] >> s, lo, 127));
-                pk = put_byte<3>(pk, (uint32_t)med3_i32(yv[tb][3][p] >> s, lo, 127));
-                *(uint32_t*)(ot + 64 * p) = pk;
-            }
+                    for (int tb = 0; tb < KR_TB; ++tb)
+                        fb[b & 1][tb] = *(const v4i*)(base + b * KR_CHUNK + frag_b + 16 * 64 * tb);
+                };
+                frag(0);
+                frag(1);
+                const v4i zero = (v4i){0, 0, 0, 0};
+#pragma unroll
+                for (int b = 0; b < 6; ++b) {
+#pragma unroll
+                    for (int tb = 0; tb < KR_TB; ++tb)
+                        m[b][tb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(fa[b & 1], fb[b & 1][tb],
+                                                                         first ? zero : m[b][tb], 0, 0, 0);
+                    if (b + 2 < 6) frag(b + 2);
+                }
+                // keep that order (masks: 0x100 LDS read, 0x008 MFMA)
+                __builtin_amdgcn_sched_group_barrier(0x100, 2 * (1 + KR_TB), 0);
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, KR_TB, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1 + KR_TB, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, 2 * KR_TB, 0);
+            };
+            stage(true);
+            for (int kc = klo + 1; kc < khi; ++kc) stage(false);
+
+            // bias plus rounding constant, injected through tap (1,1): its row
+            // and column of A^T are all ones, so it reaches every output of
+            // the tile once.  Taken by the piece holding row 1's first chunk,
+            // and read only here, after the stages' barriers: wave 0 wrote
+            // bias_blk at the start of the piece, and a piece that starts at
+            // row 1 has no barrier before its first stage.
+            v4i bias_rnd = (v4i){0, 0, 0, 0};
+            if (a == 1 && klo == 0) bias_rnd = *(const v4i*)(bias_blk + (co0 - co_blk)) + rnd;
+
+            // fold row a: z = (M'[a, :]) A, then Y += A^T[:, a] z
+#pragma unroll
+            for (int tb = 0; tb < KR_TB; ++tb)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    int mv[6], z[4];
+#pragma unroll
+                    for (int b = 0; b < 6; ++b) mv[b] = m[b][tb][r] << (SK ? sh_tab[6 * a + b] : g.tab.sh[6 * a + b]);
+                    if (a == 1) mv[1] += bias_rnd[r];
+                    at_1d(mv, z);
+                    int* yr = yv[tb][r];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        // column a of A^T: 1 1 1 1 1 0 / 0 1 -1 2 -2 0 / 0 1 1 4 4 0 / 0 1 -1 8 -8 1
+                        if (a < 5) yr[j] += z[j];
+                        if (a == 1) { yr[4 + j] += z[j]; yr[8 + j] += z[j]; yr[12 + j] += z[j]; }
+                        if (a == 2) { yr[4 + j] -= z[j]; yr[8 + j] += z[j]; yr[12 + j] -= z[j]; }
+                        if (a == 3) { yr[4 + j] += z[j] << 1; yr[8 + j] += z[j] << 2; yr[12 + j] += z[j] << 3; }
+                        if (a == 4) { yr[4 + j] -= z[j] << 1; yr[8 + j] += z[j] << 2; yr[12 + j] -= z[j] << 3; }
+                        if (a == 5) yr[12 + j] += z[j];
+                    }
+                }
+            // materialize Y here: Y is only read at the very end, and the
+            // compiler would otherwise sink the folds past the later rows and
+            // keep every row's accumulators live at once
+#pragma unroll
+            for (int tb = 0; tb < KR_TB; ++tb)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+#pragma unroll
+                    for (int p = 0; p < 16; ++p) asm volatile("" : "+v"(yv[tb][r][p]));
         }
-        __syncthreads();
-        // wave w copies tiles w, w + 16, ...: lane = 16-byte quarter q of pixel p
-        const int p = lane >> 2, q = lane & 3;
-        for (int tl = wave; tl < KR_TL; tl += KR_WAVES) {
-            const long long tile = tl_blk + tl;   // wave-uniform
-            if (tile >= g.ntiles) break;
-            int img, ty, tx;
-            tile_coords(tile, g, img, ty, tx);
-            const int yy = 4 * ty + (p >> 2), xx = 4 * tx + (p & 3);
-            if (yy < g.h && xx < g.w) {
-                // non-temporal: the output is not read again here, and in
-                // L2 it would evict the operands the next round of blocks
-                // reads (measured 2-3% of the kernel at C5 and C4)
-                __builtin_nontemporal_store(*(const v4i*)(lds + tl * PITCH + 64 * p + 16 * q),
-                                            (v4i*)(y + (((long long)img * g.h + yy) * g.w + xx) * g.cout + co_blk +
-                                                   16 * q));
+
+        if (SK && (sb != 0 || se != nstage)) {
+            // a piece of a split block: finish the block or leave a partial Y
+            const int jb = (lbid - g.n_dp) * nstage;   // its first stage in the split sequence
+            const int glo = sk_owner(jb, g), ghi = sk_owner(jb + nstage - 1, g);
+            const int others = ghi - glo;
+            int* const cnt = g.sk_cnt + (lbid - g.n_dp);
+            if (threadIdx.x == 0) {
+                const int c = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (c == others) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+                sk_last = c == others;
             }
+            __syncthreads();
+            bool last = sk_last;
+            if (!last) {
+                int* const slot = g.sk_part + (size_t)(2 * sk + (at_start ? 0 : 1)) * KR_SLOT;
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    *(v4i*)(slot + 4 * (i * KR_THREADS + (int)threadIdx.x)) =
+                        (v4i){yv[0][i >> 2][4 * (i & 3)], yv[0][i >> 2][4 * (i & 3) + 1],
+                              yv[0][i >> 2][4 * (i & 3) + 2], yv[0][i >> 2][4 * (i & 3) + 3]};
+                WINO_WAIT_VM(0);   // this wave's stores have reached L2
+                __syncthreads();
+                if (threadIdx.x == 0) {
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                    const int c = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (c == others) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+                    sk_last = c == others;
+                }
+                __syncthreads();
+                last = sk_last;
+            }
+            if (!last) return;
+            // the other pieces' partial Y: slot 0 of a workgroup whose range
+            // starts inside this block, slot 1 of the one that enters it
+            for (int c = glo; c <= ghi; ++c) {
+                if (c == sk) continue;
+                const int* const slot = g.sk_part + (size_t)(2 * c + (sk_start(c, g) >= jb ? 0 : 1)) * KR_SLOT;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const v4i v = *(const v4i*)(slot + 4 * (i * KR_THREADS + (int)threadIdx.x));
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) yv[0][i >> 2][4 * (i & 3) + e] += v[e];
+                }
+            }
+            if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
+
+        if (LAYOUT == WINO_NHWC && g.y_staged) {
+            // NHWC with whole 64-channel blocks: gather the block's output in
+            // LDS (the ring is idle now) so every pixel's 64 channel bytes leave
+            // as four 16-byte stores of adjacent lanes -- 64-byte write requests
+            // instead of 16-byte pieces scattered over 16 lines per instruction
+            constexpr int PITCH = 16 * 64 + 16;   // bytes per tile; the pad spreads lanes over banks
+            static_assert(KR_TL * PITCH <= KR_NBUF * KR_STAGE, "output staging fits the ring");
+            const int sft = g.out_shift, lo = g.relu ? 0 : -128;
+            __syncthreads();                      // every wave is done reading the ring
+#pragma unroll
+            for (int tb = 0; tb < KR_TB; ++tb) {
+                uint8_t* ot = lds + (16 * (KR_TB * tw + tb) + lr) * PITCH + 16 * cw + 4 * lk;
+#pragma unroll
+                for (int p = 0; p < 16; ++p) {
+                    uint32_t pk = put_byte<0>(0u, (uint32_t)med3_i32(yv[tb][0][p] >> sft, lo, 127));
+                    pk = put_byte<1>(pk, (uint32_t)med3_i32(yv[tb][1][p] >> sft, lo, 127));
+                    pk = put_byte<2>(pk, (uint32_t)med3_i32(yv[tb][2][p] >> sft, lo, 127));
+                    pk = put_byte<3>(pk, (uint32_t)med3_i32(yv[tb][3][p] >> sft, lo, 127));
+                    *(uint32_t*)(ot + 64 * p) = pk;
+                }
+            }
+            __syncthreads();
+            // wave w copies tiles w, w + 16, ...: lane = 16-byte quarter q of pixel p
+            const int p = lane >> 2, q = lane & 3;
+            for (int tl = wave; tl < KR_TL; tl += KR_WAVES) {
+                const long long tile = tl_blk + tl;   // wave-uniform
+                if (tile >= g.ntiles) break;
+                int img, ty, tx;
+                tile_coords(tile, g, img, ty, tx);
+                const int yy = 4 * ty + (p >> 2), xx = 4 * tx + (p & 3);
+                if (yy < g.h && xx < g.w) {
+                    // non-temporal: the output is not read again here, and in
+                    // L2 it would evict the operands the next round of blocks
+                    // reads (measured 2-3% of the kernel at C5 and C4)
+                    __builtin_nontemporal_store(*(const v4i*)(lds + tl * PITCH + 64 * p + 16 * q),
+                                                (v4i*)(y + (((long long)img * g.h + yy) * g.w + xx) * g.cout +
+                                                       co_blk + 16 * q));
+                }
+            }
+        } else {
+#pragma unroll
+            for (int tb = 0; tb < KR_TB; ++tb)
+                store_tile<LAYOUT>(yv[tb], g, y, co0, tl_blk + 16 * (KR_TB * tw + tb) + lr);
+        }
+    };
+
+    // Whole blocks and the (at most two) pieces of a stream-K range each take
+    // a copy of the piece code: as a loop over pieces, the compiler kept the
+    // loop-invariant scalars of the whole body live across it and spilled.
+    if (!SK || sk < 0) {
+        piece(xcd_remap(blockIdx.x, g.n_dp), 0, nstage, true);
         return;
     }
-#pragma unroll
-    for (int tb = 0; tb < KR_TB; ++tb) store_tile<LAYOUT>(yv[tb], g, y, co0, tl_blk + 16 * (KR_TB * tw + tb) + lr);
+    // this workgroup's stages [u0, u1) of the split sequence (stage s of split
+    // block j is j * nstage + s); the host keeps u1 - u0 <= nstage, so the
+    // range ends in the block it starts in or in the next one
+    const int u0 = sk_start(sk, g), u1 = sk_start(sk + 1, g);
+    const int j = u0 / nstage;
+    const int sb = u0 - j * nstage;
+    const int se = u1 - u0 < nstage - sb ? sb + (u1 - u0) : nstage;
+    piece(g.n_dp + j, sb, se, true);
+    if (u0 + (se - sb) < u1) {
+        // The ring's vmcnt waits count its own copies and assume they complete
+        // in issue order; stores still in flight from the first piece's
+        // epilogue may complete after later loads, so they are waited for
+        // first.  Then every wave is done with the first piece's LDS.
+        WINO_WAIT_VM(0);
+        __syncthreads();
+        piece(g.n_dp + j + 1, 0, u1 - u0 - (se - sb), false);
+    }
+}
+
+template <int LAYOUT>
+__global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows(const int8_t* __restrict__ uq,
+                                                                 const int8_t* __restrict__ vq,
+                                                                 const int32_t* __restrict__ bias,
+                                                                 int8_t* __restrict__ y, K2Args g) {
+    tap_gemm_rows_body<LAYOUT, false>(uq, vq, bias, y, g);
+}
+
+template <int LAYOUT>
+__global__ __launch_bounds__(KR_THREADS) void wino_tap_gemm_rows_sk(const int8_t* __restrict__ uq,
+                                                                    const int8_t* __restrict__ vq,
+                                                                    const int32_t* __restrict__ bias,
+                                                                    int8_t* __restrict__ y, K2Args g) {
+    tap_gemm_rows_body<LAYOUT, true>(uq, vq, bias, y, g);
 }
 
 #include "wino_tap_ws.h"
@@ -1139,6 +1300,8 @@ K1Args k1_args(const Geometry& g, int cin, int cin_pad, const TapTables& tab, in
     a.vq_buf = a.plane_bytes < 0x7fffffffLL;
     a.x_vec = 0;
     a.x_dw = 0;
+    a.sk_cnt = nullptr;
+    a.sk_ncnt = 0;
     return a;
 }
 
@@ -1235,7 +1398,8 @@ int tap_kernel_for(const wino_f4_plan_s* p, const Geometry& g, int mode) {
         return sh5 ? WINO_TAP_WAVES : WINO_TAP_ROWS;
     }
     if (p->epi_bits == 32 && k != WINO_TAP_RESIDENT &&
-        (k == WINO_TAP_ROWS || (long long)(p->cout_pad / KR_CO) * (g.t_pad / KR_TL) >= num_cus()))
+        (k == WINO_TAP_ROWS || k == WINO_TAP_ROWS_STREAMK ||
+         (long long)(p->cout_pad / KR_CO) * (g.t_pad / KR_TL) >= num_cus()))
         return WINO_TAP_ROWS;
     return WINO_TAP_RESIDENT_64X32;
 }
@@ -1247,6 +1411,47 @@ int ws_chunks_per_stage(int cin_pad) {
     for (int nk = 4; nk > 1; --nk)
         if (nkc % nk == 0) return nk;
     return 1;
+}
+
+// Stream-K split of the row-streamed tap GEMM's last round (the workspace
+// past Vq holds its counters and partial sums), forced only
+// (WINO_TAP_ROWS_STREAMK): it splits whenever a partial round exists (also
+// below one round), spreading the stages as thinly as one per workgroup.
+// Measured at C5 (400 blocks: one whole round, 144 blocks split over 256
+// workgroups), K2 takes 80 us against 52 us unsplit: the split round alone
+// takes 57 us, 30 us of it without the partial-sum exchange (each workgroup
+// runs two pieces and pays a block's fixed costs -- ring start, row folds,
+// epilogue -- for each) and the rest in the exchange (61 MB of partial sums
+// written and read back, and the agent-scope fences).
+struct SkPlan {
+    int n_dp = 0, groups = 0, nsplit = 0, units = 0;
+    size_t cnt_off = 0, part_off = 0, end = 0;   // byte offsets in the workspace
+};
+
+bool sk_plan_for(const wino_f4_plan_s* p, const Geometry& g, SkPlan& sk) {
+    if (p->bits != 8 || p->m != 4 || g.ntiles == 0 || tap_kernel_for(p, g, 0) != WINO_TAP_ROWS) return false;
+    const long long nblocks = (long long)(p->cout_pad / KR_CO) * (g.t_pad / KR_TL);
+    const long long ncu = num_cus();
+    const long long rem = nblocks % ncu;
+    if (rem == 0 || p->tap_kernel != WINO_TAP_ROWS_STREAMK) return false;
+    const long long nstage = 6 * (p->cin_pad / kKStep);
+    const long long units = rem * nstage, groups = std::min<long long>(ncu, units);
+    // 32-bit stage arithmetic in the kernel; every range within two blocks
+    if (units * groups >= (1ll << 31) || (units + groups - 1) / groups > nstage) return false;
+    sk.n_dp = (int)(nblocks - rem);
+    sk.nsplit = (int)rem;
+    sk.units = (int)units;
+    sk.groups = (int)groups;
+    sk.cnt_off = (size_t)round_up((long long)vq_bytes(p, g), 256);
+    sk.part_off = sk.cnt_off + (size_t)round_up(rem * 4, 256);
+    sk.end = sk.part_off + (size_t)2 * sk.groups * KR_SLOT * sizeof(int32_t);
+    return true;
+}
+
+// The split applies when the plan and shape call for it and the caller's
+// workspace holds it.
+bool sk_in_workspace(const wino_f4_plan_s* p, const Geometry& g, size_t ws_bytes, SkPlan& sk) {
+    return sk_plan_for(p, g, sk) && ws_bytes >= sk.end;
 }
 
 template <class C, int M, int MODE, int Q = 8>
@@ -1291,9 +1496,10 @@ wino_status launch_rows_wide(const wino_f4_plan_s* p, const Geometry& g, wino_la
     return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
 }
 
+// ws_bytes: the workspace at vq (the stream-K split uses the part past Vq)
 template <int MODE>
 wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout layout, const int8_t* vq,
-                      int8_t* y, void* aux, hipStream_t stream) {
+                      int8_t* y, void* aux, hipStream_t stream, size_t ws_bytes = 0) {
     if (g.ntiles == 0) return WINO_OK;
     K2Args a;
     a.cin_pad = p->cin_pad;
@@ -1309,6 +1515,11 @@ wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout la
     a.out_shift = p->out_shift;
     a.relu = p->relu;
     a.y_staged = layout == WINO_NHWC && p->cout % KR_CO == 0 && ((uintptr_t)y & 15) == 0;
+    a.n_dp = 0;
+    a.sk_groups = 0;
+    a.sk_units = 0;
+    a.sk_cnt = nullptr;
+    a.sk_part = nullptr;
     a.dimg = make_fastdiv((uint32_t)(g.th * g.tw));
     a.dtw = make_fastdiv((uint32_t)g.tw);
     a.tab = tables_of(p);
@@ -1340,12 +1551,31 @@ wino_status launch_k2(const wino_f4_plan_s* p, const Geometry& g, wino_layout la
             if (rblocks > 0x7fffffffll) return WINO_EUNSUPPORTED;
             a.nbco = p->cout_pad / KR_CO;
             a.nblocks = (int)rblocks;
-            if (layout == WINO_NHWC)
-                hipLaunchKernelGGL(wino_tap_gemm_rows<WINO_NHWC>, dim3((unsigned)rblocks), dim3(KR_THREADS), 0,
-                                   stream, p->uq_dev, vq, p->bias_dev, y, a);
-            else
-                hipLaunchKernelGGL(wino_tap_gemm_rows<WINO_NCHW>, dim3((unsigned)rblocks), dim3(KR_THREADS), 0,
-                                   stream, p->uq_dev, vq, p->bias_dev, y, a);
+            a.n_dp = (int)rblocks;
+            SkPlan sk;
+            if (MODE == 0 && sk_in_workspace(p, g, ws_bytes, sk)) {
+                uint8_t* const ws = (uint8_t*)const_cast<int8_t*>(vq);
+                a.n_dp = sk.n_dp;
+                a.sk_groups = sk.groups;
+                a.sk_units = sk.units;
+                a.sk_cnt = (int*)(ws + sk.cnt_off);
+                a.sk_part = (int*)(ws + sk.part_off);
+            }
+            const unsigned grid = (unsigned)(a.n_dp + a.sk_groups);
+            if (a.sk_groups > 0) {
+                if (layout == WINO_NHWC)
+                    hipLaunchKernelGGL(wino_tap_gemm_rows_sk<WINO_NHWC>, dim3(grid), dim3(KR_THREADS), 0, stream,
+                                       p->uq_dev, vq, p->bias_dev, y, a);
+                else
+                    hipLaunchKernelGGL(wino_tap_gemm_rows_sk<WINO_NCHW>, dim3(grid), dim3(KR_THREADS), 0, stream,
+                                       p->uq_dev, vq, p->bias_dev, y, a);
+            } else if (layout == WINO_NHWC) {
+                hipLaunchKernelGGL(wino_tap_gemm_rows<WINO_NHWC>, dim3(grid), dim3(KR_THREADS), 0, stream, p->uq_dev,
+                                   vq, p->bias_dev, y, a);
+            } else {
+                hipLaunchKernelGGL(wino_tap_gemm_rows<WINO_NCHW>, dim3(grid), dim3(KR_THREADS), 0, stream, p->uq_dev,
+                                   vq, p->bias_dev, y, a);
+            }
             return hipGetLastError() == hipSuccess ? WINO_OK : WINO_EHIP;
         }
         case WINO_TAP_WAVES: {
@@ -1427,8 +1657,23 @@ extern "C" size_t wino_f4_workspace_bytes(wino_f4_plan_t p, int32_t n, int32_t h
     Geometry g;
     if (!p || geometry(n, h, w, p->m, g) != WINO_OK) return 0;
     if (variant == WINO_FUSED) return 0;
-    return vq_bytes(p, g);
+    SkPlan sk;
+    return sk_plan_for(p, g, sk) ? sk.end : vq_bytes(p, g);
 }
+
+namespace {
+// K1 arguments of a SPLIT launch; with a stream-K tap GEMM to follow, K1
+// also zeroes its counters
+K1Args split_k1_args(const wino_f4_plan_s* p, const Geometry& g, void* ws, size_t ws_bytes) {
+    K1Args a = k1_args(g, p->cin, p->cin_pad, tables_of(p), p->bits);
+    SkPlan sk;
+    if (sk_in_workspace(p, g, ws_bytes, sk)) {
+        a.sk_cnt = (int*)((uint8_t*)ws + sk.cnt_off);
+        a.sk_ncnt = sk.nsplit;
+    }
+    return a;
+}
+}  // namespace
 
 // FUSED is served by the kernel in wino_fused.hip.
 wino_status wino_f4_conv_fused(const wino_f4_plan_s* p, const int8_t* x, int8_t* y, int n, int h, int w,
@@ -1460,6 +1705,8 @@ extern "C" wino_status wino_f4_tap_kernel_choice(wino_f4_plan_t p, int32_t n, in
     const wino_status st = geometry(n, h, w, p->m, g);
     if (st != WINO_OK) return st;
     *kind = tap_kernel_for(p, g, 0);
+    SkPlan sk;
+    if (*kind == WINO_TAP_ROWS && sk_plan_for(p, g, sk)) *kind = WINO_TAP_ROWS_STREAMK;
     return WINO_OK;
 }
 
@@ -1478,9 +1725,9 @@ extern "C" wino_status wino_f4_conv_int8(wino_f4_plan_t p, const int8_t* x, int8
     }
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
     int8_t* vq = (int8_t*)ws;
-    st = run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p), p->bits), layout, x, vq, nullptr, stream);
+    st = run_k1<0>(p->m, p->bits, split_k1_args(p, g, ws, ws_bytes), layout, x, vq, nullptr, stream);
     if (st != WINO_OK) return st;
-    return launch_k2<0>(p, g, layout, vq, y, nullptr, stream);
+    return launch_k2<0>(p, g, layout, vq, y, nullptr, stream, ws_bytes);
 }
 
 // ---------------------------------------------------------------------------
@@ -1541,10 +1788,10 @@ extern "C" wino_status wino_f4_input_transform(wino_f4_plan_t p, const int8_t* x
     if (st != WINO_OK) return st;
     if (g.ntiles == 0) return WINO_OK;
     if (!ws || ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
-    return run_k1<0>(p->m, p->bits, k1_args(g, p->cin, p->cin_pad, tables_of(p), p->bits), layout, x, (int8_t*)ws, nullptr, stream);
+    return run_k1<0>(p->m, p->bits, split_k1_args(p, g, ws, ws_bytes), layout, x, (int8_t*)ws, nullptr, stream);
 }
 
-extern "C" wino_status wino_f4_tap_gemm(wino_f4_plan_t p, const void* ws, size_t ws_bytes, int8_t* y, int32_t n,
+extern "C" wino_status wino_f4_tap_gemm(wino_f4_plan_t p, void* ws, size_t ws_bytes, int8_t* y, int32_t n,
                                         int32_t h, int32_t w, wino_layout layout, hipStream_t stream) {
     Geometry g;
     wino_status st = check_common(p, ws, n, h, w, layout, g);
@@ -1552,7 +1799,7 @@ extern "C" wino_status wino_f4_tap_gemm(wino_f4_plan_t p, const void* ws, size_t
     if (!y) return WINO_EINVAL;
     if (g.ntiles == 0) return WINO_OK;
     if (ws_bytes < vq_bytes(p, g)) return WINO_EWORKSPACE;
-    return launch_k2<0>(p, g, layout, (const int8_t*)ws, y, nullptr, stream);
+    return launch_k2<0>(p, g, layout, (const int8_t*)ws, y, nullptr, stream, ws_bytes);
 }
 
 // per-tap max |V| over the input and the exponents e_B = max(0, cexp(.)) for

@@ -53,7 +53,8 @@ def _run_layer(x, f, b, spec, rec, layout, variant=W.SPLIT, tap_kernel=W.TAP_AUT
 RUNS = [(W.NHWC, W.SPLIT, W.TAP_AUTO), (W.NCHW, W.SPLIT, W.TAP_AUTO), (W.NHWC, W.FUSED, W.TAP_AUTO),
         (W.NCHW, W.FUSED, W.TAP_AUTO), (W.NHWC, W.SPLIT, W.TAP_RESIDENT_64X32), (W.NCHW, W.SPLIT, W.TAP_ROWS),
         (W.NHWC, W.SPLIT, W.TAP_ROWS), (W.NCHW, W.SPLIT, W.TAP_WAVES), (W.NHWC, W.SPLIT, W.TAP_WAVES),
-        (W.NHWC, W.SPLIT, W.TAP_RESIDENT_32X32)]
+        (W.NHWC, W.SPLIT, W.TAP_RESIDENT_32X32), (W.NHWC, W.SPLIT, W.TAP_ROWS_STREAMK),
+        (W.NCHW, W.SPLIT, W.TAP_ROWS_STREAMK)]
 
 
 @pytest.mark.parametrize("layout,variant,tap_kernel", RUNS)
